@@ -1,0 +1,433 @@
+// EWSJF scheduler core -- CPU oracle.
+//
+// TEST INFRASTRUCTURE ONLY.  This file is the plain, slow, single-threaded
+// definition that the HIP library is checked against.  Only the tests, the
+// smoke check and the benchmark's CPU-baseline leg may load it; the product
+// path never calls it.  It shares no code, header, table or helper with the
+// HIP library.
+//
+// Every floating-point step is IEEE-754 binary64 in the order written here
+// (built with -ffp-contract=off so no multiply-add is fused).
+//
+// What it computes (EWSJF, arXiv 2601.21758):
+//   * Refine-and-Prune partitioning of an observation window of prompt
+//     lengths into contiguous queue intervals (Section 4.2, Stages 1-3,
+//     Eq. 2 and Eq. 3).
+//   * Dynamic Queue Routing of each request to the one interval containing
+//     its prompt length (Section 3.3 "Dispatcher"; Section 5 "Stability and
+//     Correctness").
+//   * Density-Weighted Scoring Phi(r, q) (Eq. 1 / Eq. 4) with the affine
+//     context-aware weights of the meta-policy (Section 4.1, Section 4.4.1).
+//   * Top-B admission ordered by (score desc, request id asc).
+//
+// Readings of passages the paper leaves open are listed next to the code
+// that adopts them.
+#include <algorithm>
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <limits>
+#include <utility>
+#include <vector>
+
+namespace {
+
+constexpr int kOk = 0;
+constexpr int kErrArg = -2;
+
+// ---------------------------------------------------------------------------
+// Window: clamp to [1, L], sort, and list the distinct values with their
+// multiplicities.  The paper's D is the sorted set of window prompt lengths
+// (Section 4.2, "Formalism").
+// ---------------------------------------------------------------------------
+struct Distinct {
+  std::vector<int32_t> v;  // strictly increasing
+  std::vector<int64_t> c;  // multiplicity of v[j]
+};
+
+Distinct sorted_distinct(const int32_t* w, int64_t n, int32_t max_len) {
+  std::vector<int32_t> d(w, w + n);
+  for (auto& x : d) x = std::min(std::max(x, 1), max_len);
+  std::sort(d.begin(), d.end());
+  Distinct out;
+  for (int64_t i = 0; i < n; ++i) {
+    if (out.v.empty() || out.v.back() != d[i]) {
+      out.v.push_back(d[i]);
+      out.c.push_back(1);
+    } else {
+      out.c.back() += 1;
+    }
+  }
+  return out;
+}
+
+// ---------------------------------------------------------------------------
+// Stage 1: coarse partitioning (Section 4.2, "Stage 1").  Returns cluster
+// start indices into the distinct-value list; cluster i is
+// [start[i], start[i+1]).
+//
+// EQUAL_WIDTH(K): the workloads start from K equal-width queues over the
+//   window's [min, max]; value v goes to bin floor((v - lo) * K / (hi-lo+1)),
+//   non-empty bins in order.
+// KMEANS3: the paper's k-means with k = 3, taken as the exact 1-D optimum
+//   (minimum within-cluster sum of squares over the multiset).  In one
+//   dimension optimal clusters are contiguous runs of the sorted values, so
+//   every split (i, j) is tried; F = S1^2/N1 + S2^2/N2 + S3^2/N3 is maximal
+//   exactly where the sum of squares is minimal.  Ties keep the
+//   lexicographically smallest (i, j).
+// ---------------------------------------------------------------------------
+std::vector<int32_t> stage1_equal_width(const Distinct& d, int32_t K) {
+  const int32_t V = (int32_t)d.v.size();
+  std::vector<int32_t> starts;
+  const int64_t lo = d.v[0], hi = d.v[V - 1];
+  const int64_t width = hi - lo + 1;
+  int64_t prev_bin = -1;
+  for (int32_t j = 0; j < V; ++j) {
+    const int64_t bin = ((int64_t)d.v[j] - lo) * (int64_t)K / width;
+    if (j == 0 || bin != prev_bin) starts.push_back(j);
+    prev_bin = bin;
+  }
+  return starts;
+}
+
+std::vector<int32_t> stage1_kmeans3(const Distinct& d) {
+  const int32_t V = (int32_t)d.v.size();
+  std::vector<int32_t> starts;
+  if (V <= 3) {
+    for (int32_t j = 0; j < V; ++j) starts.push_back(j);
+    return starts;
+  }
+  // Exact integer prefix sums of counts and of count * value.
+  std::vector<int64_t> N(V + 1, 0), S(V + 1, 0);
+  for (int32_t j = 0; j < V; ++j) {
+    N[j + 1] = N[j] + d.c[j];
+    S[j + 1] = S[j] + d.c[j] * (int64_t)d.v[j];
+  }
+  double best = -1.0;
+  int32_t bi = 1, bj = 2;
+  for (int32_t i = 1; i <= V - 2; ++i) {
+    for (int32_t j = i + 1; j <= V - 1; ++j) {
+      const double n1 = (double)N[i], s1 = (double)S[i];
+      const double n2 = (double)(N[j] - N[i]), s2 = (double)(S[j] - S[i]);
+      const double n3 = (double)(N[V] - N[j]), s3 = (double)(S[V] - S[j]);
+      const double F = ((s1 * s1) / n1 + (s2 * s2) / n2) + (s3 * s3) / n3;
+      if (F > best) {
+        best = F;
+        bi = i;
+        bj = j;
+      }
+    }
+  }
+  starts.push_back(0);
+  starts.push_back(bi);
+  starts.push_back(bj);
+  return starts;
+}
+
+// ---------------------------------------------------------------------------
+// Stage 2: recursive refinement (Section 4.2, "Stage 2", Eq. 2).
+//
+// A cluster is the distinct-value range [s, e).  G is the set of gaps
+// between consecutive members; a gap is significant when it exceeds
+// alpha * mean(G).
+//   gap_mode 0 (default): G is taken over distinct values, so
+//     mean(G) = span / (V_C - 1)  (the gaps telescope to the span);
+//     the test is gap * (V_C - 1) > alpha * span.
+//   gap_mode 1: G is taken over the multiset, zero gaps between duplicates
+//     included, so mean(G) = span / (n_C - 1); test gap * (n_C-1) > alpha*span.
+// The cluster is cut at every significant gap at once and each piece is
+// refined again.  Recursion stops when no gap is significant, or when the
+// value span (the cluster's width) is below min_width, or when the cluster
+// has too few distinct values to hold a significant gap.
+// ---------------------------------------------------------------------------
+std::vector<int32_t> stage2(const Distinct& d, const std::vector<int32_t>& coarse_starts,
+                            double alpha, int32_t min_width, int32_t gap_mode) {
+  const int32_t V = (int32_t)d.v.size();
+  std::vector<std::pair<int32_t, int32_t>> work, leaves;
+  for (size_t i = 0; i < coarse_starts.size(); ++i) {
+    const int32_t s = coarse_starts[i];
+    const int32_t e = (i + 1 < coarse_starts.size()) ? coarse_starts[i + 1] : V;
+    work.push_back({s, e});
+  }
+  const int32_t min_distinct = (gap_mode == 0) ? 3 : 2;
+  while (!work.empty()) {
+    const auto [s, e] = work.back();
+    work.pop_back();
+    const int32_t VC = e - s;
+    const int64_t span = (int64_t)d.v[e - 1] - (int64_t)d.v[s];
+    if (VC < min_distinct || span < (int64_t)min_width) {
+      leaves.push_back({s, e});
+      continue;
+    }
+    int64_t members_minus_one;
+    if (gap_mode == 0) {
+      members_minus_one = VC - 1;
+    } else {
+      int64_t nC = 0;
+      for (int32_t j = s; j < e; ++j) nC += d.c[j];
+      members_minus_one = nC - 1;
+    }
+    const double rhs = alpha * (double)span;
+    std::vector<int32_t> cut_after;
+    for (int32_t j = s; j < e - 1; ++j) {
+      const double lhs = (double)((int64_t)d.v[j + 1] - (int64_t)d.v[j]) * (double)members_minus_one;
+      if (lhs > rhs) cut_after.push_back(j);
+    }
+    if (cut_after.empty()) {
+      leaves.push_back({s, e});
+      continue;
+    }
+    int32_t piece_start = s;
+    for (int32_t j : cut_after) {
+      work.push_back({piece_start, j + 1});
+      piece_start = j + 1;
+    }
+    work.push_back({piece_start, e});
+  }
+  std::sort(leaves.begin(), leaves.end());
+  std::vector<int32_t> starts;
+  for (auto& l : leaves) starts.push_back(l.first);
+  return starts;
+}
+
+// ---------------------------------------------------------------------------
+// Stage 3: intelligent pruning (Section 4.2, "Stage 3", Eq. 3).
+//
+// Adjacent queues are merged, lowest scheduling utility first, until at most
+// max_queues remain.  Density rho(q) = n_q / (hi_q - lo_q + 1): window
+// requests per token of the queue's value span.  Mean = S_q / n_q.
+//   U_i = (rho_i + rho_{i+1}) / (|mean_{i+1} - mean_i| + eps).
+// One merge at a time; U is recomputed from the current queues before every
+// merge; ties go to the leftmost pair.  A merged queue sums counts and
+// length sums and spans both intervals.
+// ---------------------------------------------------------------------------
+struct Leaf {
+  int64_t n, S;
+  int32_t lo, hi;
+};
+
+std::vector<Leaf> stage3(std::vector<Leaf> q, int32_t max_queues, double eps) {
+  while ((int32_t)q.size() > max_queues) {
+    int32_t best_i = 0;
+    double best_u = 0.0;
+    for (int32_t i = 0; i + 1 < (int32_t)q.size(); ++i) {
+      const double rho_a = (double)q[i].n / (double)((int64_t)q[i].hi - (int64_t)q[i].lo + 1);
+      const double rho_b = (double)q[i + 1].n / (double)((int64_t)q[i + 1].hi - (int64_t)q[i + 1].lo + 1);
+      const double m_a = (double)q[i].S / (double)q[i].n;
+      const double m_b = (double)q[i + 1].S / (double)q[i + 1].n;
+      const double u = (rho_a + rho_b) / (std::fabs(m_b - m_a) + eps);
+      if (i == 0 || u < best_u) {
+        best_u = u;
+        best_i = i;
+      }
+    }
+    Leaf merged{q[best_i].n + q[best_i + 1].n, q[best_i].S + q[best_i + 1].S, q[best_i].lo,
+                q[best_i + 1].hi};
+    q[best_i] = merged;
+    q.erase(q.begin() + best_i + 1);
+  }
+  return q;
+}
+
+std::vector<Leaf> leaves_from_starts(const Distinct& d, const std::vector<int32_t>& starts) {
+  const int32_t V = (int32_t)d.v.size();
+  std::vector<Leaf> out;
+  for (size_t i = 0; i < starts.size(); ++i) {
+    const int32_t s = starts[i];
+    const int32_t e = (i + 1 < starts.size()) ? starts[i + 1] : V;
+    Leaf l{0, 0, d.v[s], d.v[e - 1]};
+    for (int32_t j = s; j < e; ++j) {
+      l.n += d.c[j];
+      l.S += d.c[j] * (int64_t)d.v[j];
+    }
+    out.push_back(l);
+  }
+  return out;
+}
+
+bool params_ok(int64_t n, int32_t init_mode, int32_t init_queues, int32_t max_queues, int32_t min_width,
+               int32_t max_len, double alpha, double eps, int32_t gap_mode) {
+  if (n < 1) return false;
+  if (init_mode != 0 && init_mode != 1) return false;
+  if (init_mode == 0 && init_queues < 1) return false;
+  if (max_queues < 1 || min_width < 0 || max_len < 1) return false;
+  if (!(alpha > 1.0) || !std::isfinite(alpha)) return false;
+  if (!(eps > 0.0) || !std::isfinite(eps)) return false;
+  if (gap_mode != 0 && gap_mode != 1) return false;
+  return true;
+}
+
+// Route one prompt length (Section 3.3 "Dispatcher").  The queues form a
+// contiguous cover of the length axis: bounds[i] is the smallest window
+// length of queue i+1, queue 0 extends down to 1 and the last queue up
+// without limit, so each length b >= 1 lies in exactly one interval.
+// Empty slots (b <= 0) route nowhere (-1).
+int32_t route_one(int32_t b, const int32_t* bounds, int32_t k) {
+  if (b <= 0) return -1;
+  return (int32_t)(std::upper_bound(bounds, bounds + (k - 1), b) - bounds);
+}
+
+}  // namespace
+
+extern "C" {
+
+int oracle_version(void) { return 1; }
+
+// Distinct clamped window values; returns V (v_out/c_out need n entries).
+int64_t oracle_distinct(const int32_t* window, int64_t n, int32_t max_len, int32_t* v_out,
+                        int64_t* c_out) {
+  if (n < 0 || max_len < 1) return kErrArg;
+  Distinct d = sorted_distinct(window, n, max_len);
+  for (size_t j = 0; j < d.v.size(); ++j) {
+    v_out[j] = d.v[j];
+    c_out[j] = d.c[j];
+  }
+  return (int64_t)d.v.size();
+}
+
+// Stage 1 over a distinct list; writes cluster starts, returns their count.
+int32_t oracle_stage1(const int32_t* v, const int64_t* c, int32_t V, int32_t init_mode,
+                      int32_t init_queues, int32_t* starts_out) {
+  if (V < 1) return kErrArg;
+  Distinct d{std::vector<int32_t>(v, v + V), std::vector<int64_t>(c, c + V)};
+  std::vector<int32_t> st = init_mode == 0 ? stage1_equal_width(d, init_queues) : stage1_kmeans3(d);
+  for (size_t i = 0; i < st.size(); ++i) starts_out[i] = st[i];
+  return (int32_t)st.size();
+}
+
+// Stage 2 from given coarse starts; writes leaf starts, returns their count.
+int32_t oracle_stage2(const int32_t* v, const int64_t* c, int32_t V, const int32_t* coarse_starts,
+                      int32_t n_coarse, double alpha, int32_t min_width, int32_t gap_mode,
+                      int32_t* leaf_starts_out) {
+  if (V < 1 || n_coarse < 1) return kErrArg;
+  Distinct d{std::vector<int32_t>(v, v + V), std::vector<int64_t>(c, c + V)};
+  std::vector<int32_t> cs(coarse_starts, coarse_starts + n_coarse);
+  std::vector<int32_t> st = stage2(d, cs, alpha, min_width, gap_mode);
+  for (size_t i = 0; i < st.size(); ++i) leaf_starts_out[i] = st[i];
+  return (int32_t)st.size();
+}
+
+// Stage 3 over explicit queues (n, S, lo, hi in length order); returns k.
+int32_t oracle_stage3(const int64_t* n, const int64_t* S, const int32_t* lo, const int32_t* hi,
+                      int32_t n_leaves, int32_t max_queues, double eps, int64_t* n_out, int64_t* S_out,
+                      int32_t* lo_out, int32_t* hi_out) {
+  if (n_leaves < 1 || max_queues < 1) return kErrArg;
+  std::vector<Leaf> q;
+  for (int32_t i = 0; i < n_leaves; ++i) q.push_back({n[i], S[i], lo[i], hi[i]});
+  q = stage3(q, max_queues, eps);
+  for (size_t i = 0; i < q.size(); ++i) {
+    n_out[i] = q[i].n;
+    S_out[i] = q[i].S;
+    lo_out[i] = q[i].lo;
+    hi_out[i] = q[i].hi;
+  }
+  return (int32_t)q.size();
+}
+
+// Full Refine-and-Prune.  Output arrays hold max_queues entries (bounds:
+// max_queues - 1).  diag[0..2] = distinct values, coarse clusters, leaves.
+int oracle_partition(const int32_t* window, int64_t n, int32_t init_mode, int32_t init_queues,
+                     int32_t max_queues, int32_t min_width, int32_t max_len, double alpha, double eps,
+                     int32_t gap_mode, int32_t* k_out, int32_t* bounds, int64_t* count, int64_t* sum,
+                     int32_t* lo, int32_t* hi, double* mean, int32_t* diag) {
+  if (!params_ok(n, init_mode, init_queues, max_queues, min_width, max_len, alpha, eps, gap_mode))
+    return kErrArg;
+  Distinct d = sorted_distinct(window, n, max_len);
+  std::vector<int32_t> coarse =
+      init_mode == 0 ? stage1_equal_width(d, init_queues) : stage1_kmeans3(d);
+  std::vector<int32_t> leaf_starts = stage2(d, coarse, alpha, min_width, gap_mode);
+  std::vector<Leaf> q = stage3(leaves_from_starts(d, leaf_starts), max_queues, eps);
+  const int32_t k = (int32_t)q.size();
+  *k_out = k;
+  for (int32_t i = 0; i < k; ++i) {
+    if (i > 0) bounds[i - 1] = q[i].lo;
+    count[i] = q[i].n;
+    sum[i] = q[i].S;
+    lo[i] = q[i].lo;
+    hi[i] = q[i].hi;
+    mean[i] = (double)q[i].S / (double)q[i].n;
+  }
+  if (diag) {
+    diag[0] = (int32_t)d.v.size();
+    diag[1] = (int32_t)coarse.size();
+    diag[2] = (int32_t)leaf_starts.size();
+  }
+  return kOk;
+}
+
+void oracle_route(const int32_t* len, int64_t n, const int32_t* bounds, int32_t k, int32_t* qid) {
+  for (int64_t i = 0; i < n; ++i) qid[i] = route_one(len[i], bounds, k);
+}
+
+// Density-Weighted Scoring, Eq. 1 / Eq. 4, for every pending request:
+//   Phi = qf * ((w_base + w_urg * cs) + w_fair * ln(b + 1))
+//   qf  = q_i / (b + 1) with q_i the 1-based queue index in length order,
+//   cs  = W_t / C_prefill(b), W_t = max(0, now - arrival) seconds,
+//   C_prefill(b) = c0 + c1*b + c2*b*b seconds,
+//   w_x = a_x * mean_q + b_x (the affine meta-policy of Section 4.1 applied
+//   to all three weights), mean_q the queue's window mean length.
+// theta is [n_theta][6] = (a_base, b_base, a_urg, b_urg, a_fair, b_fair).
+// Output score[t * n + i] is Phi rounded once to binary32; a request whose
+// Phi is NaN gets -inf; an empty slot (len <= 0) gets NaN, which marks it
+// as not admissible.
+void oracle_score(const int32_t* len, const float* arrival, int64_t n, float now, int32_t k,
+                  const int32_t* bounds, const double* mean, const float* theta, int32_t n_theta,
+                  double c0, double c1, double c2, float* score) {
+  for (int32_t t = 0; t < n_theta; ++t) {
+    const float* th = theta + 6 * t;
+    for (int64_t i = 0; i < n; ++i) {
+      const int32_t q = route_one(len[i], bounds, k);
+      if (q < 0) {
+        score[(int64_t)t * n + i] = std::numeric_limits<float>::quiet_NaN();
+        continue;
+      }
+      const double m = mean[q];
+      const double w_base = (double)th[0] * m + (double)th[1];
+      const double w_urg = (double)th[2] * m + (double)th[3];
+      const double w_fair = (double)th[4] * m + (double)th[5];
+      double W = (double)now - (double)arrival[i];
+      if (!(W > 0.0)) W = 0.0;
+      const double b = (double)len[i];
+      const double C = c0 + c1 * b + c2 * b * b;
+      const double cs = W / C;
+      const double qf = (double)(q + 1) / (b + 1.0);
+      const double phi = qf * ((w_base + w_urg * cs) + w_fair * std::log(b + 1.0));
+      float key = (float)phi;
+      if (std::isnan(key)) key = -std::numeric_limits<float>::infinity();
+      score[(int64_t)t * n + i] = key;
+    }
+  }
+}
+
+// Top-B admission for each parameter vector: the admissible requests
+// (score not NaN) in order of (score desc, id asc); the first min(B, count)
+// are admitted.  ids/top are [n_theta][B]; unused slots get id -1 / NaN.
+void oracle_select(const float* score, int64_t n, int32_t n_theta, int32_t B, int32_t* ids, float* top,
+                   int32_t* n_sel) {
+  for (int32_t t = 0; t < n_theta; ++t) {
+    const float* s = score + (int64_t)t * n;
+    std::vector<int64_t> idx;
+    for (int64_t i = 0; i < n; ++i)
+      if (!std::isnan(s[i])) idx.push_back(i);
+    const int64_t take = std::min<int64_t>(B, (int64_t)idx.size());
+    auto before = [s](int64_t a, int64_t b) { return s[a] > s[b] || (s[a] == s[b] && a < b); };
+    std::partial_sort(idx.begin(), idx.begin() + take, idx.end(), before);
+    for (int64_t r = 0; r < B; ++r) {
+      ids[(int64_t)t * B + r] = r < take ? (int32_t)idx[r] : -1;
+      top[(int64_t)t * B + r] = r < take ? s[idx[r]] : std::numeric_limits<float>::quiet_NaN();
+    }
+    n_sel[t] = (int32_t)take;
+  }
+}
+
+// One scheduling step: route, score and select (the scratch score array is
+// [n_theta][n] floats supplied by the caller).
+void oracle_step(const int32_t* len, const float* arrival, int64_t n, float now, int32_t k,
+                 const int32_t* bounds, const double* mean, const float* theta, int32_t n_theta, double c0,
+                 double c1, double c2, int32_t B, float* score_scratch, int32_t* ids, float* top,
+                 int32_t* n_sel) {
+  oracle_score(len, arrival, n, now, k, bounds, mean, theta, n_theta, c0, c1, c2, score_scratch);
+  oracle_select(score_scratch, n, n_theta, B, ids, top, n_sel);
+}
+
+}  // extern "C"
