@@ -14,7 +14,7 @@ from dataclasses import dataclass
 import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libewsjf_oracle.so")
+LIB_PATH = os.environ.get("EWSJF_ORACLE_LIB") or os.path.join(HERE, "libewsjf_oracle.so")
 
 EQUAL_WIDTH = 0
 KMEANS3 = 1
