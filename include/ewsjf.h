@@ -1,0 +1,212 @@
+/*
+ * ewsjf.h -- C ABI of the EWSJF scheduler core for AMD Instinct MI355X (gfx950).
+ *
+ * EWSJF (arXiv 2601.21758) schedules LLM requests above the execution engine.
+ * This library implements its data-parallel core:
+ *
+ *   ewsjf_partition  Refine-and-Prune: an observation window of prompt lengths
+ *                    -> contiguous queue intervals (Section 4.2, Stages 1-3,
+ *                    Eq. 2 split test, Eq. 3 scheduling utility).
+ *   ewsjf_route      Dynamic Queue Routing: each request -> the one queue whose
+ *                    interval holds its prompt length (Section 3.3 Dispatcher;
+ *                    Section 5, deterministic routing over contiguous,
+ *                    non-overlapping intervals).
+ *   ewsjf_score      Density-Weighted Scoring Phi(r, q) of every request
+ *                    (Eq. 1 / Eq. 4) with context-aware weights produced by the
+ *                    affine meta-policy w_x = a_x * mean_q + b_x (Section 4.1,
+ *                    Section 4.4.1).
+ *   ewsjf_select     Top-B admission: the B admissible requests with the highest
+ *                    score, ties to the lowest request id.
+ *   ewsjf_step       route + score + select fused into one pass over the pool.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  * Array arguments are DEVICE pointers (hipMalloc'd or torch CUDA tensors)
+ *    owned by the caller, except where marked "host".  Parameter structs are
+ *    host memory, read before the call returns.
+ *  * Request id = index into the pool arrays (a ring slot in a streaming pool).
+ *    A prompt length <= 0 marks an empty slot: it routes to -1, scores NaN and
+ *    is never admitted.
+ *  * Pool arrays (len, arrival, qid, score) must be 16-byte aligned; they may
+ *    be NULL when n == 0.
+ *  * All work is enqueued on `stream`; nothing synchronizes the host.  The
+ *    library allocates no memory: scratch space is the caller's workspace,
+ *    sized by ewsjf_workspace_bytes().  Calls that share a workspace must not
+ *    overlap.  Outputs are valid once the stream reaches the call's end.
+ *  * Argument checks run on the host before any launch and return a negative
+ *    status without touching the device.  Asynchronous faults surface at the
+ *    caller's next synchronization.
+ *  * Data-dependent conditions are not errors: fewer than B admissible
+ *    requests give n_sel < B; window lengths outside [1, max_len] are clamped.
+ */
+#ifndef EWSJF_H_
+#define EWSJF_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  EWSJF_OK = 0,
+  EWSJF_ERR_NULL = -1,      /* a required pointer is NULL */
+  EWSJF_ERR_ARG = -2,       /* a size or parameter is out of range */
+  EWSJF_ERR_WORKSPACE = -3, /* workspace smaller than ewsjf_workspace_bytes() */
+  EWSJF_ERR_LAUNCH = -4,    /* the HIP runtime refused a launch or copy */
+  EWSJF_ERR_ALIGN = -5,     /* a pool array is not 16-byte aligned */
+  EWSJF_ERR_DEVICE = -6     /* no usable gfx950 device is current */
+} ewsjf_status;
+
+enum {
+  EWSJF_MAX_QUEUES = 256,    /* queue budget cap (the paper's example is 32) */
+  EWSJF_MAX_LEN = 32768,     /* cap on the window clamp L */
+  EWSJF_MAX_B = 4096,        /* admissions per step per parameter vector */
+  EWSJF_MAX_THETA = 1024     /* parameter vectors per call */
+};
+
+/* Stage-1 initializers (Section 4.2, Stage 1). */
+enum {
+  EWSJF_INIT_EQUAL_WIDTH = 0, /* K equal-width bins over the window's [min, max] */
+  EWSJF_INIT_KMEANS3 = 1      /* exact one-dimensional 3-means (the paper's k=3) */
+};
+
+/* Which gaps form G in the Eq. 2 split test. */
+enum {
+  EWSJF_GAPS_DISTINCT = 0, /* gaps between distinct window values (default) */
+  EWSJF_GAPS_MULTISET = 1  /* gaps between consecutive sorted window entries */
+};
+
+/* ewsjf_step flags */
+enum {
+  EWSJF_STEP_TOMBSTONE = 1 /* after selecting, set len[id] = 0 for every admitted id (n_theta == 1) */
+};
+
+/* Operations for ewsjf_workspace_bytes(). */
+enum { EWSJF_OP_PARTITION = 0, EWSJF_OP_SELECT = 1, EWSJF_OP_STEP = 2 };
+
+/* Refine-and-Prune parameters (host struct).  Section 4.2: Stage 1 picks the
+ * initializer; Stage 2 splits at gaps larger than alpha * mean gap (alpha > 1,
+ * Eq. 2) until no such gap remains or the cluster's value span is below
+ * min_width; Stage 3 merges adjacent queues with the lowest utility (Eq. 3,
+ * eps in the denominator) until at most max_queues remain. */
+typedef struct {
+  int32_t init_mode;   /* EWSJF_INIT_* */
+  int32_t init_queues; /* K for EWSJF_INIT_EQUAL_WIDTH, 1..EWSJF_MAX_LEN */
+  int32_t max_queues;  /* 1..EWSJF_MAX_QUEUES */
+  int32_t min_width;   /* >= 0 tokens */
+  int32_t max_len;     /* L: window lengths are clamped to [1, L]; 1..EWSJF_MAX_LEN */
+  int32_t gap_mode;    /* EWSJF_GAPS_* */
+  double alpha;        /* significance ratio, > 1 */
+  double eps;          /* > 0 */
+} ewsjf_partition_params;
+
+/* One scoring parameter vector (device array of n_theta): the meta-policy maps
+ * a queue's mean window length mean_q to the three weights of Eq. 1/Eq. 4:
+ *   w_base = a_base*mean_q + b_base, w_urg = a_urg*mean_q + b_urg,
+ *   w_fair = a_fair*mean_q + b_fair. */
+typedef struct {
+  float a_base, b_base, a_urg, b_urg, a_fair, b_fair;
+} ewsjf_theta;
+
+/* Estimated prefill cost C_prefill(b) = c0 + c1*b + c2*b^2 seconds (host struct).
+ * Requires c0 > 0, c1 >= 0, c2 >= 0, all finite. */
+typedef struct {
+  double c0, c1, c2;
+} ewsjf_cost;
+
+/* Queue table: the queue structure of the active policy (Section 3.1).  A
+ * fixed-size device blob of ewsjf_queue_table_bytes() bytes written by
+ * ewsjf_partition or ewsjf_table_upload.  Queue i covers prompt lengths
+ * [bounds[i-1], bounds[i]) with queue 0 open below and queue k-1 open above,
+ * so the intervals cover every length exactly once.  lo/hi/count/sum/mean
+ * describe the window lengths that fell in each queue; mean is the queue's
+ * profile used by the meta-policy.  lut[b] = queue of length b for b in
+ * [1, max_len] (longer lengths belong to queue k-1). */
+typedef struct {
+  int32_t k;
+  int32_t max_len;
+  int32_t n_distinct; /* diagnostics of the last partition (0 after upload) */
+  int32_t n_coarse;
+  int32_t n_leaves;
+  int32_t reserved0;
+  int64_t n_window;
+  int32_t bounds[EWSJF_MAX_QUEUES]; /* bounds[i] = lowest length of queue i+1, i < k-1 */
+  int32_t lo[EWSJF_MAX_QUEUES];
+  int32_t hi[EWSJF_MAX_QUEUES];
+  int64_t count[EWSJF_MAX_QUEUES];
+  int64_t sum[EWSJF_MAX_QUEUES];
+  double mean[EWSJF_MAX_QUEUES];
+  uint8_t lut[EWSJF_MAX_LEN + 16];
+} ewsjf_queue_table;
+
+/* Size in bytes of the device queue table. */
+size_t ewsjf_queue_table_bytes(void);
+
+/* Workspace bytes needed by an operation.  `n` is the pool (or window) size;
+ * p is read only for EWSJF_OP_PARTITION (may be NULL otherwise). */
+size_t ewsjf_workspace_bytes(int op, int64_t n, int32_t n_theta, int32_t B, const ewsjf_partition_params* p);
+
+/* Install a queue structure computed elsewhere (for example a policy loaded
+ * from storage).  host_table: host struct with k, max_len, bounds, lo, hi,
+ * count, sum, mean filled in (lut and diagnostics are ignored).  Requires
+ * 1 <= k <= EWSJF_MAX_QUEUES, 1 <= max_len <= EWSJF_MAX_LEN and bounds strictly
+ * increasing within [1, max_len], finite means.  The device copy and its
+ * routing lut are written on `stream`; this set-up call then synchronizes
+ * `stream` so the host struct may be released on return. */
+ewsjf_status ewsjf_table_upload(const ewsjf_queue_table* host_table, void* table, hipStream_t stream);
+
+/* Refine-and-Prune (Section 4.2) over window[0..n_window) (device int32,
+ * n_window >= 1).  Writes the queue table.  Needs a workspace of
+ * ewsjf_workspace_bytes(EWSJF_OP_PARTITION, n_window, 0, 0, p) bytes. */
+ewsjf_status ewsjf_partition(const int32_t* window, int64_t n_window, const ewsjf_partition_params* p,
+                             void* table, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Dynamic Queue Routing: qid[i] = queue of len[i], or -1 for len[i] <= 0.
+ * len, qid: device int32 [n]. */
+ewsjf_status ewsjf_route(const int32_t* len, int64_t n, const void* table, int32_t* qid, hipStream_t stream);
+
+/* Density-Weighted Scoring (Eq. 1 / Eq. 4) of every request for every
+ * parameter vector:
+ *   Phi = qf * (w_base + w_urg * cs + w_fair * ln(b + 1)),
+ *   qf = (q + 1) / (b + 1) with q the 0-based queue (so q_i is 1-based),
+ *   cs = max(0, now - arrival) / C_prefill(b).
+ * len: device int32 [n]; arrival: device float32 [n] seconds; theta: device
+ * ewsjf_theta [n_theta]; score: device float32 [n_theta][n].  Empty slots get
+ * NaN; a NaN Phi of an occupied slot is stored as -inf.  Computed in binary32;
+ * agrees with the binary64 definition to about 1e-6 relative. */
+ewsjf_status ewsjf_score(const int32_t* len, const float* arrival, int64_t n, float now, const void* table,
+                         const ewsjf_theta* theta, int32_t n_theta, const ewsjf_cost* cost, float* score,
+                         hipStream_t stream);
+
+/* Top-B admission over precomputed scores (device float32 [n_theta][n]; NaN
+ * = not admissible).  For each parameter vector t: ids[t][0..n_sel[t]) are the
+ * admitted request ids in order of (score desc, id asc), top[t][.] their
+ * scores; remaining slots get id -1 and score NaN.  ids/top: device [n_theta][B],
+ * n_sel: device int32 [n_theta].  1 <= B <= EWSJF_MAX_B. */
+ewsjf_status ewsjf_select(const float* score, int64_t n, int32_t n_theta, int32_t B, int32_t* ids, float* top,
+                          int32_t* n_sel, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* One scheduling step: ewsjf_route + ewsjf_score + ewsjf_select fused, reading
+ * each request's length and arrival once and never materializing scores.
+ * Outputs as for ewsjf_select.  With EWSJF_STEP_TOMBSTONE (n_theta == 1) the
+ * admitted slots are emptied (len[id] = 0) on the device after selection. */
+ewsjf_status ewsjf_step(int32_t* len, const float* arrival, int64_t n, float now, const void* table,
+                        const ewsjf_theta* theta, int32_t n_theta, const ewsjf_cost* cost, int32_t B,
+                        int32_t flags, int32_t* ids, float* top, int32_t* n_sel, void* ws, size_t ws_bytes,
+                        hipStream_t stream);
+
+/* Human-readable name of a status code (static storage). */
+const char* ewsjf_status_string(ewsjf_status s);
+
+/* Library version (major * 10000 + minor * 100 + patch). */
+int32_t ewsjf_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* EWSJF_H_ */

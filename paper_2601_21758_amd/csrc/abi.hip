@@ -1,0 +1,189 @@
+// C ABI of the EWSJF scheduler core: argument checks on the host, then
+// launches on the caller's stream.  Nothing here allocates device memory or
+// synchronizes, except ewsjf_table_upload (a set-up call, documented).
+#include <hip/hip_runtime.h>
+
+#include <atomic>
+#include <cmath>
+#include <cstddef>
+#include <cstring>
+#include <memory>
+
+#include "ewsjf.h"
+#include "ewsjf_launch.h"
+
+namespace {
+
+static_assert(offsetof(ewsjf_queue_table, lut) % 16 == 0, "routing lut must be 16-byte aligned");
+static_assert(sizeof(ewsjf_partition_params) == 40, "ABI layout");
+static_assert(sizeof(ewsjf_cost) == 24, "ABI layout");
+
+constexpr int kMaxDevices = 64;
+std::atomic<int> g_arch_ok[kMaxDevices];  // 0 unknown, 1 gfx950, -1 other/no device
+
+ewsjf_status check_device() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return EWSJF_ERR_DEVICE;
+  if (dev >= kMaxDevices) return EWSJF_ERR_DEVICE;
+  int st = g_arch_ok[dev].load(std::memory_order_relaxed);
+  if (st == 0) {
+    hipDeviceProp_t prop;
+    if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return EWSJF_ERR_DEVICE;
+    st = std::strncmp(prop.gcnArchName, "gfx950", 6) == 0 ? 1 : -1;
+    g_arch_ok[dev].store(st, std::memory_order_relaxed);
+  }
+  return st == 1 ? EWSJF_OK : EWSJF_ERR_DEVICE;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+bool cost_ok(const ewsjf_cost* c) {
+  return std::isfinite(c->c0) && std::isfinite(c->c1) && std::isfinite(c->c2) && c->c0 > 0.0 && c->c1 >= 0.0 &&
+         c->c2 >= 0.0;
+}
+
+bool params_ok(const ewsjf_partition_params* p) {
+  if (p->init_mode != EWSJF_INIT_EQUAL_WIDTH && p->init_mode != EWSJF_INIT_KMEANS3) return false;
+  if (p->init_mode == EWSJF_INIT_EQUAL_WIDTH && (p->init_queues < 1 || p->init_queues > EWSJF_MAX_LEN)) return false;
+  if (p->max_queues < 1 || p->max_queues > EWSJF_MAX_QUEUES) return false;
+  if (p->min_width < 0) return false;
+  if (p->max_len < 1 || p->max_len > EWSJF_MAX_LEN) return false;
+  if (p->gap_mode != EWSJF_GAPS_DISTINCT && p->gap_mode != EWSJF_GAPS_MULTISET) return false;
+  if (!(p->alpha > 1.0) || !std::isfinite(p->alpha)) return false;
+  if (!(p->eps > 0.0) || !std::isfinite(p->eps)) return false;
+  return true;
+}
+
+constexpr int64_t kMaxN = 0x7fffffffLL;  // request ids are int32
+
+ewsjf_status launched(hipError_t e) { return e == hipSuccess ? EWSJF_OK : EWSJF_ERR_LAUNCH; }
+
+}  // namespace
+
+extern "C" {
+
+int32_t ewsjf_version(void) { return 10000; }
+
+const char* ewsjf_status_string(ewsjf_status s) {
+  switch (s) {
+    case EWSJF_OK: return "ok";
+    case EWSJF_ERR_NULL: return "a required pointer is NULL";
+    case EWSJF_ERR_ARG: return "a size or parameter is out of range";
+    case EWSJF_ERR_WORKSPACE: return "workspace too small";
+    case EWSJF_ERR_LAUNCH: return "kernel launch or copy failed";
+    case EWSJF_ERR_ALIGN: return "a pool array is not 16-byte aligned";
+    case EWSJF_ERR_DEVICE: return "no usable gfx950 device is current";
+  }
+  return "unknown status";
+}
+
+size_t ewsjf_queue_table_bytes(void) { return sizeof(ewsjf_queue_table); }
+
+size_t ewsjf_workspace_bytes(int op, int64_t n, int32_t n_theta, int32_t B, const ewsjf_partition_params* p) {
+  if (n < 0 || n > kMaxN) return 0;
+  if (op == EWSJF_OP_PARTITION) {
+    if (p == nullptr || !params_ok(p)) return 0;
+    return ewsjf::partition_ws_bytes(n, *p);
+  }
+  if (op == EWSJF_OP_SELECT || op == EWSJF_OP_STEP) {
+    if (n_theta < 1 || n_theta > EWSJF_MAX_THETA || B < 1 || B > EWSJF_MAX_B) return 0;
+    return ewsjf::plan_select(n, n_theta, B).ws_bytes;
+  }
+  return 0;
+}
+
+ewsjf_status ewsjf_table_upload(const ewsjf_queue_table* host_table, void* table, hipStream_t stream) {
+  if (host_table == nullptr || table == nullptr) return EWSJF_ERR_NULL;
+  const ewsjf_queue_table& h = *host_table;
+  if (h.k < 1 || h.k > EWSJF_MAX_QUEUES || h.max_len < 1 || h.max_len > EWSJF_MAX_LEN) return EWSJF_ERR_ARG;
+  for (int i = 0; i < h.k - 1; ++i) {
+    if (h.bounds[i] < 1 || h.bounds[i] > h.max_len) return EWSJF_ERR_ARG;
+    if (i > 0 && h.bounds[i] <= h.bounds[i - 1]) return EWSJF_ERR_ARG;
+  }
+  for (int i = 0; i < h.k; ++i)
+    if (!std::isfinite(h.mean[i])) return EWSJF_ERR_ARG;
+  const ewsjf_status ds = check_device();
+  if (ds != EWSJF_OK) return ds;
+  std::unique_ptr<ewsjf_queue_table> copy(new ewsjf_queue_table(h));
+  copy->n_distinct = copy->n_coarse = copy->n_leaves = copy->reserved0 = 0;
+  const size_t head = offsetof(ewsjf_queue_table, lut);
+  if (hipMemcpyAsync(table, copy.get(), head, hipMemcpyHostToDevice, stream) != hipSuccess) return EWSJF_ERR_LAUNCH;
+  if (ewsjf::launch_build_lut(static_cast<ewsjf_queue_table*>(table), stream) != hipSuccess)
+    return EWSJF_ERR_LAUNCH;
+  // The host copy must outlive the transfer.
+  if (hipStreamSynchronize(stream) != hipSuccess) return EWSJF_ERR_LAUNCH;
+  return EWSJF_OK;
+}
+
+ewsjf_status ewsjf_partition(const int32_t* window, int64_t n_window, const ewsjf_partition_params* p, void* table,
+                             void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (window == nullptr || p == nullptr || table == nullptr || ws == nullptr) return EWSJF_ERR_NULL;
+  if (n_window < 1 || n_window > kMaxN || !params_ok(p)) return EWSJF_ERR_ARG;
+  if (ws_bytes < ewsjf::partition_ws_bytes(n_window, *p)) return EWSJF_ERR_WORKSPACE;
+  if (!aligned16(ws)) return EWSJF_ERR_ALIGN;
+  const ewsjf_status ds = check_device();
+  if (ds != EWSJF_OK) return ds;
+  return launched(
+      ewsjf::launch_partition(window, n_window, *p, static_cast<ewsjf_queue_table*>(table), ws, stream));
+}
+
+ewsjf_status ewsjf_route(const int32_t* len, int64_t n, const void* table, int32_t* qid, hipStream_t stream) {
+  if (table == nullptr || (n > 0 && (len == nullptr || qid == nullptr))) return EWSJF_ERR_NULL;
+  if (n < 0 || n > kMaxN) return EWSJF_ERR_ARG;
+  if (n == 0) return EWSJF_OK;
+  if (!aligned16(len) || !aligned16(qid)) return EWSJF_ERR_ALIGN;
+  const ewsjf_status ds = check_device();
+  if (ds != EWSJF_OK) return ds;
+  return launched(ewsjf::launch_route(len, n, static_cast<const ewsjf_queue_table*>(table), qid, stream));
+}
+
+ewsjf_status ewsjf_score(const int32_t* len, const float* arrival, int64_t n, float now, const void* table,
+                         const ewsjf_theta* theta, int32_t n_theta, const ewsjf_cost* cost, float* score,
+                         hipStream_t stream) {
+  if (table == nullptr || theta == nullptr || cost == nullptr ||
+      (n > 0 && (len == nullptr || arrival == nullptr || score == nullptr)))
+    return EWSJF_ERR_NULL;
+  if (n < 0 || n > kMaxN || n_theta < 1 || n_theta > EWSJF_MAX_THETA || !cost_ok(cost) || !std::isfinite(now))
+    return EWSJF_ERR_ARG;
+  if (n == 0) return EWSJF_OK;
+  if (!aligned16(len) || !aligned16(arrival) || !aligned16(score)) return EWSJF_ERR_ALIGN;
+  const ewsjf_status ds = check_device();
+  if (ds != EWSJF_OK) return ds;
+  return launched(ewsjf::launch_score(len, arrival, n, now, static_cast<const ewsjf_queue_table*>(table), theta,
+                                      n_theta, *cost, score, stream));
+}
+
+ewsjf_status ewsjf_select(const float* score, int64_t n, int32_t n_theta, int32_t B, int32_t* ids, float* top,
+                          int32_t* n_sel, void* ws, size_t ws_bytes, hipStream_t stream) {
+  if ((n > 0 && score == nullptr) || ids == nullptr || top == nullptr || n_sel == nullptr || ws == nullptr)
+    return EWSJF_ERR_NULL;
+  if (n < 0 || n > kMaxN || n_theta < 1 || n_theta > EWSJF_MAX_THETA || B < 1 || B > EWSJF_MAX_B)
+    return EWSJF_ERR_ARG;
+  if (ws_bytes < ewsjf::plan_select(n, n_theta, B).ws_bytes) return EWSJF_ERR_WORKSPACE;
+  if ((n > 0 && !aligned16(score)) || !aligned16(ws)) return EWSJF_ERR_ALIGN;
+  const ewsjf_status ds = check_device();
+  if (ds != EWSJF_OK) return ds;
+  return launched(ewsjf::launch_select(score, n, n_theta, B, ids, top, n_sel, ws, stream));
+}
+
+ewsjf_status ewsjf_step(int32_t* len, const float* arrival, int64_t n, float now, const void* table,
+                        const ewsjf_theta* theta, int32_t n_theta, const ewsjf_cost* cost, int32_t B, int32_t flags,
+                        int32_t* ids, float* top, int32_t* n_sel, void* ws, size_t ws_bytes, hipStream_t stream) {
+  if ((n > 0 && (len == nullptr || arrival == nullptr)) || table == nullptr || theta == nullptr ||
+      cost == nullptr || ids == nullptr || top == nullptr || n_sel == nullptr || ws == nullptr)
+    return EWSJF_ERR_NULL;
+  if (n < 0 || n > kMaxN || n_theta < 1 || n_theta > EWSJF_MAX_THETA || B < 1 || B > EWSJF_MAX_B ||
+      !cost_ok(cost) || !std::isfinite(now))
+    return EWSJF_ERR_ARG;
+  if ((flags & ~EWSJF_STEP_TOMBSTONE) != 0) return EWSJF_ERR_ARG;
+  if ((flags & EWSJF_STEP_TOMBSTONE) && n_theta != 1) return EWSJF_ERR_ARG;
+  if (ws_bytes < ewsjf::plan_select(n, n_theta, B).ws_bytes) return EWSJF_ERR_WORKSPACE;
+  if ((n > 0 && (!aligned16(len) || !aligned16(arrival))) || !aligned16(ws)) return EWSJF_ERR_ALIGN;
+  const ewsjf_status ds = check_device();
+  if (ds != EWSJF_OK) return ds;
+  return launched(ewsjf::launch_step(len, arrival, n, now, static_cast<const ewsjf_queue_table*>(table), theta,
+                                     n_theta, *cost, B, (flags & EWSJF_STEP_TOMBSTONE) ? len : nullptr, ids, top,
+                                     n_sel, ws, stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,47 @@
+// Host-side launch entry points of the kernel translation units, called by
+// the C ABI layer after it has validated every argument.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "ewsjf.h"
+
+namespace ewsjf {
+
+// Launch geometry and workspace layout of the two-kernel top-B selection.
+struct SelectPlan {
+  int G = 1;        // streaming workgroups
+  int m = 4;        // per-wave order statistic used as the candidate bar
+  int M = 16;       // list entries kept per workgroup
+  int n_theta = 1;
+  size_t lists_bytes = 0, counts_bytes = 0, bounds_bytes = 0, ws_bytes = 0;
+};
+
+SelectPlan plan_select(int64_t n, int32_t n_theta, int32_t B);
+
+hipError_t launch_step(const int32_t* len, const float* arrival, int64_t n, float now,
+                       const ewsjf_queue_table* table, const ewsjf_theta* theta, int32_t n_theta,
+                       const ewsjf_cost& cost, int32_t B, int32_t* tomb_len, int32_t* ids, float* top,
+                       int32_t* n_sel, void* ws, hipStream_t stream);
+
+hipError_t launch_select(const float* score, int64_t n, int32_t n_theta, int32_t B, int32_t* ids, float* top,
+                         int32_t* n_sel, void* ws, hipStream_t stream);
+
+hipError_t launch_route(const int32_t* len, int64_t n, const ewsjf_queue_table* table, int32_t* qid,
+                        hipStream_t stream);
+
+hipError_t launch_score(const int32_t* len, const float* arrival, int64_t n, float now,
+                        const ewsjf_queue_table* table, const ewsjf_theta* theta, int32_t n_theta,
+                        const ewsjf_cost& cost, float* score, hipStream_t stream);
+
+// Builds the routing lut of a device table whose header and bounds are set.
+hipError_t launch_build_lut(ewsjf_queue_table* table, hipStream_t stream);
+
+// Refine-and-Prune.
+size_t partition_ws_bytes(int64_t n_window, const ewsjf_partition_params& p);
+hipError_t launch_partition(const int32_t* window, int64_t n_window, const ewsjf_partition_params& p,
+                            ewsjf_queue_table* table, void* ws, hipStream_t stream);
+
+}  // namespace ewsjf

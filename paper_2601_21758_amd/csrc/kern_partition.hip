@@ -1,0 +1,683 @@
+// Refine-and-Prune (Section 4.2) on the GPU.
+//
+// The paper sorts the window (the O(N log N) step of the strategic loop).
+// Prompt lengths are bounded integers, so a length histogram carries exactly
+// the information of the sorted window: the distinct values in order and
+// their multiplicities.  Kernels:
+//
+//   window_hist      LDS-privatized histogram of clamped window lengths, one
+//                    partial histogram per workgroup (no global atomics).
+//   hist_reduce      column sums of the partial histograms.
+//   rp_distinct      one workgroup: distinct values v[], counts c[] and exact
+//                    int64 prefix sums of counts and of count * value.
+//   rp_kmeans3 /     the exact 1-D 3-means initializer: every split (i, j) of
+//   rp_kmeans3_pick  the distinct values, binary64 objective, ties to the
+//                    smallest (i, j).
+//   rp_refine_prune  one workgroup: Stage 1 cluster starts, Stage 2 as
+//                    level-synchronous passes (every significant gap of every
+//                    current cluster is cut in the same pass; a pass without a
+//                    new cut ends the recursion), Stage 3 greedy merges of the
+//                    lowest-utility adjacent pair, then the queue table.
+//
+// Every binary64 expression is evaluated in the same order as the oracle's
+// definition and the library is built without floating-point contraction, so
+// boundaries, counts, sums and means agree bit for bit.
+#include <hip/hip_runtime.h>
+
+#include "ewsjf_device.h"
+#include "ewsjf_launch.h"
+
+namespace ewsjf {
+
+namespace {
+
+constexpr int kHistPerBlock = 16384;   // window entries per histogram workgroup
+constexpr int kMaxHistBlocks = 64;
+constexpr int kKmeansBlocks = 256;
+constexpr int kLeafLds = 4096;         // Stage-3 leaves kept in LDS
+constexpr int kBinsPerThread = EWSJF_MAX_LEN / kBlock;  // 32
+
+struct PartWs {
+  uint32_t* partial;  // [Gh][L+1]
+  uint32_t* hist;     // [L+1]
+  int32_t* v;         // [L] distinct values
+  uint32_t* c;        // [L] multiplicities
+  int64_t* PN;        // [L+1] prefix sums of c
+  int64_t* PS;        // [L+1] prefix sums of c * v
+  int32_t* meta;      // [16]: 0 V, 1 km_i, 2 km_j
+  double* km_F;       // [kKmeansBlocks]
+  int32_t* km_ij;     // [kKmeansBlocks][2]
+  int64_t* gn;        // [L] Stage-3 leaves (global mode)
+  int64_t* gS;
+  int32_t* glo;
+  int32_t* ghi;
+  double* gU;
+  int32_t* gnext;
+  int32_t* gprev;
+  int32_t* galive;
+  int Gh;
+};
+
+size_t up256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+int hist_blocks(int64_t n) {
+  int64_t g = (n + kHistPerBlock - 1) / kHistPerBlock;
+  if (g < 1) g = 1;
+  if (g > kMaxHistBlocks) g = kMaxHistBlocks;
+  return (int)g;
+}
+
+PartWs carve_part(void* ws, int64_t n, int L) {
+  PartWs w;
+  w.Gh = hist_blocks(n);
+  char* b = static_cast<char*>(ws);
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    char* p = b + o;
+    o += up256(bytes);
+    return p;
+  };
+  w.partial = reinterpret_cast<uint32_t*>(take((size_t)w.Gh * (L + 1) * 4));
+  w.hist = reinterpret_cast<uint32_t*>(take((size_t)(L + 1) * 4));
+  w.v = reinterpret_cast<int32_t*>(take((size_t)L * 4));
+  w.c = reinterpret_cast<uint32_t*>(take((size_t)L * 4));
+  w.PN = reinterpret_cast<int64_t*>(take((size_t)(L + 1) * 8));
+  w.PS = reinterpret_cast<int64_t*>(take((size_t)(L + 1) * 8));
+  w.meta = reinterpret_cast<int32_t*>(take(16 * 4));
+  w.km_F = reinterpret_cast<double*>(take(kKmeansBlocks * 8));
+  w.km_ij = reinterpret_cast<int32_t*>(take(kKmeansBlocks * 8));
+  w.gn = reinterpret_cast<int64_t*>(take((size_t)L * 8));
+  w.gS = reinterpret_cast<int64_t*>(take((size_t)L * 8));
+  w.glo = reinterpret_cast<int32_t*>(take((size_t)L * 4));
+  w.ghi = reinterpret_cast<int32_t*>(take((size_t)L * 4));
+  w.gU = reinterpret_cast<double*>(take((size_t)L * 8));
+  w.gnext = reinterpret_cast<int32_t*>(take((size_t)L * 4));
+  w.gprev = reinterpret_cast<int32_t*>(take((size_t)L * 4));
+  w.galive = reinterpret_cast<int32_t*>(take((size_t)L * 4));
+  return w;
+}
+
+size_t carve_size(int64_t n, int L) {
+  PartWs w = carve_part(nullptr, n, L);
+  return reinterpret_cast<size_t>(w.galive) + up256((size_t)L * 4);
+}
+
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kBlock) void window_hist(const int32_t* __restrict__ win, int64_t n, int L,
+                                                      uint32_t* __restrict__ partial) {
+  __shared__ uint32_t h[EWSJF_MAX_LEN + 1];
+  for (int b = threadIdx.x; b <= L; b += kBlock) h[b] = 0u;
+  __syncthreads();
+  const int64_t per = (n + gridDim.x - 1) / gridDim.x;
+  const int64_t beg = per * blockIdx.x;
+  const int64_t end = beg + per < n ? beg + per : n;
+  for (int64_t i = beg + threadIdx.x; i < end; i += kBlock) {
+    int x = win[i];
+    x = x < 1 ? 1 : (x > L ? L : x);
+    atomicAdd(&h[x], 1u);
+  }
+  __syncthreads();
+  uint32_t* out = partial + (size_t)blockIdx.x * (L + 1);
+  for (int b = threadIdx.x; b <= L; b += kBlock) out[b] = h[b];
+}
+
+__global__ void hist_reduce(const uint32_t* __restrict__ partial, int Gh, int L, uint32_t* __restrict__ hist) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b > L) return;
+  uint32_t s = 0;
+  for (int g = 0; g < Gh; ++g) s += partial[(size_t)g * (L + 1) + b];
+  hist[b] = s;
+}
+
+// Exclusive int64 block scan (kBlock threads).
+__device__ int64_t block_exclusive_scan64(int64_t x, int64_t* scratch, int64_t* total) {
+  const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
+  int64_t incl = x;
+  for (int off = 1; off < kWave; off <<= 1) {
+    const int64_t y = __shfl_up(incl, off);
+    if (lane >= off) incl += y;
+  }
+  __syncthreads();
+  if (lane == kWave - 1) scratch[wv] = incl;
+  __syncthreads();
+  int64_t base = 0, sum = 0;
+  for (int i = 0; i < kWavesPerBlock; ++i) {
+    if (i < wv) base += scratch[i];
+    sum += scratch[i];
+  }
+  __syncthreads();
+  *total = sum;
+  return base + incl - x;
+}
+
+// Distinct values and exact prefix sums, one workgroup.
+__global__ __launch_bounds__(kBlock) void rp_distinct(PartWs w, int L) {
+  __shared__ int64_t scr[kWavesPerBlock];
+  __shared__ int iscr[kWavesPerBlock];
+  const int t = threadIdx.x;
+  const int b0 = 1 + t * kBinsPerThread;
+  int nz = 0;
+  int64_t cn = 0, cs = 0;
+  for (int q = 0; q < kBinsPerThread; ++q) {
+    const int b = b0 + q;
+    if (b <= L) {
+      const uint32_t h = w.hist[b];
+      if (h) {
+        ++nz;
+        cn += h;
+        cs += (int64_t)h * b;
+      }
+    }
+  }
+  int V = 0;
+  int64_t totN = 0, totS = 0;
+  int pos = block_exclusive_scan(nz, iscr, &V);
+  int64_t pn = block_exclusive_scan64(cn, scr, &totN);
+  int64_t ps = block_exclusive_scan64(cs, scr, &totS);
+  for (int q = 0; q < kBinsPerThread; ++q) {
+    const int b = b0 + q;
+    if (b <= L) {
+      const uint32_t h = w.hist[b];
+      if (h) {
+        w.v[pos] = b;
+        w.c[pos] = h;
+        w.PN[pos] = pn;
+        w.PS[pos] = ps;
+        pn += h;
+        ps += (int64_t)h * b;
+        ++pos;
+      }
+    }
+  }
+  if (t == 0) {
+    w.PN[V] = totN;
+    w.PS[V] = totS;
+    w.meta[0] = V;
+    w.meta[1] = -1;
+    w.meta[2] = -1;
+  }
+}
+
+// Exact 1-D 3-means over splits 1 <= i < j <= V-1 of the distinct values.
+__device__ __forceinline__ bool km_better(double F, int i, int j, double bF, int bi, int bj) {
+  if (F > bF) return true;
+  if (F < bF) return false;
+  return i < bi || (i == bi && j < bj);
+}
+
+__global__ __launch_bounds__(kBlock) void rp_kmeans3(PartWs w) {
+  __shared__ double sF[kWavesPerBlock];
+  __shared__ int si[kWavesPerBlock], sj[kWavesPerBlock];
+  const int V = w.meta[0];
+  double bF = -1.0;
+  int bi = 0x7fffffff, bj = 0x7fffffff;
+  if (V > 3) {
+    const double nV = (double)w.PN[V], sV = (double)w.PS[V];
+    (void)nV;
+    (void)sV;
+    for (int i = 1 + blockIdx.x; i <= V - 2; i += gridDim.x) {
+      const int64_t Ni = w.PN[i], Si = w.PS[i];
+      for (int j = i + 1 + threadIdx.x; j <= V - 1; j += kBlock) {
+        const int64_t Nj = w.PN[j], Sj = w.PS[j];
+        const double n1 = (double)Ni, s1 = (double)Si;
+        const double n2 = (double)(Nj - Ni), s2 = (double)(Sj - Si);
+        const double n3 = (double)(w.PN[V] - Nj), s3 = (double)(w.PS[V] - Sj);
+        const double F = ((s1 * s1) / n1 + (s2 * s2) / n2) + (s3 * s3) / n3;
+        if (km_better(F, i, j, bF, bi, bj)) {
+          bF = F;
+          bi = i;
+          bj = j;
+        }
+      }
+    }
+  }
+  // block argmax with the tie rule
+  for (int off = 32; off > 0; off >>= 1) {
+    const double oF = __shfl_xor(bF, off);
+    const int oi = __shfl_xor(bi, off), oj = __shfl_xor(bj, off);
+    if (km_better(oF, oi, oj, bF, bi, bj)) {
+      bF = oF;
+      bi = oi;
+      bj = oj;
+    }
+  }
+  const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
+  if (lane == 0) {
+    sF[wv] = bF;
+    si[wv] = bi;
+    sj[wv] = bj;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int q = 0; q < kWavesPerBlock; ++q)
+      if (km_better(sF[q], si[q], sj[q], bF, bi, bj)) {
+        bF = sF[q];
+        bi = si[q];
+        bj = sj[q];
+      }
+    w.km_F[blockIdx.x] = bF;
+    w.km_ij[2 * blockIdx.x] = bi;
+    w.km_ij[2 * blockIdx.x + 1] = bj;
+  }
+}
+
+__global__ void rp_kmeans3_pick(PartWs w, int nblocks) {
+  if (threadIdx.x != 0) return;
+  double bF = -1.0;
+  int bi = 0x7fffffff, bj = 0x7fffffff;
+  for (int q = 0; q < nblocks; ++q)
+    if (km_better(w.km_F[q], w.km_ij[2 * q], w.km_ij[2 * q + 1], bF, bi, bj)) {
+      bF = w.km_F[q];
+      bi = w.km_ij[2 * q];
+      bj = w.km_ij[2 * q + 1];
+    }
+  w.meta[1] = bi;
+  w.meta[2] = bj;
+}
+
+// ---------------------------------------------------------------------------
+// Stage 3 utility of the adjacent pair (a, b), Eq. 3 with density = count per
+// token of value span.  Same binary64 expression order as the definition.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ double utility(int64_t na, int64_t Sa, int32_t loa, int32_t hia, int64_t nb, int64_t Sb,
+                                          int32_t lob, int32_t hib, double eps) {
+  const double rho_a = (double)na / (double)((int64_t)hia - (int64_t)loa + 1);
+  const double rho_b = (double)nb / (double)((int64_t)hib - (int64_t)lob + 1);
+  const double m_a = (double)Sa / (double)na;
+  const double m_b = (double)Sb / (double)nb;
+  return (rho_a + rho_b) / (fabs(m_b - m_a) + eps);
+}
+
+struct ArgMin {
+  double u;
+  int i;
+};
+
+__device__ __forceinline__ ArgMin argmin_pick(ArgMin a, ArgMin b) {
+  if (b.u < a.u || (b.u == a.u && b.i < a.i)) return b;
+  return a;
+}
+
+__device__ ArgMin block_argmin(ArgMin x, double* su, int* si) {
+  for (int off = 32; off > 0; off >>= 1) {
+    ArgMin o;
+    o.u = __shfl_xor(x.u, off);
+    o.i = __shfl_xor(x.i, off);
+    x = argmin_pick(x, o);
+  }
+  const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
+  __syncthreads();
+  if (lane == 0) {
+    su[wv] = x.u;
+    si[wv] = x.i;
+  }
+  __syncthreads();
+  ArgMin r{su[0], si[0]};
+  for (int q = 1; q < kWavesPerBlock; ++q) r = argmin_pick(r, ArgMin{su[q], si[q]});
+  __syncthreads();
+  return r;
+}
+
+struct RpShared {
+  union {
+    struct {
+      uint16_t v[EWSJF_MAX_LEN];
+      uint8_t start[EWSJF_MAX_LEN];
+    } a;
+    struct {
+      int64_t n[kLeafLds];
+      int64_t S[kLeafLds];
+      int32_t lo[kLeafLds];
+      int32_t hi[kLeafLds];
+      double U[kLeafLds];
+    } b;
+  } u;
+  int64_t scr64[kWavesPerBlock];
+  double su[kWavesPerBlock];
+  int si[kWavesPerBlock];
+  int iscr[kWavesPerBlock];
+  int flag;
+};
+
+// For thread-owned index ranges [j0, j0 + 32): carry_s = the last segment
+// start before j0 (-1 if none), carry_e = the first segment start after the
+// range (V if none).
+__device__ void segment_carries(RpShared& sm, int V, int j0, int* carry_s, int* carry_e) {
+  const int tid = threadIdx.x;
+  int last = -1, first = 0x7fffffff;
+  for (int q = 0; q < kBinsPerThread; ++q) {
+    const int j = j0 + q;
+    if (j < V && sm.u.a.start[j]) {
+      last = j;
+      if (first == 0x7fffffff) first = j;
+    }
+  }
+  const int lane = tid & (kWave - 1), wv = tid / kWave;
+  int incl = last;
+  for (int off = 1; off < kWave; off <<= 1) {
+    const int y = __shfl_up(incl, off);
+    if (lane >= off) incl = incl > y ? incl : y;
+  }
+  int rincl = first;
+  for (int off = 1; off < kWave; off <<= 1) {
+    const int y = __shfl_down(rincl, off);
+    if (lane + off < kWave) rincl = rincl < y ? rincl : y;
+  }
+  __syncthreads();
+  if (lane == kWave - 1) sm.iscr[wv] = incl;
+  if (lane == 0) sm.si[wv] = rincl;
+  __syncthreads();
+  int wmax = -1, wmin = 0x7fffffff;
+  for (int q = 0; q < wv; ++q) wmax = sm.iscr[q] > wmax ? sm.iscr[q] : wmax;
+  for (int q = wv + 1; q < kWavesPerBlock; ++q) wmin = sm.si[q] < wmin ? sm.si[q] : wmin;
+  const int prev_in_wave = __shfl_up(incl, 1);
+  const int next_in_wave = __shfl_down(rincl, 1);
+  const int cs = lane > 0 ? (prev_in_wave > wmax ? prev_in_wave : wmax) : wmax;
+  const int ce = lane < kWave - 1 ? (next_in_wave < wmin ? next_in_wave : wmin) : wmin;
+  __syncthreads();
+  *carry_s = cs;
+  *carry_e = ce < V ? ce : V;
+}
+
+__global__ __launch_bounds__(kBlock) void rp_refine_prune(PartWs w, ewsjf_partition_params p, int64_t n_window,
+                                                          ewsjf_queue_table* tab) {
+  __shared__ RpShared sm;
+  const int tid = threadIdx.x;
+  const int V = w.meta[0];
+  const int L = p.max_len;
+  const double inf = __builtin_inf();
+
+  // ---- Stage 1: coarse cluster starts -------------------------------------
+  for (int j = tid; j < V; j += kBlock) sm.u.a.v[j] = (uint16_t)w.v[j];
+  __syncthreads();
+  const int64_t vlo = sm.u.a.v[0], vhi = sm.u.a.v[V - 1];
+  if (p.init_mode == EWSJF_INIT_EQUAL_WIDTH) {
+    const int64_t width = vhi - vlo + 1;
+    for (int j = tid; j < V; j += kBlock) {
+      uint8_t s = 1;
+      if (j > 0) {
+        const int64_t b1 = ((int64_t)sm.u.a.v[j] - vlo) * (int64_t)p.init_queues / width;
+        const int64_t b0 = ((int64_t)sm.u.a.v[j - 1] - vlo) * (int64_t)p.init_queues / width;
+        s = b1 != b0;
+      }
+      sm.u.a.start[j] = s;
+    }
+  } else {
+    const int ki = w.meta[1], kj = w.meta[2];
+    for (int j = tid; j < V; j += kBlock) {
+      uint8_t s;
+      if (V <= 3) s = 1;
+      else s = (j == 0 || j == ki || j == kj) ? 1 : 0;
+      sm.u.a.start[j] = s;
+    }
+  }
+  __syncthreads();
+  int n_coarse = 0;
+  {
+    int cnt = 0;
+    for (int j = tid; j < V; j += kBlock) cnt += sm.u.a.start[j];
+    int tot = 0;
+    block_exclusive_scan(cnt, sm.iscr, &tot);
+    n_coarse = tot;
+  }
+
+  // ---- Stage 2: level-synchronous refinement --------------------------------
+  // Thread t owns distinct indices [32t, 32t + 32).
+  const int j0 = tid * kBinsPerThread;
+  const int min_distinct = p.gap_mode == EWSJF_GAPS_DISTINCT ? 3 : 2;
+  int carry_s = -1, carry_e = V;
+  for (;;) {
+    segment_carries(sm, V, j0, &carry_s, &carry_e);
+    int ends[kBinsPerThread];
+    {
+      int nxt = carry_e;
+      for (int q = kBinsPerThread - 1; q >= 0; --q) {
+        const int j = j0 + q;
+        ends[q] = nxt;
+        if (j < V && sm.u.a.start[j]) nxt = j;
+      }
+    }
+    uint32_t newcuts = 0;
+    int s = carry_s;
+    for (int q = 0; q < kBinsPerThread; ++q) {
+      const int j = j0 + q;
+      if (j >= V) break;
+      if (sm.u.a.start[j]) s = j;
+      // the gap between j and j+1 inside the current segment [s, e)
+      const int e = ends[q];
+      if (j + 1 >= e) continue;
+      const int VC = e - s;
+      const int64_t span = (int64_t)sm.u.a.v[e - 1] - (int64_t)sm.u.a.v[s];
+      if (VC < min_distinct || span < (int64_t)p.min_width) continue;
+      int64_t mm1;
+      if (p.gap_mode == EWSJF_GAPS_DISTINCT) mm1 = VC - 1;
+      else mm1 = (w.PN[e] - w.PN[s]) - 1;
+      const double rhs = p.alpha * (double)span;
+      const double lhs = (double)((int64_t)sm.u.a.v[j + 1] - (int64_t)sm.u.a.v[j]) * (double)mm1;
+      if (lhs > rhs) newcuts |= 1u << q;
+    }
+    const int any = __syncthreads_or(newcuts != 0);
+    if (!any) break;
+    for (int q = 0; q < kBinsPerThread; ++q)
+      if (newcuts & (1u << q)) sm.u.a.start[j0 + q + 1] = 1;
+    __syncthreads();
+  }
+
+  // ---- Leaves: one per segment, aggregates from the exact prefix sums -------
+  int nl = 0;
+  {
+    segment_carries(sm, V, j0, &carry_s, &carry_e);
+    int cnt = 0;
+    for (int q = 0; q < kBinsPerThread; ++q) {
+      const int j = j0 + q;
+      if (j < V) cnt += sm.u.a.start[j];
+    }
+    int tot = 0;
+    int pos = block_exclusive_scan(cnt, sm.iscr, &tot);
+    nl = tot;
+    int e = carry_e;
+    // walk owned indices from the right so each start knows its segment end
+    int ends_pos = pos + cnt;
+    for (int q = kBinsPerThread - 1; q >= 0; --q) {
+      const int j = j0 + q;
+      if (j < V && sm.u.a.start[j]) {
+        --ends_pos;
+        w.gn[ends_pos] = w.PN[e] - w.PN[j];
+        w.gS[ends_pos] = w.PS[e] - w.PS[j];
+        w.glo[ends_pos] = sm.u.a.v[j];
+        w.ghi[ends_pos] = sm.u.a.v[e - 1];
+        e = j;
+      }
+    }
+  }
+  __threadfence();
+  __syncthreads();
+  const int n_leaves = nl;
+  bool in_lds = false;
+
+  // ---- Stage 3, global-memory phase while the leaves exceed the LDS arrays ---
+  if (nl > p.max_queues && nl > kLeafLds) {
+    volatile double* gU = w.gU;
+    volatile int64_t* gn = w.gn;
+    volatile int64_t* gS = w.gS;
+    volatile int32_t* glo = w.glo;
+    volatile int32_t* ghi = w.ghi;
+    volatile int32_t* gnext = w.gnext;
+    volatile int32_t* gprev = w.gprev;
+    volatile int32_t* galive = w.galive;
+    const int nl0 = nl;
+    for (int i = tid; i < nl0; i += kBlock) {
+      gnext[i] = i + 1 < nl0 ? i + 1 : -1;
+      gprev[i] = i - 1;
+      galive[i] = 1;
+      gU[i] = i + 1 < nl0 ? utility(gn[i], gS[i], glo[i], ghi[i], gn[i + 1], gS[i + 1], glo[i + 1], ghi[i + 1], p.eps)
+                          : inf;
+    }
+    __threadfence();
+    __syncthreads();
+    int alive = nl0;
+    while (alive > p.max_queues && alive > kLeafLds) {
+      ArgMin x{inf, 0x7fffffff};
+      for (int i = tid; i < nl0; i += kBlock) x = argmin_pick(x, ArgMin{gU[i], i});
+      const ArgMin best = block_argmin(x, sm.su, sm.si);
+      if (tid == 0) {
+        const int a = best.i;
+        const int b = gnext[a];
+        gn[a] = gn[a] + gn[b];
+        gS[a] = gS[a] + gS[b];
+        ghi[a] = ghi[b];
+        const int c = gnext[b];
+        gnext[a] = c;
+        if (c >= 0) gprev[c] = a;
+        galive[b] = 0;
+        gU[b] = inf;
+        gU[a] = c >= 0 ? utility(gn[a], gS[a], glo[a], ghi[a], gn[c], gS[c], glo[c], ghi[c], p.eps) : inf;
+        const int pr = gprev[a];
+        if (pr >= 0) gU[pr] = utility(gn[pr], gS[pr], glo[pr], ghi[pr], gn[a], gS[a], glo[a], ghi[a], p.eps);
+      }
+      __threadfence();
+      __syncthreads();
+      --alive;
+    }
+    // Survivors, in index (= length) order, go straight into the LDS arrays.
+    const int per = (nl0 + kBlock - 1) / kBlock;
+    const int i0 = tid * per;
+    int cnt = 0;
+    for (int q = 0; q < per; ++q)
+      if (i0 + q < nl0) cnt += galive[i0 + q];
+    int tot = 0;
+    int pos = block_exclusive_scan(cnt, sm.iscr, &tot);
+    __syncthreads();  // the LDS union switches from the Stage-2 view to the leaf view
+    for (int q = 0; q < per; ++q) {
+      const int i = i0 + q;
+      if (i < nl0 && galive[i]) {
+        sm.u.b.n[pos] = gn[i];
+        sm.u.b.S[pos] = gS[i];
+        sm.u.b.lo[pos] = glo[i];
+        sm.u.b.hi[pos] = ghi[i];
+        ++pos;
+      }
+    }
+    nl = tot;
+    in_lds = true;
+    __syncthreads();
+  }
+
+  // ---- Stage 3 in LDS ----------------------------------------------------------
+  if (nl > p.max_queues) {
+    if (!in_lds) {
+      __syncthreads();
+      for (int i = tid; i < nl; i += kBlock) {
+        sm.u.b.n[i] = w.gn[i];
+        sm.u.b.S[i] = w.gS[i];
+        sm.u.b.lo[i] = w.glo[i];
+        sm.u.b.hi[i] = w.ghi[i];
+      }
+      in_lds = true;
+      __syncthreads();
+    }
+    for (int i = tid; i < nl; i += kBlock)
+      sm.u.b.U[i] = i + 1 < nl ? utility(sm.u.b.n[i], sm.u.b.S[i], sm.u.b.lo[i], sm.u.b.hi[i], sm.u.b.n[i + 1],
+                                         sm.u.b.S[i + 1], sm.u.b.lo[i + 1], sm.u.b.hi[i + 1], p.eps)
+                               : inf;
+    __syncthreads();
+    while (nl > p.max_queues) {
+      ArgMin x{inf, 0x7fffffff};
+      for (int i = tid; i < nl - 1; i += kBlock) x = argmin_pick(x, ArgMin{sm.u.b.U[i], i});
+      const ArgMin best = block_argmin(x, sm.su, sm.si);
+      const int a = best.i;
+      // remove entry a+1: shift a+2.. left by one (two phases through registers)
+      int64_t tn[kLeafLds / kBlock], tS[kLeafLds / kBlock];
+      int32_t tlo[kLeafLds / kBlock], thi[kLeafLds / kBlock];
+      double tU[kLeafLds / kBlock];
+      int cntq = 0;
+      for (int i = a + 1 + tid; i < nl - 1; i += kBlock) {
+        tn[cntq] = sm.u.b.n[i + 1];
+        tS[cntq] = sm.u.b.S[i + 1];
+        tlo[cntq] = sm.u.b.lo[i + 1];
+        thi[cntq] = sm.u.b.hi[i + 1];
+        tU[cntq] = sm.u.b.U[i + 1];
+        ++cntq;
+      }
+      const int64_t nb = sm.u.b.n[a + 1], Sb = sm.u.b.S[a + 1];
+      const int32_t hib = sm.u.b.hi[a + 1];
+      __syncthreads();
+      cntq = 0;
+      for (int i = a + 1 + tid; i < nl - 1; i += kBlock) {
+        sm.u.b.n[i] = tn[cntq];
+        sm.u.b.S[i] = tS[cntq];
+        sm.u.b.lo[i] = tlo[cntq];
+        sm.u.b.hi[i] = thi[cntq];
+        sm.u.b.U[i] = tU[cntq];
+        ++cntq;
+      }
+      if (tid == 0) {
+        sm.u.b.n[a] += nb;
+        sm.u.b.S[a] += Sb;
+        sm.u.b.hi[a] = hib;
+      }
+      --nl;
+      __syncthreads();
+      if (tid == 0) {
+        if (a + 1 < nl)
+          sm.u.b.U[a] = utility(sm.u.b.n[a], sm.u.b.S[a], sm.u.b.lo[a], sm.u.b.hi[a], sm.u.b.n[a + 1],
+                                sm.u.b.S[a + 1], sm.u.b.lo[a + 1], sm.u.b.hi[a + 1], p.eps);
+        else
+          sm.u.b.U[a] = inf;
+        if (a > 0)
+          sm.u.b.U[a - 1] = utility(sm.u.b.n[a - 1], sm.u.b.S[a - 1], sm.u.b.lo[a - 1], sm.u.b.hi[a - 1],
+                                    sm.u.b.n[a], sm.u.b.S[a], sm.u.b.lo[a], sm.u.b.hi[a], p.eps);
+      }
+      __syncthreads();
+    }
+  }
+
+  // ---- Queue table ------------------------------------------------------------
+  const int k = nl;
+  for (int i = tid; i < k; i += kBlock) {
+    const int64_t cn = in_lds ? sm.u.b.n[i] : w.gn[i];
+    const int64_t cs = in_lds ? sm.u.b.S[i] : w.gS[i];
+    const int32_t lo = in_lds ? sm.u.b.lo[i] : w.glo[i];
+    const int32_t hi = in_lds ? sm.u.b.hi[i] : w.ghi[i];
+    if (i > 0) tab->bounds[i - 1] = lo;
+    tab->lo[i] = lo;
+    tab->hi[i] = hi;
+    tab->count[i] = cn;
+    tab->sum[i] = cs;
+    tab->mean[i] = (double)cs / (double)cn;
+  }
+  if (tid == 0) {
+    tab->k = k;
+    tab->max_len = L;
+    tab->n_distinct = V;
+    tab->n_coarse = n_coarse;
+    tab->n_leaves = n_leaves;
+    tab->reserved0 = 0;
+    tab->n_window = n_window;
+  }
+}
+
+}  // namespace
+
+size_t partition_ws_bytes(int64_t n_window, const ewsjf_partition_params& p) {
+  return carve_size(n_window, p.max_len);
+}
+
+hipError_t launch_partition(const int32_t* window, int64_t n_window, const ewsjf_partition_params& p,
+                            ewsjf_queue_table* table, void* ws, hipStream_t stream) {
+  const int L = p.max_len;
+  PartWs w = carve_part(ws, n_window, L);
+  hipLaunchKernelGGL(window_hist, dim3(w.Gh), dim3(kBlock), 0, stream, window, n_window, L, w.partial);
+  hipLaunchKernelGGL(hist_reduce, dim3((L + 1 + 255) / 256), dim3(256), 0, stream, w.partial, w.Gh, L, w.hist);
+  hipLaunchKernelGGL(rp_distinct, dim3(1), dim3(kBlock), 0, stream, w, L);
+  if (p.init_mode == EWSJF_INIT_KMEANS3) {
+    hipLaunchKernelGGL(rp_kmeans3, dim3(kKmeansBlocks), dim3(kBlock), 0, stream, w);
+    hipLaunchKernelGGL(rp_kmeans3_pick, dim3(1), dim3(64), 0, stream, w, kKmeansBlocks);
+  }
+  hipLaunchKernelGGL(rp_refine_prune, dim3(1), dim3(kBlock), 0, stream, w, p, n_window, table);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return launch_build_lut(table, stream);
+}
+
+}  // namespace ewsjf

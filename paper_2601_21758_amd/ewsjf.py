@@ -1,0 +1,195 @@
+"""Thin PyTorch binding of the EWSJF C ABI (include/ewsjf.h).
+
+Each function checks tensor dtypes and devices, passes raw device pointers
+and the current HIP stream to libewsjf.so and returns output tensors.  All
+computation happens in the library's HIP kernels.
+"""
+from __future__ import annotations
+
+import ctypes as C
+
+import numpy as np
+import torch
+
+from . import _lib as L
+
+DEFAULT_COST = (0.01, 1e-4, 0.0)
+
+
+def _vp(t: torch.Tensor) -> C.c_void_p:
+    return C.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None) -> C.c_void_p:
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return C.c_void_p(s.cuda_stream)
+
+
+def _need(t: torch.Tensor, dtype: torch.dtype, name: str) -> torch.Tensor:
+    if not isinstance(t, torch.Tensor) or t.dtype != dtype or not t.is_cuda or not t.is_contiguous():
+        raise TypeError(f"{name} must be a contiguous CUDA tensor of {dtype}")
+    return t
+
+
+def params(init_mode: int = L.INIT_EQUAL_WIDTH, init_queues: int = 16, max_queues: int = 16,
+           min_width: int = 16, max_len: int = L.MAX_LEN, gap_mode: int = L.GAPS_DISTINCT,
+           alpha: float = 2.0, eps: float = 1e-6) -> L.PartitionParams:
+    return L.PartitionParams(init_mode, init_queues, max_queues, min_width, max_len, gap_mode, alpha, eps)
+
+
+def cost(c0: float = DEFAULT_COST[0], c1: float = DEFAULT_COST[1], c2: float = DEFAULT_COST[2]) -> L.Cost:
+    return L.Cost(c0, c1, c2)
+
+
+def _cost(c) -> L.Cost:
+    if isinstance(c, L.Cost):
+        return c
+    return L.Cost(*[float(x) for x in c])
+
+
+def table_bytes() -> int:
+    return int(L.lib().ewsjf_queue_table_bytes())
+
+
+def workspace_bytes(op: int, n: int, n_theta: int = 1, B: int = 1, p: L.PartitionParams | None = None) -> int:
+    pp = C.byref(p) if p is not None else None
+    return int(L.lib().ewsjf_workspace_bytes(op, int(n), int(n_theta), int(B), pp))
+
+
+class Workspace:
+    """A growable device scratch buffer for the calls that need one."""
+
+    def __init__(self, device=None):
+        self.device = torch.device(device or "cuda")
+        self.buf = None
+
+    def get(self, nbytes: int) -> torch.Tensor:
+        nbytes = max(256, int(nbytes))
+        if self.buf is None or self.buf.numel() < nbytes:
+            self.buf = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
+        return self.buf
+
+
+def new_table(device=None) -> torch.Tensor:
+    return torch.zeros(table_bytes(), dtype=torch.uint8, device=device or "cuda")
+
+
+def partition(window: torch.Tensor, p: L.PartitionParams, table: torch.Tensor | None = None,
+              ws: Workspace | None = None, stream=None) -> torch.Tensor:
+    """Refine-and-Prune over `window` (int32 lengths) -> device queue table."""
+    _need(window, torch.int32, "window")
+    table = table if table is not None else new_table(window.device)
+    ws = ws or Workspace(window.device)
+    need = workspace_bytes(L.OP_PARTITION, window.numel(), p=p)
+    buf = ws.get(need)
+    L.check(L.lib().ewsjf_partition(_vp(window), window.numel(), C.byref(p), _vp(table), _vp(buf), buf.numel(),
+                                    _stream(stream)), "ewsjf_partition")
+    return table
+
+
+def upload_table(bounds, mean, max_len: int = L.MAX_LEN, lo=None, hi=None, count=None, sum=None,
+                 device=None, stream=None) -> torch.Tensor:
+    """Install a queue structure given on the host (bounds: k-1 ints, mean: k floats)."""
+    bounds = np.asarray(bounds, np.int64).reshape(-1)
+    mean = np.asarray(mean, np.float64).reshape(-1)
+    k = mean.size
+    if bounds.size != k - 1:
+        raise ValueError("need k-1 bounds for k means")
+    h = L.QueueTable()
+    h.k, h.max_len = k, int(max_len)
+    for i, b in enumerate(bounds):
+        h.bounds[i] = int(b)
+    for i in range(k):
+        h.mean[i] = float(mean[i])
+        h.lo[i] = int(lo[i]) if lo is not None else 0
+        h.hi[i] = int(hi[i]) if hi is not None else 0
+        h.count[i] = int(count[i]) if count is not None else 0
+        h.sum[i] = int(sum[i]) if sum is not None else 0
+    table = new_table(device)
+    L.check(L.lib().ewsjf_table_upload(C.byref(h), _vp(table), _stream(stream)), "ewsjf_table_upload")
+    return table
+
+
+def read_table(table: torch.Tensor) -> dict:
+    """Copy a device queue table to the host and decode it."""
+    raw = table.detach().to("cpu").numpy().tobytes()
+    h = L.QueueTable.from_buffer_copy(raw[:C.sizeof(L.QueueTable)])
+    k = h.k
+    return {
+        "k": k, "max_len": h.max_len, "n_distinct": h.n_distinct, "n_coarse": h.n_coarse,
+        "n_leaves": h.n_leaves, "n_window": h.n_window,
+        "bounds": np.array(h.bounds[:max(k - 1, 0)], np.int32),
+        "lo": np.array(h.lo[:k], np.int32), "hi": np.array(h.hi[:k], np.int32),
+        "count": np.array(h.count[:k], np.int64), "sum": np.array(h.sum[:k], np.int64),
+        "mean": np.array(h.mean[:k], np.float64),
+        "lut": np.frombuffer(bytes(h.lut), np.uint8)[:h.max_len + 1].copy(),
+    }
+
+
+def route(length: torch.Tensor, table: torch.Tensor, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    _need(length, torch.int32, "length")
+    out = out if out is not None else torch.empty_like(length)
+    L.check(L.lib().ewsjf_route(_vp(length), length.numel(), _vp(table), _vp(out), _stream(stream)), "ewsjf_route")
+    return out
+
+
+def _theta(theta: torch.Tensor) -> torch.Tensor:
+    _need(theta, torch.float32, "theta")
+    if theta.dim() == 1:
+        theta = theta.reshape(1, -1)
+    if theta.shape[-1] != 6:
+        raise ValueError("theta rows are (a_base, b_base, a_urg, b_urg, a_fair, b_fair)")
+    return theta
+
+
+def score(length: torch.Tensor, arrival: torch.Tensor, now: float, table: torch.Tensor, theta: torch.Tensor,
+          cost_=DEFAULT_COST, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    _need(length, torch.int32, "length")
+    _need(arrival, torch.float32, "arrival")
+    theta = _theta(theta)
+    n, nt = length.numel(), theta.shape[0]
+    out = out if out is not None else torch.empty((nt, n), dtype=torch.float32, device=length.device)
+    c = _cost(cost_)
+    L.check(L.lib().ewsjf_score(_vp(length), _vp(arrival), n, float(now), _vp(table), _vp(theta), nt, C.byref(c),
+                                _vp(out), _stream(stream)), "ewsjf_score")
+    return out
+
+
+def _outs(nt: int, B: int, device, out):
+    if out is not None:
+        return out
+    ids = torch.empty((nt, B), dtype=torch.int32, device=device)
+    top = torch.empty((nt, B), dtype=torch.float32, device=device)
+    nsel = torch.empty((nt,), dtype=torch.int32, device=device)
+    return ids, top, nsel
+
+
+def select(scores: torch.Tensor, B: int, out=None, ws: Workspace | None = None, stream=None):
+    _need(scores, torch.float32, "scores")
+    if scores.dim() == 1:
+        scores = scores.reshape(1, -1)
+    nt, n = scores.shape
+    ids, top, nsel = _outs(nt, B, scores.device, out)
+    ws = ws or Workspace(scores.device)
+    buf = ws.get(workspace_bytes(L.OP_SELECT, n, nt, B))
+    L.check(L.lib().ewsjf_select(_vp(scores), n, nt, int(B), _vp(ids), _vp(top), _vp(nsel), _vp(buf), buf.numel(),
+                                 _stream(stream)), "ewsjf_select")
+    return ids, top, nsel
+
+
+def step(length: torch.Tensor, arrival: torch.Tensor, now: float, table: torch.Tensor, theta: torch.Tensor, B: int,
+         cost_=DEFAULT_COST, tombstone: bool = False, out=None, ws: Workspace | None = None, stream=None):
+    """One fused scheduling step: route + score + top-B admission."""
+    _need(length, torch.int32, "length")
+    _need(arrival, torch.float32, "arrival")
+    theta = _theta(theta)
+    n, nt = length.numel(), theta.shape[0]
+    ids, top, nsel = _outs(nt, B, length.device, out)
+    ws = ws or Workspace(length.device)
+    buf = ws.get(workspace_bytes(L.OP_STEP, n, nt, B))
+    c = _cost(cost_)
+    flags = L.STEP_TOMBSTONE if tombstone else 0
+    L.check(L.lib().ewsjf_step(_vp(length), _vp(arrival), n, float(now), _vp(table), _vp(theta), nt, C.byref(c),
+                               int(B), flags, _vp(ids), _vp(top), _vp(nsel), _vp(buf), buf.numel(), _stream(stream)),
+            "ewsjf_step")
+    return ids, top, nsel

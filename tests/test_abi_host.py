@@ -1,0 +1,159 @@
+"""Host-side checks of the C ABI: the library loads, exports every function
+include/ewsjf.h declares, and rejects bad arguments before touching a device."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+from paper_2601_21758_amd import _lib as L
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ewsjf.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(L.LIB_PATH), reason="libewsjf.so not built")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ewsjf_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported():
+    lib = L.lib()
+    names = declared_functions()
+    assert set(names) == set(L.EXPORTED)
+    for name in names:
+        assert hasattr(lib, name), name
+
+
+def test_struct_layouts_match_header():
+    lib = L.lib()
+    assert lib.ewsjf_queue_table_bytes() == C.sizeof(L.QueueTable)
+    assert C.sizeof(L.PartitionParams) == 40
+    assert C.sizeof(L.Cost) == 24
+    assert lib.ewsjf_version() >= 10000
+
+
+def test_status_strings():
+    for s in (L.OK, L.ERR_NULL, L.ERR_ARG, L.ERR_WORKSPACE, L.ERR_LAUNCH, L.ERR_ALIGN, L.ERR_DEVICE):
+        assert L.status_string(s) and L.status_string(s) != "unknown status"
+
+
+FAKE = C.c_void_p(0x10000)       # 16-byte aligned, never dereferenced: calls fail validation first
+FAKE_MIS = C.c_void_p(0x10004)   # misaligned
+
+
+def _p(**kw):
+    d = dict(init_mode=0, init_queues=16, max_queues=16, min_width=16, max_len=32768, gap_mode=0, alpha=2.0,
+             eps=1e-6)
+    d.update(kw)
+    return L.PartitionParams(**d)
+
+
+def test_workspace_bytes_rules():
+    lib = L.lib()
+    assert lib.ewsjf_workspace_bytes(L.OP_STEP, 4 << 20, 1, 1024, None) > 0
+    assert lib.ewsjf_workspace_bytes(L.OP_STEP, 1, 1, 0, None) == 0            # B < 1
+    assert lib.ewsjf_workspace_bytes(L.OP_STEP, 10, 1, 4097, None) == 0        # B too large
+    assert lib.ewsjf_workspace_bytes(L.OP_SELECT, 10, 0, 8, None) == 0         # n_theta < 1
+    assert lib.ewsjf_workspace_bytes(L.OP_PARTITION, 10, 0, 0, None) == 0      # params missing
+    assert lib.ewsjf_workspace_bytes(L.OP_PARTITION, 10, 0, 0, C.byref(_p())) > 0
+    assert lib.ewsjf_workspace_bytes(L.OP_PARTITION, 10, 0, 0, C.byref(_p(alpha=1.0))) == 0
+    assert lib.ewsjf_workspace_bytes(99, 10, 1, 1, None) == 0
+
+
+def test_step_argument_errors():
+    lib = L.lib()
+    c = L.Cost(0.01, 1e-4, 0.0)
+    ws_need = lib.ewsjf_workspace_bytes(L.OP_STEP, 1000, 1, 64, None)
+
+    def step(length=FAKE, arr=FAKE, n=1000, now=60.0, table=FAKE, theta=FAKE, nt=1, cost=c, B=64, flags=0,
+             ids=FAKE, top=FAKE, nsel=FAKE, ws=FAKE, wsb=ws_need):
+        return lib.ewsjf_step(length, arr, n, now, table, theta, nt, C.byref(cost) if cost is not None else None,
+                              B, flags, ids, top, nsel, ws, wsb, None)
+
+    assert step(length=None) == L.ERR_NULL
+    assert step(arr=None) == L.ERR_NULL
+    assert step(table=None) == L.ERR_NULL
+    assert step(cost=None) == L.ERR_NULL
+    assert step(ws=None) == L.ERR_NULL
+    assert step(n=-1) == L.ERR_ARG
+    assert step(n=1 << 31) == L.ERR_ARG
+    assert step(B=0) == L.ERR_ARG
+    assert step(B=4097) == L.ERR_ARG
+    assert step(nt=0) == L.ERR_ARG
+    assert step(nt=1025) == L.ERR_ARG
+    assert step(now=float("nan")) == L.ERR_ARG
+    assert step(cost=L.Cost(0.0, 1e-4, 0.0)) == L.ERR_ARG
+    assert step(cost=L.Cost(0.01, -1e-4, 0.0)) == L.ERR_ARG
+    assert step(cost=L.Cost(0.01, 1e-4, float("inf"))) == L.ERR_ARG
+    assert step(flags=2) == L.ERR_ARG
+    assert step(flags=L.STEP_TOMBSTONE, nt=2) == L.ERR_ARG
+    assert step(wsb=ws_need - 1) == L.ERR_WORKSPACE
+    assert step(length=FAKE_MIS) == L.ERR_ALIGN
+    assert step(arr=FAKE_MIS) == L.ERR_ALIGN
+
+
+def test_select_route_score_argument_errors():
+    lib = L.lib()
+    c = L.Cost(0.01, 1e-4, 0.0)
+    need = lib.ewsjf_workspace_bytes(L.OP_SELECT, 100, 2, 8, None)
+    assert lib.ewsjf_select(None, 100, 2, 8, FAKE, FAKE, FAKE, FAKE, need, None) == L.ERR_NULL
+    assert lib.ewsjf_select(FAKE, 100, 2, 0, FAKE, FAKE, FAKE, FAKE, need, None) == L.ERR_ARG
+    assert lib.ewsjf_select(FAKE, 100, 2, 8, FAKE, FAKE, FAKE, FAKE, need - 1, None) == L.ERR_WORKSPACE
+    assert lib.ewsjf_select(FAKE_MIS, 100, 2, 8, FAKE, FAKE, FAKE, FAKE, need, None) == L.ERR_ALIGN
+    assert lib.ewsjf_route(None, 10, FAKE, FAKE, None) == L.ERR_NULL
+    assert lib.ewsjf_route(FAKE, -5, FAKE, FAKE, None) == L.ERR_ARG
+    assert lib.ewsjf_route(FAKE, 10, FAKE, FAKE_MIS, None) == L.ERR_ALIGN
+    assert lib.ewsjf_route(FAKE, 0, FAKE, FAKE, None) == L.OK  # nothing to do, no device touched
+    assert lib.ewsjf_score(FAKE, FAKE, 10, 1.0, FAKE, FAKE, 1, None, FAKE, None) == L.ERR_NULL
+    assert lib.ewsjf_score(FAKE, FAKE, 10, 1.0, FAKE, FAKE, 0, C.byref(c), FAKE, None) == L.ERR_ARG
+    assert lib.ewsjf_score(FAKE, FAKE, 10, 1.0, FAKE, FAKE, 1, C.byref(c), FAKE_MIS, None) == L.ERR_ALIGN
+
+
+def test_partition_argument_errors():
+    lib = L.lib()
+    need = lib.ewsjf_workspace_bytes(L.OP_PARTITION, 100, 0, 0, C.byref(_p()))
+
+    def part(win=FAKE, n=100, p=_p(), table=FAKE, ws=FAKE, wsb=need):
+        return lib.ewsjf_partition(win, n, C.byref(p) if p is not None else None, table, ws, wsb, None)
+
+    assert part(win=None) == L.ERR_NULL
+    assert part(p=None) == L.ERR_NULL
+    assert part(n=0) == L.ERR_ARG
+    assert part(p=_p(alpha=1.0)) == L.ERR_ARG
+    assert part(p=_p(eps=0.0)) == L.ERR_ARG
+    assert part(p=_p(max_queues=0)) == L.ERR_ARG
+    assert part(p=_p(max_queues=257)) == L.ERR_ARG
+    assert part(p=_p(max_len=32769)) == L.ERR_ARG
+    assert part(p=_p(min_width=-1)) == L.ERR_ARG
+    assert part(p=_p(init_mode=2)) == L.ERR_ARG
+    assert part(p=_p(gap_mode=3)) == L.ERR_ARG
+    assert part(p=_p(init_queues=0)) == L.ERR_ARG
+    assert part(wsb=need - 1) == L.ERR_WORKSPACE
+
+
+def test_table_upload_argument_errors():
+    lib = L.lib()
+    h = L.QueueTable()
+    h.k, h.max_len = 3, 1000
+    h.bounds[0], h.bounds[1] = 100, 50   # not increasing
+    assert lib.ewsjf_table_upload(C.byref(h), FAKE, None) == L.ERR_ARG
+    h.bounds[1] = 2000                   # above max_len
+    assert lib.ewsjf_table_upload(C.byref(h), FAKE, None) == L.ERR_ARG
+    h.k = 0
+    assert lib.ewsjf_table_upload(C.byref(h), FAKE, None) == L.ERR_ARG
+    assert lib.ewsjf_table_upload(None, FAKE, None) == L.ERR_NULL
+
+
+def test_valid_call_without_gpu_reports_no_device():
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is present")
+    lib = L.lib()
+    h = L.QueueTable()
+    h.k, h.max_len = 1, 100
+    h.mean[0] = 10.0
+    assert lib.ewsjf_table_upload(C.byref(h), FAKE, None) == L.ERR_DEVICE

@@ -1,0 +1,334 @@
+"""GPU parity: the HIP library (through its C ABI) against the CPU oracle on
+the same seeded inputs."""
+import os
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2601_21758_amd import workloads as W
+from parity_util import check_admission, check_scores, check_table
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def E():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2601_21758_amd import ewsjf
+    ewsjf.table_bytes()  # loads libewsjf.so or raises
+    return ewsjf
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def host(t):
+    return t.detach().cpu().numpy()
+
+
+def upload(E, t: oracle.Table, max_len=32768):
+    return E.upload_table(t.bounds, t.mean, max_len, t.lo, t.hi, t.count, t.sum)
+
+
+def oracle_table(p: W.Pool, **kw):
+    return oracle.partition(p.window, init_queues=p.init_queues, max_queues=p.max_queues, **kw)
+
+
+POOLS = {
+    "cfg0": lambda: W.config(0),
+    "cfg1": lambda: W.config(1),
+    "cfg2_quarter": lambda: W.config(2, scale=0.25),
+    "ragged_300001": lambda: W.make_pool("two", 300001, 11, arrivals="poisson", rate=1e4, window=65537,
+                                         K=32, B=300),
+    "tiny_7": lambda: W.make_pool("three", 7, 12, arrivals="uniform", horizon=10.0, window=None, K=4, B=3),
+}
+
+
+# --------------------------------------------------------------------------
+# Routing
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("name", list(POOLS))
+def test_route_bit_exact(E, name):
+    p = POOLS[name]()
+    say(f"route {name} n={p.n}")
+    t = oracle_table(p)
+    tab = upload(E, t)
+    q = host(E.route(dev(p.length), tab))
+    assert np.array_equal(q, oracle.route(p.length, t))
+
+
+@pytest.mark.parametrize("kind", W.ADVERSARIAL_KINDS)
+def test_route_adversarial(E, kind):
+    L, A, now = W.adversarial(kind, 4099, 3)
+    say(f"route adversarial {kind}")
+    t = oracle.partition(np.clip(L, 1, None), init_queues=8, max_queues=8)
+    q = host(E.route(dev(L), upload(E, t)))
+    assert np.array_equal(q, oracle.route(L, t))
+
+
+# --------------------------------------------------------------------------
+# Scoring
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("name", list(POOLS))
+def test_score_within_tolerance(E, name):
+    p = POOLS[name]()
+    say(f"score {name} n={p.n}")
+    t = oracle_table(p)
+    rng = np.random.default_rng(5)
+    theta = np.concatenate([W.THETA_MID.reshape(1, 6),
+                            rng.uniform(W.THETA_LO, W.THETA_HI, (2, 6)).astype(np.float32)])
+    cost = (0.01, 1e-4, 2e-9)
+    g = host(E.score(dev(p.length), dev(p.arrival), p.now, upload(E, t), dev(theta), cost))
+    r = oracle.score(p.length, p.arrival, p.now, t, theta, cost)
+    check_scores(g, r)
+
+
+@pytest.mark.parametrize("kind", W.ADVERSARIAL_KINDS)
+def test_score_adversarial(E, kind):
+    L, A, now = W.adversarial(kind, 1027, 4)
+    A = A.copy()
+    A[::97] = np.nan
+    say(f"score adversarial {kind}")
+    t = oracle.partition(np.clip(L, 1, None), init_queues=8, max_queues=8)
+    g = host(E.score(dev(L), dev(A), now, upload(E, t), dev(W.THETA_MID)))
+    check_scores(g, oracle.score(L, A, now, t, W.THETA_MID))
+
+
+# --------------------------------------------------------------------------
+# Selection on identical scores: bit-exact
+# --------------------------------------------------------------------------
+
+SELECT_CASES = [
+    ("cfg0", 64), ("cfg1", 256), ("cfg2_quarter", 1024), ("ragged_300001", 4096), ("tiny_7", 3),
+    ("tiny_7", 64), ("cfg1", 1),
+]
+
+
+@pytest.mark.parametrize("name,B", SELECT_CASES)
+def test_select_on_oracle_scores_bit_exact(E, name, B):
+    p = POOLS[name]()
+    say(f"select {name} B={B}")
+    t = oracle_table(p)
+    s = oracle.score(p.length, p.arrival, p.now, t, p.theta[:1])
+    ids, top, nsel = E.select(dev(s), B)
+    rids, rtop, rnsel = oracle.select(s, B)
+    assert np.array_equal(host(nsel), rnsel)
+    assert np.array_equal(host(ids), rids)
+    assert np.array_equal(host(top).view(np.uint32), rtop.view(np.uint32))
+
+
+@pytest.mark.parametrize("kind", W.ADVERSARIAL_KINDS)
+@pytest.mark.parametrize("B", [1, 100, 4096])
+def test_select_adversarial_bit_exact(E, kind, B):
+    L, A, now = W.adversarial(kind, 70001, 6)
+    say(f"select adversarial {kind} B={B}")
+    t = oracle.partition(np.clip(L, 1, None), init_queues=8, max_queues=8)
+    s = oracle.score(L, A, now, t, W.THETA_MID)
+    ids, top, nsel = E.select(dev(s), B)
+    rids, rtop, rnsel = oracle.select(s, B)
+    assert np.array_equal(host(nsel), rnsel)
+    assert np.array_equal(host(ids), rids)
+
+
+def test_select_many_theta_rows_misaligned(E):
+    # n % 4 != 0 makes rows t > 0 start off a 16-byte boundary
+    rng = np.random.default_rng(8)
+    s = rng.standard_normal((5, 10007)).astype(np.float32)
+    s[rng.random(s.shape) < 0.1] = np.nan
+    s[:, 5:50] = 1.5  # ties
+    say("select 5 rows n=10007")
+    ids, top, nsel = E.select(dev(s), 300)
+    rids, rtop, rnsel = oracle.select(s, 300)
+    assert np.array_equal(host(ids), rids) and np.array_equal(host(nsel), rnsel)
+
+
+def test_select_special_values(E):
+    s = np.array([np.nan, -np.inf, np.inf, 0.0, -0.0, 1.0, -1.0, np.nan, 3.5, 3.5, -np.inf] * 37, np.float32)
+    for B in (1, 5, 64, 400, 4096):
+        say(f"select special B={B}")
+        ids, top, nsel = E.select(dev(s), B)
+        rids, rtop, rnsel = oracle.select(s, B)
+        assert np.array_equal(host(ids), rids) and np.array_equal(host(nsel), rnsel)
+
+
+def test_select_empty_and_all_nan(E):
+    for n in (0, 1, 5):
+        s = np.full(n, np.nan, np.float32)
+        ids, top, nsel = E.select(dev(s), 8)
+        assert host(nsel)[0] == 0 and np.all(host(ids) == -1)
+
+
+# --------------------------------------------------------------------------
+# Fused step
+# --------------------------------------------------------------------------
+
+def run_step(E, p, t, theta=None, B=None, tombstone=False, length=None):
+    theta = p.theta if theta is None else theta
+    B = p.B if B is None else B
+    Ld = dev(p.length) if length is None else length
+    ids, top, nsel = E.step(Ld, dev(p.arrival), p.now, upload(E, t), dev(theta), B, p.cost, tombstone=tombstone)
+    return host(ids), host(top), host(nsel), Ld
+
+
+@pytest.mark.parametrize("name", list(POOLS))
+def test_step_admission(E, name):
+    p = POOLS[name]()
+    say(f"step {name} n={p.n} B={p.B}")
+    t = oracle_table(p)
+    ids, top, nsel, _ = run_step(E, p, t)
+    rids, rtop, rnsel, rs = oracle.step(p.length, p.arrival, p.now, t, p.theta, p.B, p.cost)
+    for ti in range(p.theta.shape[0]):
+        check_admission(ids[ti], top[ti], nsel[ti], rids[ti], rtop[ti], rnsel[ti], rs[ti])
+
+
+def test_step_full_4m_pool(E):
+    p = W.config(2)
+    say(f"step cfg2 full n={p.n}")
+    t = oracle_table(p)
+    ids, top, nsel, _ = run_step(E, p, t)
+    rids, rtop, rnsel, rs = oracle.step(p.length, p.arrival, p.now, t, p.theta, p.B, p.cost)
+    check_admission(ids[0], top[0], nsel[0], rids[0], rtop[0], rnsel[0], rs[0])
+
+
+def test_step_batched_theta(E):
+    p = W.config(3)
+    say(f"step cfg3 n={p.n} n_theta={p.theta.shape[0]}")
+    t = oracle_table(p)
+    ids, top, nsel, _ = run_step(E, p, t)
+    for ti in range(0, p.theta.shape[0], 37):
+        rids, rtop, rnsel, rs = oracle.step(p.length, p.arrival, p.now, t, p.theta[ti:ti + 1], p.B, p.cost)
+        check_admission(ids[ti], top[ti], nsel[ti], rids[0], rtop[0], rnsel[0], rs[0])
+
+
+@pytest.mark.parametrize("kind", W.ADVERSARIAL_KINDS)
+@pytest.mark.parametrize("B", [1, 512, 4096])
+def test_step_adversarial(E, kind, B):
+    L, A, now = W.adversarial(kind, 200003, 9)
+    say(f"step adversarial {kind} B={B}")
+    t = oracle.partition(np.clip(L, 1, None), init_queues=16, max_queues=16)
+    ids, top, nsel = E.step(dev(L), dev(A), now, upload(E, t), dev(W.THETA_MID), B)
+    rids, rtop, rnsel, rs = oracle.step(L, A, now, t, W.THETA_MID, B)
+    check_admission(host(ids)[0], host(top)[0], host(nsel)[0], rids[0], rtop[0], rnsel[0], rs[0])
+
+
+def test_step_small_and_empty_pools(E):
+    t = oracle.partition([5, 50, 500], init_queues=2, max_queues=2)
+    for n in (0, 1, 3, 4, 5, 63, 255, 257):
+        L = (np.arange(n) % 700 + 1).astype(np.int32)
+        A = np.linspace(0, 50, n).astype(np.float32)
+        for B in (1, 4, 300):
+            say(f"step small n={n} B={B}")
+            ids, top, nsel = E.step(dev(L), dev(A), 60.0, upload(E, t), dev(W.THETA_MID), B)
+            rids, rtop, rnsel, rs = oracle.step(L, A, 60.0, t, W.THETA_MID, B)
+            check_admission(host(ids)[0], host(top)[0], host(nsel)[0], rids[0], rtop[0], rnsel[0], rs[0])
+
+
+def test_step_tombstone_flag(E):
+    p = W.config(1)
+    t = oracle_table(p)
+    say("step tombstone")
+    Ld = dev(p.length)
+    ids, top, nsel, Ld = run_step(E, p, t, tombstone=True, length=Ld)
+    after = host(Ld)
+    adm = ids[0][:nsel[0]]
+    assert np.all(after[adm] == 0)
+    keep = np.ones(p.n, bool)
+    keep[adm] = False
+    assert np.array_equal(after[keep], p.length[keep])
+    # the next step never re-admits a tombstoned slot
+    ids2, _, nsel2 = E.step(Ld, dev(p.arrival), p.now, upload(E, t), dev(p.theta), p.B)
+    assert not set(host(ids2)[0][:host(nsel2)[0]].tolist()) & set(adm.tolist())
+
+
+def test_step_deterministic(E):
+    p = W.config(2, scale=0.5)
+    t = oracle_table(p)
+    say("step determinism")
+    a = run_step(E, p, t)
+    b = run_step(E, p, t)
+    for x, y in zip(a[:3], b[:3]):
+        assert np.array_equal(x.view(np.uint8), y.view(np.uint8))
+
+
+# --------------------------------------------------------------------------
+# Refine-and-Prune
+# --------------------------------------------------------------------------
+
+def gpu_partition(E, window, **kw):
+    prm = E.params(**kw)
+    tab = E.partition(dev(np.asarray(window, np.int32)), prm)
+    return E.read_table(tab), tab
+
+
+def ora_partition(window, **kw):
+    return oracle.partition(window, **kw)
+
+
+PART_CASES = {
+    "cfg0": lambda: (W.config(0).window, dict(init_queues=16, max_queues=16)),
+    "cfg1": lambda: (W.config(1).window, dict(init_queues=64, max_queues=64)),
+    "cfg2": lambda: (W.config(2).window, dict(init_queues=256, max_queues=256)),
+    "cfg3": lambda: (W.config(3).window, dict(init_queues=64, max_queues=64)),
+    "cfg1_multiset": lambda: (W.config(1).window, dict(init_queues=64, max_queues=64, gap_mode=1)),
+    "cfg1_k1_mq8": lambda: (W.config(1).window, dict(init_queues=1, max_queues=8, min_width=0, alpha=1.5)),
+    "cfg0_mq1": lambda: (W.config(0).window, dict(init_queues=16, max_queues=1)),
+    "single_value": lambda: (np.full(1000, 77, np.int32), dict(init_queues=16, max_queues=16)),
+    "two_values": lambda: (np.array([3, 9000] * 50, np.int32), dict(init_queues=4, max_queues=4)),
+    "one_entry": lambda: (np.array([12], np.int32), dict(init_queues=3, max_queues=2)),
+    "clamped": lambda: (np.array([-5, 0, 1, 40000, 32768, 7, 7, 100000], np.int32),
+                        dict(init_queues=4, max_queues=4, min_width=0)),
+    "max_len_1000": lambda: (W.config(0).window, dict(init_queues=16, max_queues=16, max_len=1000)),
+    "dense_all_values": lambda: (np.arange(1, 32769, dtype=np.int32), dict(init_queues=256, max_queues=256)),
+    "alternating_gaps_8000_leaves": lambda: (np.cumsum(np.tile([1, 3], 8000)).astype(np.int32),
+                                            dict(init_queues=1, max_queues=64, min_width=0, alpha=1.05)),
+    "many_leaves": lambda: (np.cumsum(np.random.default_rng(3).integers(1, 40, 3000)).astype(np.int32) % 32768 + 1,
+                            dict(init_queues=1, max_queues=50, min_width=0, alpha=1.05)),
+}
+
+
+@pytest.mark.parametrize("name", list(PART_CASES))
+def test_partition_bit_exact(E, name):
+    win, kw = PART_CASES[name]()
+    say(f"partition {name} W={len(win)}")
+    g, _ = gpu_partition(E, win, **kw)
+    r = ora_partition(win, **kw)
+    check_table(g, r)
+    # the routing lut routes every length like the oracle
+    lens = np.arange(1, g["max_len"] + 1, dtype=np.int32)
+    assert np.array_equal(g["lut"][1:], oracle.route(lens, r))
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_partition_kmeans3_bit_exact(E, seed):
+    rng = np.random.default_rng(50 + seed)
+    win = W.make_pool("three", 3000, 60 + seed, arrivals="uniform").window
+    if seed == 3:
+        win = rng.integers(1, 6, 50).astype(np.int32)  # V <= 5
+    say(f"partition kmeans3 seed={seed}")
+    kw = dict(init_mode=oracle.KMEANS3, max_queues=32)
+    g, _ = gpu_partition(E, win, **kw)
+    check_table(g, ora_partition(win, **kw))
+
+
+def test_partition_then_step_end_to_end(E):
+    p = W.config(1)
+    say("partition -> step cfg1")
+    prm = E.params(init_queues=p.init_queues, max_queues=p.max_queues)
+    tab = E.partition(dev(p.window), prm)
+    t = oracle_table(p)
+    check_table(E.read_table(tab), t)
+    ids, top, nsel = E.step(dev(p.length), dev(p.arrival), p.now, tab, dev(p.theta), p.B)
+    rids, rtop, rnsel, rs = oracle.step(p.length, p.arrival, p.now, t, p.theta, p.B)
+    check_admission(host(ids)[0], host(top)[0], host(nsel)[0], rids[0], rtop[0], rnsel[0], rs[0])
