@@ -1,0 +1,270 @@
+#!/usr/bin/env python3
+"""Benchmark of the EWSJF scheduling step on one MI355X.
+
+Workload: the large mixed pool -- 4,194,304 pending requests (80% short /
+20% long lognormal prompt lengths, Poisson arrivals at 10k/s), a 256-queue
+Refine-and-Prune policy built from the last 1,048,576 lengths, one scoring
+parameter vector at the midpoint of its ranges, top B = 1,024 admissions.
+
+A timed step is one fused ewsjf_step: every pending request is routed,
+scored and considered for admission, and the top-B ids come back.  The pool
+sits in HBM; `--rotate` distinct copies (10 x 32 MiB by default, more than
+the 256 MiB Infinity Cache) are stepped in turn so each step reads HBM.
+Steps run from a captured HIP graph (chunks of up to 50 steps) so host
+launch cost does not bound the loop; an eager pass with per-kernel events
+gives the streaming kernel's own duration for the roofline figure.
+
+Prints one JSON line.  Flags: --gpus (only 1 is supported), --steps,
+--warmup, --rotate, --no-cpu (skip the oracle baseline).
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes as C
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "pending requests routed+scored+selected per sec at 4M pool; % HBM peak"
+HBM_PEAK_GBS = 8000.0
+BYTES_PER_REQUEST = 8  # int32 prompt length + float32 arrival, each read once
+PROFILE = os.path.join(ROOT, "profiles", "local_candidates_large_mixed_4m.pmc.txt")
+KERNEL_SOURCES = ("paper_2601_21758_amd/csrc/kern_select.hip", "paper_2601_21758_amd/csrc/ewsjf_device.h")
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def read_traffic(n_bytes_alg: int):
+    """HBM bytes per launch of the streaming kernel from the committed
+    rocprofv3 counter summary, or None when it is missing or stale."""
+    if not os.path.exists(PROFILE):
+        return None
+    kv = {}
+    for line in open(PROFILE):
+        if "=" in line and not line.startswith("#"):
+            k, v = line.strip().split("=", 1)
+            kv[k.strip()] = v.strip()
+    if kv.get("kernel_source_sha256_16") != kernel_source_hash():
+        return None
+    try:
+        return int(float(kv["hbm_bytes_per_dispatch"]))
+    except (KeyError, ValueError):
+        return None
+
+
+class Hip:
+    """Raw HIP events (timing on the stream the library launches on)."""
+
+    def __init__(self):
+        self.rt = C.CDLL("libamdhip64.so")
+        self.rt.hipEventCreate.argtypes = [C.POINTER(C.c_void_p)]
+        self.rt.hipEventElapsedTime.argtypes = [C.POINTER(C.c_float), C.c_void_p, C.c_void_p]
+        self.rt.hipEventSynchronize.argtypes = [C.c_void_p]
+        self.rt.hipEventDestroy.argtypes = [C.c_void_p]
+
+    def event(self):
+        e = C.c_void_p()
+        assert self.rt.hipEventCreate(C.byref(e)) == 0
+        return e
+
+    def elapsed_ms(self, a, b) -> float:
+        ms = C.c_float()
+        assert self.rt.hipEventSynchronize(b) == 0
+        assert self.rt.hipEventElapsedTime(C.byref(ms), a, b) == 0
+        return float(ms.value)
+
+
+def cpu_baseline(pool, table_ref, budget_s: float):
+    import oracle
+    reps, t0 = 0, time.perf_counter()
+    res = None
+    while True:
+        res = oracle.step(pool.length, pool.arrival, pool.now, table_ref, pool.theta, pool.B, pool.cost)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s or reps >= 200:
+            break
+    rate = reps * pool.n / el
+    return {"value": rate, "unit": "requests/s", "cores": 1, "kind": "oracle",
+            "sample": f"{reps} full passes of route+score+select (oracle_step) over the same "
+                      f"{pool.n:,}-request pool, single thread, {el:.1f} s"}, res
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=1000)
+    ap.add_argument("--warmup", type=int, default=100)
+    ap.add_argument("--rotate", type=int, default=10)
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py: this build runs on one GPU only (the scheduler core has no multi-GPU path here); "
+              "use --gpus 1", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    from paper_2601_21758_amd import _lib as L
+    from paper_2601_21758_amd import ewsjf as E
+    from paper_2601_21758_amd import workloads as W
+
+    L.lib()  # raises if libewsjf.so is missing: no fallback path exists
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda:0")
+    hip = Hip()
+
+    pool = W.config(2)
+    n, B = pool.n, pool.B
+    lens = [torch.from_numpy(pool.length).to(dev) for _ in range(args.rotate)]
+    arrs = [torch.from_numpy(pool.arrival).to(dev) for _ in range(args.rotate)]
+    theta = torch.from_numpy(pool.theta).to(dev)
+    window = torch.from_numpy(pool.window).to(dev)
+    prm = E.params(init_queues=pool.init_queues, max_queues=pool.max_queues)
+
+    # Refine-and-Prune on the 1M window (strategic loop, timed on its own).
+    pws = E.Workspace(dev)
+    table = E.partition(window, prm, ws=pws)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    e0, e1 = hip.event(), hip.event()
+    rt = hip.rt
+    rt.hipEventRecord.argtypes = [C.c_void_p, C.c_void_p]
+    rt.hipEventRecord(e0, C.c_void_p(stream.cuda_stream))
+    for _ in range(10):
+        E.partition(window, prm, table=table, ws=pws)
+    rt.hipEventRecord(e1, C.c_void_p(stream.cuda_stream))
+    partition_ms = hip.elapsed_ms(e0, e1) / 10
+    k_queues = E.read_table(table)["k"]
+
+    ids = torch.empty((1, B), dtype=torch.int32, device=dev)
+    top = torch.empty((1, B), dtype=torch.float32, device=dev)
+    nsel = torch.empty((1,), dtype=torch.int32, device=dev)
+    ws_bytes = E.workspace_bytes(L.OP_STEP, n, 1, B)
+    ws = torch.empty(max(256, ws_bytes), dtype=torch.uint8, device=dev)
+    cost = E.cost(*pool.cost)
+    lib = L.lib()
+    vp = C.c_void_p
+    args_fixed = dict(table=vp(table.data_ptr()), theta=vp(theta.data_ptr()), ids=vp(ids.data_ptr()),
+                      top=vp(top.data_ptr()), nsel=vp(nsel.data_ptr()), ws=vp(ws.data_ptr()))
+    lp = [vp(t.data_ptr()) for t in lens]
+    ap_ = [vp(t.data_ptr()) for t in arrs]
+    now = float(pool.now)
+
+    def step(i, s, marks=None):
+        r = i % args.rotate
+        if marks is None:
+            st = lib.ewsjf_step(lp[r], ap_[r], n, now, args_fixed["table"], args_fixed["theta"], 1, C.byref(cost), B,
+                                0, args_fixed["ids"], args_fixed["top"], args_fixed["nsel"], args_fixed["ws"],
+                                ws_bytes, s)
+        else:
+            st = lib.ewsjf_step_timed(lp[r], ap_[r], n, now, args_fixed["table"], args_fixed["theta"], 1,
+                                      C.byref(cost), B, 0, args_fixed["ids"], args_fixed["top"], args_fixed["nsel"],
+                                      args_fixed["ws"], ws_bytes, s, marks)
+        if st != 0:
+            raise L.EwsjfError(st, "ewsjf_step")
+
+    # ---- eager pass with per-kernel events (streaming kernel duration) -----
+    s_eager = vp(stream.cuda_stream)
+    for i in range(args.warmup):
+        step(i, s_eager)
+    torch.cuda.synchronize()
+    K = args.steps
+    marks = [(hip.event(), hip.event(), hip.event()) for _ in range(K)]
+    ev_arr = [(vp * 3)(*m) for m in marks]
+    rt.hipEventRecord(e0, s_eager)
+    for i in range(K):
+        step(i, s_eager, ev_arr[i])
+    rt.hipEventRecord(e1, s_eager)
+    eager_ms = hip.elapsed_ms(e0, e1) / K
+    k1 = [hip.elapsed_ms(m[0], m[1]) for m in marks]
+    k2 = [hip.elapsed_ms(m[1], m[2]) for m in marks]
+    k1_ms = float(np.mean(k1))
+    k2_ms = float(np.mean(k2))
+    eager_ids = ids.clone()
+    for m in marks:
+        for e in m:
+            rt.hipEventDestroy(e)
+
+    # ---- graph pass: the timed steps ------------------------------------------
+    chunk = max(c for c in range(1, min(K, 50) + 1) if K % c == 0)
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step(0, vp(side.cuda_stream))
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g):
+        cs = vp(torch.cuda.current_stream().cuda_stream)
+        for i in range(chunk):
+            step(i, cs)
+    for _ in range((args.warmup + chunk - 1) // chunk):
+        g.replay()
+    torch.cuda.synchronize()
+    gs = vp(torch.cuda.current_stream().cuda_stream)
+    rt.hipEventRecord(e0, gs)
+    for _ in range(K // chunk):
+        g.replay()
+    rt.hipEventRecord(e1, gs)
+    graph_ms = hip.elapsed_ms(e0, e1) / K
+    torch.cuda.synchronize()
+    graph_ok = bool(torch.equal(ids, eager_ids))
+
+    ms_per_step = graph_ms
+    value = n / (ms_per_step * 1e-3)
+    alg_bytes = BYTES_PER_REQUEST * n + 8 * B
+    achieved = alg_bytes / (k1_ms * 1e-3) / 1e9
+    traffic = read_traffic(alg_bytes)
+
+    out = {
+        "metric": METRIC, "value": value, "unit": "requests/s", "n_gpus": 1, "steps": K,
+        "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": "large_mixed_4m: 4,194,304 pending requests, 80/20 lognormal prompt-length mix, "
+                               "Poisson arrivals at 10k/s, 256-queue Refine-and-Prune policy from a "
+                               "1,048,576-length window, midpoint scoring parameters, top B=1024",
+                   "pool": n, "B": B, "queues": k_queues, "rotated_pool_copies": args.rotate,
+                   "execution": f"HIP graph, {chunk} steps per graph", "input_sha256": pool.digest()[:16]},
+        "roofline": {"bound": "hbm", "kernel": "local_candidates (route+score+local top-B)",
+                     "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": traffic, "bytes_per_launch": alg_bytes, "kernel_ms": k1_ms},
+        "step_hbm_frac": alg_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
+        "kernels_ms": {"local_candidates": k1_ms, "merge_candidates": k2_ms},
+        "eager_ms_per_step": eager_ms, "graph_matches_eager": graph_ok,
+        "partition_ms": partition_ms,
+    }
+    if not args.no_cpu:
+        import oracle
+        ref_table = oracle.partition(pool.window, init_queues=pool.init_queues, max_queues=pool.max_queues)
+        base, res = cpu_baseline(pool, ref_table, args.cpu_seconds)
+        out["cpu_baseline"] = base
+        rids, rtop, rnsel, rs = res
+        sys.path.insert(0, os.path.join(ROOT, "tests"))
+        from parity_util import check_admission
+        try:
+            ndiff = check_admission(ids.cpu().numpy()[0], top.cpu().numpy()[0], nsel.cpu().numpy()[0], rids[0],
+                                    rtop[0], rnsel[0], rs[0])
+            out["parity"] = f"ok ({ndiff} near-tie differences)"
+        except AssertionError as exc:  # report, never hide
+            out["parity"] = f"FAILED: {exc}"
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -166,9 +166,10 @@ ewsjf_status ewsjf_select(const float* score, int64_t n, int32_t n_theta, int32_
   return launched(ewsjf::launch_select(score, n, n_theta, B, ids, top, n_sel, ws, stream));
 }
 
-ewsjf_status ewsjf_step(int32_t* len, const float* arrival, int64_t n, float now, const void* table,
-                        const ewsjf_theta* theta, int32_t n_theta, const ewsjf_cost* cost, int32_t B, int32_t flags,
-                        int32_t* ids, float* top, int32_t* n_sel, void* ws, size_t ws_bytes, hipStream_t stream) {
+ewsjf_status ewsjf_step_timed(int32_t* len, const float* arrival, int64_t n, float now, const void* table,
+                              const ewsjf_theta* theta, int32_t n_theta, const ewsjf_cost* cost, int32_t B,
+                              int32_t flags, int32_t* ids, float* top, int32_t* n_sel, void* ws, size_t ws_bytes,
+                              hipStream_t stream, hipEvent_t* marks) {
   if ((n > 0 && (len == nullptr || arrival == nullptr)) || table == nullptr || theta == nullptr ||
       cost == nullptr || ids == nullptr || top == nullptr || n_sel == nullptr || ws == nullptr)
     return EWSJF_ERR_NULL;
@@ -183,7 +184,14 @@ ewsjf_status ewsjf_step(int32_t* len, const float* arrival, int64_t n, float now
   if (ds != EWSJF_OK) return ds;
   return launched(ewsjf::launch_step(len, arrival, n, now, static_cast<const ewsjf_queue_table*>(table), theta,
                                      n_theta, *cost, B, (flags & EWSJF_STEP_TOMBSTONE) ? len : nullptr, ids, top,
-                                     n_sel, ws, stream));
+                                     n_sel, ws, stream, marks));
+}
+
+ewsjf_status ewsjf_step(int32_t* len, const float* arrival, int64_t n, float now, const void* table,
+                        const ewsjf_theta* theta, int32_t n_theta, const ewsjf_cost* cost, int32_t B, int32_t flags,
+                        int32_t* ids, float* top, int32_t* n_sel, void* ws, size_t ws_bytes, hipStream_t stream) {
+  return ewsjf_step_timed(len, arrival, n, now, table, theta, n_theta, cost, B, flags, ids, top, n_sel, ws, ws_bytes,
+                          stream, nullptr);
 }
 
 }  // extern "C"

@@ -16,7 +16,7 @@ constexpr int kChunksPerPass = 4;            // chunks a wave holds in registers
 constexpr int kElemsPerLane = 4 * kChunksPerPass;
 constexpr int kMaxGrid = 256;                // streaming workgroups (one per CU)
 constexpr int kListCap = 1024;               // per-workgroup candidate list in LDS
-constexpr int kMergeCap = 10240;             // merge kernel candidate capacity (LDS)
+constexpr int kMergeCap = 9088;              // merge kernel candidate capacity (LDS, >= 2 * kSortMax)
 constexpr int kSortMax = 4096;               // largest bitonic sort in LDS
 constexpr int kLutBytes = EWSJF_MAX_LEN + 16;
 
@@ -60,31 +60,19 @@ __device__ __forceinline__ uint32_t comp_id(uint64_t c) { return 0xFFFFFFFFu - (
 // ---------------------------------------------------------------------------
 // Wave and block reductions.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ uint32_t wave_max_u32(uint32_t x) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) {
-    uint32_t y = __shfl_xor(x, off);
-    x = x > y ? x : y;
-  }
-  return x;
-}
+// Wave reductions from the device library (DPP-based).
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t x) { return __ockl_wfred_max_u32(x); }
 
 __device__ __forceinline__ uint64_t wave_max_u64(uint64_t x) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) {
-    uint64_t y = __shfl_xor(x, off);
-    x = x > y ? x : y;
-  }
-  return x;
+  const uint32_t mh = __ockl_wfred_max_u32((uint32_t)(x >> 32));
+  const uint32_t ml = __ockl_wfred_max_u32((uint32_t)(x >> 32) == mh ? (uint32_t)x : 0u);
+  return ((uint64_t)mh << 32) | ml;
 }
 
 __device__ __forceinline__ uint64_t wave_min_u64(uint64_t x) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) {
-    uint64_t y = __shfl_xor(x, off);
-    x = x < y ? x : y;
-  }
-  return x;
+  const uint32_t mh = __ockl_wfred_min_u32((uint32_t)(x >> 32));
+  const uint32_t ml = __ockl_wfred_min_u32((uint32_t)(x >> 32) == mh ? (uint32_t)x : 0xFFFFFFFFu);
+  return ((uint64_t)mh << 32) | ml;
 }
 
 __device__ __forceinline__ int wave_sum_i32(int x) {
@@ -136,48 +124,312 @@ __device__ __forceinline__ uint64_t block_min_u64(uint64_t x, uint64_t* scratch)
   return r;
 }
 
+// Inclusive wave prefix sum with DPP: shifts by 1, 2, 4, 8 inside each row of
+// 16 lanes, then the row totals are carried with the row broadcasts of
+// lane 15 (to rows 1, 3) and lane 31 (to rows 2, 3).
+__device__ __forceinline__ int wave_incl_scan_add(int v) {
+  v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xF, 0xF, false);  // row_shr:1
+  v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xF, 0xF, false);  // row_shr:2
+  v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xF, 0xF, false);  // row_shr:4
+  v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xF, 0xF, false);  // row_shr:8
+  v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xA, 0xF, false);  // row_bcast:15
+  v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xC, 0xF, false);  // row_bcast:31
+  return v;
+}
+
 // Exclusive prefix sum over kBlock threads; returns this thread's prefix and
 // writes the total to *total.  scratch holds >= kWavesPerBlock ints.
 __device__ __forceinline__ int block_exclusive_scan(int x, int* scratch, int* total) {
   const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
-  int incl = x;
-#pragma unroll
-  for (int off = 1; off < kWave; off <<= 1) {
-    const int y = __shfl_up(incl, off);
-    if (lane >= off) incl += y;
-  }
-  __syncthreads();
+  const int incl = wave_incl_scan_add(x);
   if (lane == kWave - 1) scratch[wv] = incl;
   __syncthreads();
   int wave_base = 0, sum = 0;
+#pragma unroll
   for (int i = 0; i < kWavesPerBlock; ++i) {
-    if (i < wv) wave_base += scratch[i];
-    sum += scratch[i];
+    const int si = scratch[i];
+    wave_base += i < wv ? si : 0;
+    sum += si;
   }
   __syncthreads();
   *total = sum;
   return wave_base + incl - x;
 }
 
-// Descending bitonic sort of s[0..P) in LDS (P a power of two <= kSortMax),
-// all kBlock threads participating.
-__device__ inline void block_bitonic_desc(uint64_t* s, int P) {
+// ---------------------------------------------------------------------------
+// Lane exchange x -> x of lane (lane ^ J) without LDS traffic where the
+// hardware allows it: DPP quad permutes for J = 1, 2, a half-row mirror
+// followed by a quad reversal for J = 4, a row rotation by 8 for J = 8, a
+// bit-mode swizzle within 32 lanes for J = 16, a permute for J = 32.
+// ---------------------------------------------------------------------------
+template <int J>
+__device__ __forceinline__ uint32_t xor_lane_u32(uint32_t x) {
+  const int v = (int)x;
+  if constexpr (J == 1) {
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false);  // quad_perm [1,0,3,2]
+  } else if constexpr (J == 2) {
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false);  // quad_perm [2,3,0,1]
+  } else if constexpr (J == 4) {
+    const int y = __builtin_amdgcn_update_dpp(0, v, 0x141, 0xF, 0xF, false);    // row_half_mirror
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, y, 0x1B, 0xF, 0xF, false);  // quad_perm [3,2,1,0]
+  } else if constexpr (J == 8) {
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, v, 0x128, 0xF, 0xF, false);  // row_ror:8
+  } else if constexpr (J == 16) {
+    return (uint32_t)__builtin_amdgcn_ds_swizzle(v, 0x401F);  // and 0x1F, xor 0x10
+  } else {
+    return (uint32_t)__shfl_xor(v, 32);
+  }
+}
+
+template <int J>
+__device__ __forceinline__ uint64_t xor_lane_u64(uint64_t x) {
+  const uint32_t lo = xor_lane_u32<J>((uint32_t)x);
+  const uint32_t hi = xor_lane_u32<J>((uint32_t)(x >> 32));
+  return ((uint64_t)hi << 32) | lo;
+}
+
+__device__ __forceinline__ uint64_t xor_lane_u64_dyn(uint64_t x, int j) {
+  switch (j) {
+    case 1: return xor_lane_u64<1>(x);
+    case 2: return xor_lane_u64<2>(x);
+    case 4: return xor_lane_u64<4>(x);
+    case 8: return xor_lane_u64<8>(x);
+    case 16: return xor_lane_u64<16>(x);
+    default: return xor_lane_u64<32>(x);
+  }
+}
+
+__device__ __forceinline__ void cmpx_desc(uint64_t& a, uint64_t& b, bool desc) {
+  const uint64_t hi = a > b ? a : b, lo = a > b ? b : a;
+  a = desc ? hi : lo;
+  b = desc ? lo : hi;
+}
+
+// Descending bitonic sort of s[0..P) in LDS, all kBlock threads participating,
+// P a power of two with 64 <= P <= 64 * kWavesPerBlock * EPT.  Each wave owns
+// EPT consecutive 64-element blocks (one element per lane per block):
+// partners closer than 64 are reached by lane exchanges, partners in another
+// block of the same wave in registers, and only partners held by another wave
+// go through LDS (two barriers per such stage).
+template <int EPT>
+__device__ void block_sort_desc_t(uint64_t* s, int P) {
+  const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
+  const int nblk = P / kWave;
+  const bool active = EPT * wv < nblk;
+  const int i0 = EPT * wv * kWave + lane;  // index of x[0]
+  uint64_t x[EPT];
+#pragma unroll
+  for (int q = 0; q < EPT; ++q) x[q] = active ? s[i0 + q * kWave] : 0ull;
   for (int k = 2; k <= P; k <<= 1) {
     for (int j = k >> 1; j > 0; j >>= 1) {
-      for (int i = threadIdx.x; i < P; i += kBlock) {
-        const int ixj = i ^ j;
-        if (ixj > i) {
-          const uint64_t a = s[i], b = s[ixj];
-          const bool desc = (i & k) == 0;
-          if (desc ? (a < b) : (a > b)) {
-            s[i] = b;
-            s[ixj] = a;
+      if (j >= kWave * EPT) {
+        __syncthreads();
+        if (active) {
+#pragma unroll
+          for (int q = 0; q < EPT; ++q) s[i0 + q * kWave] = x[q];
+        }
+        __syncthreads();
+        if (active) {
+#pragma unroll
+          for (int q = 0; q < EPT; ++q) {
+            const int i = i0 + q * kWave;
+            const uint64_t y = s[i ^ j];
+            const bool keep_max = ((i & j) == 0) == ((i & k) == 0);
+            x[q] = keep_max ? (x[q] > y ? x[q] : y) : (x[q] < y ? x[q] : y);
           }
         }
+      } else if (j >= kWave) {
+        if constexpr (EPT == 2) {
+          cmpx_desc(x[0], x[1], (i0 & k) == 0);
+        } else if constexpr (EPT == 4) {
+          if (j == kWave) {
+            cmpx_desc(x[0], x[1], (i0 & k) == 0);
+            cmpx_desc(x[2], x[3], ((i0 + 2 * kWave) & k) == 0);
+          } else {
+            cmpx_desc(x[0], x[2], (i0 & k) == 0);
+            cmpx_desc(x[1], x[3], ((i0 + kWave) & k) == 0);
+          }
+        }
+      } else {
+        const bool lower = (lane & j) == 0;
+#pragma unroll
+        for (int q = 0; q < EPT; ++q) {
+          const uint64_t y = xor_lane_u64_dyn(x[q], j);
+          const bool keep_max = lower == (((i0 + q * kWave) & k) == 0);
+          x[q] = keep_max ? (x[q] > y ? x[q] : y) : (x[q] < y ? x[q] : y);
+        }
       }
-      __syncthreads();
     }
   }
+  __syncthreads();
+  if (active) {
+#pragma unroll
+    for (int q = 0; q < EPT; ++q) s[i0 + q * kWave] = x[q];
+  }
+  __syncthreads();
+}
+
+// Descending sort of s[0..P), P a power of two in [1, kSortMax]; entries
+// beyond the caller's data must already be 0.
+__device__ inline void block_sort_desc(uint64_t* s, int P) {
+  if (P < kWave) {
+    for (int i = P + threadIdx.x; i < kWave; i += kBlock) s[i] = 0ull;
+    __syncthreads();
+    P = kWave;
+  }
+  if (P <= kBlock) block_sort_desc_t<1>(s, P);
+  else if (P <= 2 * kBlock) block_sort_desc_t<2>(s, P);
+  else block_sort_desc_t<4>(s, P);
+}
+
+// ---------------------------------------------------------------------------
+// Exact cut by histogram narrowing over LDS data X[0..U) of distinct 64-bit
+// keys (0 = empty slot, never counted): returns `cut` such that exactly
+// min(need, #nonzero) elements are >= cut when stop_at_most == 0, or such
+// that at least `need` and at most `stop_at_most` elements are >= cut
+// otherwise.  Each round bins the current value range [lo, hi] into 256
+// linear bins and descends into the bin where the running count from the
+// top reaches `need`; ranges shrink 256-fold per round.  All kBlock threads
+// call it.  hist: 256 LDS words; iscan: >= 3 LDS ints; red: kWavesPerBlock
+// LDS u64.
+// ---------------------------------------------------------------------------
+__device__ inline uint64_t find_cut(const uint64_t* X, int U, int need, int stop_at_most, uint32_t* hist, int* iscan,
+                                    uint64_t* red) {
+  const int tid = threadIdx.x;
+  uint64_t mx = 0, mn = ~0ull;
+  for (int i = tid; i < U; i += kBlock) {
+    const uint64_t x = X[i];
+    if (x != 0ull) {
+      mx = x > mx ? x : mx;
+      mn = x < mn ? x : mn;
+    }
+  }
+  uint64_t hi = block_max_u64(mx, red);
+  uint64_t lo = block_min_u64(mn, red);
+  if (hi == 0ull) return ~0ull;  // nothing to select
+  int above = 0;
+  for (;;) {
+    const uint64_t diff = hi - lo;
+    const int bits = diff == 0 ? 0 : 64 - __clzll((long long)diff);
+    const int shift = bits > 8 ? bits - 8 : 0;
+    for (int i = tid; i < 256; i += kBlock) hist[i] = 0u;
+    __syncthreads();
+    for (int i = tid; i < U; i += kBlock) {
+      const uint64_t x = X[i];
+      if (x != 0ull && x >= lo && x <= hi) atomicAdd(&hist[(int)((x - lo) >> shift)], 1u);
+    }
+    __syncthreads();
+    if (tid < kWave) {
+      const int b0 = 255 - 4 * tid;  // lane 0 holds bins 255..252
+      int v[4], s = 0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        v[q] = (int)hist[b0 - q];
+        s += v[q];
+      }
+      int incl = s;
+#pragma unroll
+      for (int off = 1; off < kWave; off <<= 1) {
+        const int y = __shfl_up(incl, off);
+        if (tid >= off) incl += y;
+      }
+      const int total = __shfl(incl, kWave - 1);
+      int run = incl - s;
+      int found = -1, fa = 0, fat = 0;
+      const int want = need - above < total ? need - above : total;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        if (found < 0 && run + v[q] >= want) {
+          found = b0 - q;
+          fa = run;
+          fat = run + v[q];
+        }
+        run += v[q];
+      }
+      const uint64_t bal = __ballot(found >= 0);
+      const int first = bal ? __ffsll((long long)bal) - 1 : 0;
+      const int f0 = __shfl(found, first), f1 = __shfl(fa, first), f2 = __shfl(fat, first);
+      if (tid == 0) {
+        iscan[0] = f0;
+        iscan[1] = f1;
+        iscan[2] = f2;
+      }
+    }
+    __syncthreads();
+    const int cstar = iscan[0], cum_above = iscan[1], cum_at = iscan[2];
+    __syncthreads();
+    const uint64_t bin_lo = lo + ((uint64_t)cstar << shift);
+    const bool done = stop_at_most > 0 ? (above + cum_at <= stop_at_most) : (above + cum_at <= need);
+    if (done || shift == 0) return bin_lo;
+    above += cum_above;
+    lo = bin_lo;
+    const uint64_t width = (((uint64_t)1) << shift) - 1;
+    hi = (hi - lo > width) ? lo + width : hi;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Descending counting sort of S[0..nS) (distinct nonzero keys, nS <= 4096)
+// into O[0..nS): 4096 linear buckets over [min, max], bucket offsets from the
+// top, scatter, then each element's rank inside its bucket.  Cost is linear
+// in nS plus the squares of the bucket sizes.  cnt: 4096 LDS words.
+// ---------------------------------------------------------------------------
+__device__ inline void bucket_sort_desc(const uint64_t* S, int nS, uint64_t* T, uint64_t* O, uint32_t* cnt,
+                                        int* iscan, uint64_t* red) {
+  const int tid = threadIdx.x;
+  constexpr int NB = 4096;
+  uint64_t mx = 0, mn = ~0ull;
+  for (int i = tid; i < nS; i += kBlock) {
+    const uint64_t x = S[i];
+    mx = x > mx ? x : mx;
+    mn = x < mn ? x : mn;
+  }
+  const uint64_t hi = block_max_u64(mx, red);
+  const uint64_t lo = block_min_u64(mn, red);
+  const uint64_t diff = hi - lo;
+  const int bits = diff == 0 ? 0 : 64 - __clzll((long long)diff);
+  const int shift = bits > 12 ? bits - 12 : 0;
+  for (int i = tid; i < NB; i += kBlock) cnt[i] = 0u;
+  __syncthreads();
+  for (int i = tid; i < nS; i += kBlock) atomicAdd(&cnt[(int)((S[i] - lo) >> shift)], 1u);
+  __syncthreads();
+  // exclusive offsets in descending bucket order: thread t owns buckets
+  // NB-1-4t .. NB-4-4t
+  {
+    uint32_t v[4];
+    int sum = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      v[q] = cnt[NB - 1 - 4 * tid - q];
+      sum += (int)v[q];
+    }
+    int tot = 0;
+    int run = block_exclusive_scan(sum, iscan, &tot);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      cnt[NB - 1 - 4 * tid - q] = (uint32_t)run;  // bucket start, reused as a cursor
+      run += (int)v[q];
+    }
+  }
+  __syncthreads();
+  for (int i = tid; i < nS; i += kBlock) {
+    const uint64_t x = S[i];
+    const int b = (int)((x - lo) >> shift);
+    const uint32_t pos = atomicAdd(&cnt[b], 1u);
+    T[pos] = x;
+  }
+  __syncthreads();
+  // cnt[b] is now the end of bucket b; its start is the end of bucket b+1.
+  for (int i = tid; i < nS; i += kBlock) {
+    const uint64_t x = T[i];
+    const int b = (int)((x - lo) >> shift);
+    const int start = b == NB - 1 ? 0 : (int)cnt[b + 1];
+    const int end = (int)cnt[b];
+    int rank = 0;
+    for (int r = start; r < end; ++r) rank += T[r] > x;
+    O[start + rank] = x;
+  }
+  __syncthreads();
 }
 
 __host__ __device__ inline int pow2_ceil(int x) {
@@ -188,7 +440,11 @@ __host__ __device__ inline int pow2_ceil(int x) {
 
 // ---------------------------------------------------------------------------
 // Scoring (Eq. 1 / Eq. 4) in binary32 for one request of prompt length b >= 1:
-//   Phi = (q+1)/(b+1) * (w_base + w_urg * W/C(b) + w_fair * ln(b+1)).
+//   Phi = (q+1)/(b+1) * (w_base + w_urg * W/C(b) + w_fair * ln(b+1))
+// evaluated as (q+1) * (w_base*C + w_urg*W + w_fair*ln(b+1)*C) / ((b+1)*C),
+// which needs one reciprocal and one log2.  With the parameter ranges of the
+// evaluation every term is positive, so the binary32 result is within a few
+// ulps of the exact value.
 // ---------------------------------------------------------------------------
 struct CostF {
   float c0, c1, c2;
@@ -199,10 +455,18 @@ __device__ __forceinline__ float phi_f32(int b, float arrival, float now, const 
   const float bp1 = fb + 1.0f;
   const float W = fmaxf(now - arrival, 0.0f);  // NaN arrival or future arrival -> 0
   const float C = __builtin_fmaf(__builtin_fmaf(c.c2, fb, c.c1), fb, c.c0);
-  const float cs = W * __builtin_amdgcn_rcpf(C);
   const float lg = __builtin_amdgcn_logf(bp1);  // log2(b + 1)
-  const float inner = __builtin_fmaf(p.wf2, lg, __builtin_fmaf(p.wu, cs, p.wb));
-  return p.qn * inner * __builtin_amdgcn_rcpf(bp1);
+  const float num = __builtin_fmaf(p.wf2 * lg, C, __builtin_fmaf(p.wb, C, p.wu * W));
+  return p.qn * num * __builtin_amdgcn_rcpf(bp1 * C);
+}
+
+// Order-preserving key of a score computed in registers: NaN -> -inf,
+// -0 -> +0, then the sign-magnitude flip.  Never 0 (0 marks "no element").
+__device__ __forceinline__ uint32_t ukey_fast(float f) {
+  f = fmaxf(f, -__builtin_inff());  // maxNum: a NaN operand yields -inf
+  f = f + 0.0f;                     // -0 + 0 = +0
+  const uint32_t u = __float_as_uint(f);
+  return u ^ ((uint32_t)((int32_t)u >> 31) | 0x80000000u);
 }
 
 // Stage the routing lut and per-queue constants of one parameter vector into

@@ -28,8 +28,10 @@
 namespace ewsjf {
 
 // ---------------------------------------------------------------------------
-// Key sources.  load4 issues the loads of 4 consecutive requests; keys4
-// turns them into composites (0 = no element).
+// Key sources.  stage_load issues the global loads of any per-workgroup
+// tables; load4 issues the loads of 4 consecutive requests; stage_store
+// (after both) moves the tables into LDS; keys4 turns the 4 requests into
+// 32-bit order-preserving score keys (0 = no element).
 // ---------------------------------------------------------------------------
 struct PoolSource {
   const int32_t* len;
@@ -38,6 +40,9 @@ struct PoolSource {
   const ewsjf_theta* theta;  // [n_theta]
   float now;
   CostF cost;
+
+  static constexpr int kLutVecs = kLutBytes / 16;                       // 2049
+  static constexpr int kLutPerThread = (kLutVecs + kBlock - 1) / kBlock;  // 3
 
   struct Raw {
     i32x4 l;
@@ -48,9 +53,38 @@ struct PoolSource {
     QParams qp[EWSJF_MAX_QUEUES];
     int L;
   };
+  struct Stage {
+    i32x4 v[kLutPerThread];
+  };
 
-  __device__ __forceinline__ void stage(Shared& sh, int t) const {
-    stage_policy(table, theta + t, sh.lut, sh.qp);
+  __device__ __forceinline__ void stage_load(Stage& st) const {
+    const int nvec = (table->max_len + 1 + 15) / 16;
+    const i32x4* src = reinterpret_cast<const i32x4*>(table->lut);
+#pragma unroll
+    for (int r = 0; r < kLutPerThread; ++r) {
+      const int i = threadIdx.x + r * kBlock;
+      st.v[r] = i < nvec ? src[i] : i32x4{0, 0, 0, 0};
+    }
+  }
+
+  __device__ __forceinline__ void stage_store(Shared& sh, const Stage& st, int t) const {
+    const int nvec = (table->max_len + 1 + 15) / 16;
+    i32x4* dst = reinterpret_cast<i32x4*>(sh.lut);
+#pragma unroll
+    for (int r = 0; r < kLutPerThread; ++r) {
+      const int i = threadIdx.x + r * kBlock;
+      if (i < nvec) dst[i] = st.v[r];
+    }
+    const int k = table->k;
+    if ((int)threadIdx.x < k) {
+      const int q = threadIdx.x;
+      const double m = table->mean[q];
+      const ewsjf_theta th = theta[t];
+      const double wb = (double)th.a_base * m + (double)th.b_base;
+      const double wu = (double)th.a_urg * m + (double)th.b_urg;
+      const double wf = (double)th.a_fair * m + (double)th.b_fair;
+      sh.qp[q] = QParams{(float)wb, (float)wu, (float)(wf * 0.69314718055994530942), (float)(q + 1)};
+    }
     if (threadIdx.x == 0) sh.L = table->max_len;
   }
 
@@ -69,19 +103,18 @@ struct PoolSource {
     return r;
   }
 
-  __device__ __forceinline__ uint64_t key1(int b, float a, uint32_t id, const Shared& sh) const {
-    if (b <= 0) return 0ull;
-    const int q = sh.lut[b < sh.L ? b : sh.L];
-    const float phi = phi_f32(b, a, now, sh.qp[q], cost);
-    return make_comp(ukey_of(phi), id);
+  __device__ __forceinline__ uint32_t key1(int b, float a, const Shared& sh) const {
+    const int L = sh.L;
+    const int bc = b < 0 ? 0 : (b < L ? b : L);
+    const float phi = phi_f32(b, a, now, sh.qp[sh.lut[bc]], cost);
+    return b > 0 ? ukey_fast(phi) : 0u;
   }
 
-  __device__ __forceinline__ void keys4(const Raw& r, int64_t base, const Shared& sh, uint64_t out[4]) const {
-    const uint32_t id = (uint32_t)base;
-    out[0] = key1(r.l.x, r.a.x, id + 0, sh);
-    out[1] = key1(r.l.y, r.a.y, id + 1, sh);
-    out[2] = key1(r.l.z, r.a.z, id + 2, sh);
-    out[3] = key1(r.l.w, r.a.w, id + 3, sh);
+  __device__ __forceinline__ void keys4(const Raw& r, const Shared& sh, uint32_t out[4]) const {
+    out[0] = key1(r.l.x, r.a.x, sh);
+    out[1] = key1(r.l.y, r.a.y, sh);
+    out[2] = key1(r.l.z, r.a.z, sh);
+    out[3] = key1(r.l.w, r.a.w, sh);
   }
 };
 
@@ -93,12 +126,12 @@ struct ScoreSource {
     f32x4 s;
   };
   struct Shared {
-    int t;
+    int unused;
   };
+  struct Stage {};
 
-  __device__ __forceinline__ void stage(Shared& sh, int t) const {
-    if (threadIdx.x == 0) sh.t = t;
-  }
+  __device__ __forceinline__ void stage_load(Stage&) const {}
+  __device__ __forceinline__ void stage_store(Shared&, const Stage&, int) const {}
 
   __device__ __forceinline__ Raw load4(int64_t base, int64_t nn) const {
     Raw r;
@@ -116,16 +149,14 @@ struct ScoreSource {
     return r;
   }
 
-  __device__ __forceinline__ static uint64_t key1(float s, uint32_t id) {
-    return (s != s) ? 0ull : make_comp(ukey_of(s), id);
-  }
+  // A NaN score marks an element that is not admissible.
+  __device__ __forceinline__ static uint32_t key1(float s) { return (s != s) ? 0u : ukey_of(s); }
 
-  __device__ __forceinline__ void keys4(const Raw& r, int64_t base, const Shared&, uint64_t out[4]) const {
-    const uint32_t id = (uint32_t)base;
-    out[0] = key1(r.s.x, id + 0);
-    out[1] = key1(r.s.y, id + 1);
-    out[2] = key1(r.s.z, id + 2);
-    out[3] = key1(r.s.w, id + 3);
+  __device__ __forceinline__ void keys4(const Raw& r, const Shared&, uint32_t out[4]) const {
+    out[0] = key1(r.s.x);
+    out[1] = key1(r.s.y);
+    out[2] = key1(r.s.z);
+    out[3] = key1(r.s.w);
   }
 
   const float* row_ = nullptr;
@@ -152,10 +183,14 @@ __device__ __forceinline__ ScoreSource bind_theta<ScoreSource>(const ScoreSource
 // ---------------------------------------------------------------------------
 struct ListShared {
   uint64_t list[kListCap];
+  uint64_t list2[kListCap];
+  uint32_t hist[256];
   uint64_t red[kWavesPerBlock];
+  int iscan[kWavesPerBlock];
   uint32_t bar[kWavesPerBlock];
   int cnt;
   int ovf;
+  int nout;
 };
 
 // Chunk c of workgroup w at local index lc is c = w + G * lc.  Wave v of the
@@ -187,43 +222,42 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
   const int64_t my_chunks = nchunks > blockIdx.x ? (nchunks - blockIdx.x + G - 1) / G : 0;
   const int passes = (int)((my_chunks + kWavesPerBlock * kChunksPerPass - 1) / (kWavesPerBlock * kChunksPerPass));
 
-  // Issue the first pass's loads before staging the policy so the table
-  // fetch overlaps the pool stream.
+  // Table loads first, then the pool loads, then the table goes to LDS: the
+  // LDS stores wait only for the (older) table loads, so scoring of the
+  // first chunks starts while the rest of the pool is still streaming in.
+  typename Src::Stage st;
+  src.stage_load(st);
   typename Src::Raw raw[kChunksPerPass];
   int64_t base[kChunksPerPass];
   if (passes > 0) load_pass(src, n, nchunks, G, 0, raw, base);
-  src.stage(sh, t);
+  src.stage_store(sh, st, t);
   if (threadIdx.x == 0) {
     ls.cnt = 0;
     ls.ovf = 0;
+    ls.nout = 0;
   }
   __syncthreads();
 
-  uint32_t T_bar = 0;  // every element with key >= T_bar (over all passes) is listed
+  // Each wave emits, as soon as its own keys are ready, every element whose
+  // key is >= its bar (the m-th largest lane maximum of the wave).  The
+  // workgroup's completeness bound is the largest bar of any wave and pass;
+  // entries below it are dropped at the end.
+  uint32_t my_bar = 0;  // this wave's largest bar over the passes
   for (int pass = 0; pass < passes; ++pass) {
     if (pass > 0) load_pass(src, n, nchunks, G, pass, raw, base);
-    uint64_t c[kElemsPerLane];
+    uint32_t key[kElemsPerLane];
 #pragma unroll
-    for (int j = 0; j < kChunksPerPass; ++j) src.keys4(raw[j], base[j], sh, c + 4 * j);
+    for (int j = 0; j < kChunksPerPass; ++j) src.keys4(raw[j], sh, key + 4 * j);
     uint32_t lmax = 0;
 #pragma unroll
-    for (int e = 0; e < kElemsPerLane; ++e) {
-      const uint32_t k = (uint32_t)(c[e] >> 32);
-      lmax = k > lmax ? k : lmax;
-    }
+    for (int e = 0; e < kElemsPerLane; ++e) lmax = key[e] > lmax ? key[e] : lmax;
     const uint32_t bar = wave_mth_largest_u32(lmax, m);
-    if (lane == 0) ls.bar[wv] = bar;
-    __syncthreads();
-    uint32_t tw = 0;
-#pragma unroll
-    for (int i = 0; i < kWavesPerBlock; ++i) tw = ls.bar[i] > tw ? ls.bar[i] : tw;
-    T_bar = tw > T_bar ? tw : T_bar;
-    // Append every element with key >= T_bar (and every element at all when
-    // T_bar == 0, i.e. the share has few distinct keys).
-    if (__ballot(lmax >= T_bar && lmax != 0u)) {
+    const uint32_t wbar = bar > my_bar ? bar : my_bar;
+    my_bar = wbar;
+    if (__ballot(lmax >= wbar && lmax != 0u)) {
 #pragma unroll
       for (int e = 0; e < kElemsPerLane; ++e) {
-        const bool p = c[e] != 0ull && (uint32_t)(c[e] >> 32) >= T_bar;
+        const bool p = key[e] != 0u && key[e] >= wbar;
         const uint64_t bal = __ballot(p);
         if (bal) {
           int b0 = 0;
@@ -231,62 +265,107 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
           b0 = __shfl(b0, 0);
           const int pos = b0 + __popcll(bal & lanemask_lt());
           if (p) {
-            if (pos < kListCap) ls.list[pos] = c[e];
+            if (pos < kListCap) ls.list[pos] = make_comp(key[e], (uint32_t)(base[e / 4] + (e & 3)));
             else ls.ovf = 1;
           }
         }
       }
     }
-    __syncthreads();
     if (passes > 1) {
-      // Between passes drop entries below the running bar so the list holds
-      // exactly the elements >= T_bar seen so far.
+      // Keep the list bounded between passes: drop entries below the
+      // workgroup's running bar.
+      if (lane == 0) ls.bar[wv] = my_bar;
+      __syncthreads();
+      uint32_t tb = 0;
+#pragma unroll
+      for (int i = 0; i < kWavesPerBlock; ++i) tb = ls.bar[i] > tb ? ls.bar[i] : tb;
       const int cnt = ls.cnt < kListCap ? ls.cnt : kListCap;
-      const uint64_t lowc = (uint64_t)T_bar << 32;
-      __syncthreads();
-      int keep = 0;
-      uint64_t mine[1];
-      // compaction through a scan (cnt <= kListCap = kBlock)
-      mine[0] = (int)threadIdx.x < cnt ? ls.list[threadIdx.x] : 0ull;
-      const int flag = mine[0] >= lowc && mine[0] != 0ull;
+      const uint64_t lowc = (uint64_t)tb << 32;
+      const uint64_t mine = (int)threadIdx.x < cnt ? ls.list[threadIdx.x] : 0ull;
+      const int flag = mine >= lowc && mine != 0ull;
       int total = 0;
-      const int pos = block_exclusive_scan(flag, reinterpret_cast<int*>(ls.red), &total);
-      __syncthreads();
-      if (flag) ls.list[pos] = mine[0];
-      keep = total;
-      if (threadIdx.x == 0) ls.cnt = keep;
+      const int pos = block_exclusive_scan(flag, ls.iscan, &total);
+      if (flag) ls.list[pos] = mine;
+      if (threadIdx.x == 0) ls.cnt = total;
       __syncthreads();
     }
   }
+  if (lane == 0) ls.bar[wv] = my_bar;
+  __syncthreads();
 
-  // Sort, cut to M and publish.
-  const int cnt_all = ls.cnt;
-  const bool ovf = ls.ovf != 0;
+  // Publish into the workgroup's M fixed slots (unused slots hold 0).
   const size_t slot = (size_t)t * G + blockIdx.x;
-  if (ovf) {
+  uint64_t* out_list = lists + slot * (size_t)M;
+  if (ls.ovf != 0) {
+    for (int i = threadIdx.x; i < M; i += kBlock) out_list[i] = 0ull;
     if (threadIdx.x == 0) {
       counts[slot] = 0u;
       bounds[slot] = ~0ull;  // nothing guaranteed: the merge re-reads this share
     }
     return;
   }
-  const int cnt = cnt_all;
-  const int P = pow2_ceil(cnt < 2 ? 2 : cnt);
-  for (int i = cnt + (int)threadIdx.x; i < P; i += kBlock) ls.list[i] = 0ull;
-  __syncthreads();
-  block_bitonic_desc(ls.list, P);
+  uint32_t T_bar = 0;
+#pragma unroll
+  for (int i = 0; i < kWavesPerBlock; ++i) T_bar = ls.bar[i] > T_bar ? ls.bar[i] : T_bar;
   const uint64_t lowc = (uint64_t)T_bar << 32;
-  // entries below lowc (from earlier passes with a lower bar) were removed above
-  int out = cnt < M ? cnt : M;
-  uint64_t T = lowc;
-  if (cnt > M) {
-    const uint64_t mth = ls.list[M - 1];
-    T = mth > T ? mth : T;
+  const int raw_cnt = ls.cnt;
+  // Entries >= lowc are exactly the share's elements >= lowc.
+  {
+    const uint64_t x = (int)threadIdx.x < raw_cnt ? ls.list[threadIdx.x] : 0ull;
+    const bool keep = x >= lowc && x != 0ull;
+    const uint64_t bal = __ballot(keep);
+    if (bal) {
+      int b0 = 0;
+      if (lane == 0) b0 = atomicAdd(&ls.nout, __popcll(bal));
+      b0 = __shfl(b0, 0);
+      if (keep) ls.list2[b0 + __popcll(bal & lanemask_lt())] = x;
+    }
   }
-  for (int i = threadIdx.x; i < out; i += kBlock) lists[slot * (size_t)M + i] = ls.list[i];
+  __syncthreads();
+  const int cnt = ls.nout;
+  if (cnt <= M) {
+    for (int i = threadIdx.x; i < M; i += kBlock) out_list[i] = i < cnt ? ls.list2[i] : 0ull;
+    if (threadIdx.x == 0) {
+      counts[slot] = (uint32_t)cnt;
+      bounds[slot] = lowc;
+    }
+    return;
+  }
+  // Keep exactly the M largest: every element >= the M-th largest is listed.
+  if (cnt <= 256) {
+    // rank counting over a short list
+    if ((int)threadIdx.x < cnt) {
+      const uint64_t x = ls.list2[threadIdx.x];
+      int rank = 0;
+      for (int j = 0; j < cnt; ++j) rank += ls.list2[j] > x;
+      if (rank < M) out_list[rank] = x;
+      if (rank == M - 1) {
+        counts[slot] = (uint32_t)M;
+        bounds[slot] = x > lowc ? x : lowc;
+      }
+    }
+    return;
+  }
+  const uint64_t cut = find_cut(ls.list2, cnt, M, 0, ls.hist, ls.iscan, ls.red);
+  if (threadIdx.x == 0) ls.nout = 0;
+  __syncthreads();
+  for (int i0 = 0; i0 < cnt; i0 += kBlock) {
+    const int i = i0 + (int)threadIdx.x;
+    const uint64_t x = i < cnt ? ls.list2[i] : 0ull;
+    const bool p = x >= cut && x != 0ull;
+    const uint64_t bal = __ballot(p);
+    if (bal) {
+      int b0 = 0;
+      if (lane == 0) b0 = atomicAdd(&ls.nout, __popcll(bal));
+      b0 = __shfl(b0, 0);
+      if (p) out_list[b0 + __popcll(bal & lanemask_lt())] = x;
+    }
+  }
+  __syncthreads();
+  for (int i = ls.nout + (int)threadIdx.x; i < M; i += kBlock) out_list[i] = 0ull;
   if (threadIdx.x == 0) {
-    counts[slot] = (uint32_t)out;
-    bounds[slot] = T;
+    counts[slot] = (uint32_t)ls.nout;
+    bounds[slot] = cut > lowc ? cut : lowc;
   }
 }
 
@@ -297,120 +376,51 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
 struct MergeShared {
   uint64_t X[kMergeCap];
   uint64_t S[kSortMax];
-  uint32_t hist[256];
+  uint32_t cnt[4096];
   uint64_t red[kWavesPerBlock];
+  uint64_t wmax[kWavesPerBlock];
+  uint64_t wmin[kWavesPerBlock];
   int iscan[kWavesPerBlock];
   int cntX;
   int cntS;
+  int cut_bin;
+  int cut_cnt;
 };
 
-// Exact top-B of X[0..U) (distinct composites), sorted descending into
-// X[0..min(U, B)).  Returns min(U, B).
-__device__ inline int topb_inplace(MergeShared& ms, int U, int B) {
-  const int tid = threadIdx.x;
-  if (U <= kSortMax) {
-    const int P = pow2_ceil(U < 2 ? 2 : U);
-    for (int i = U + tid; i < P; i += kBlock) ms.X[i] = 0ull;
+// Exact top-B of the nonzero entries of X[0..U) (distinct composites; when
+// U <= B every entry must be nonzero), sorted descending into X[0..min(U, B)).
+// Returns the number selected.  When U > B the candidates at or above
+// a histogram cut (between B and kSortMax of them) are gathered first; the
+// gathered set is then ordered by a counting sort.
+__device__ inline int select_top(MergeShared& ms, int U, int B) {
+  const int tid = threadIdx.x, lane = tid & (kWave - 1);
+  if (U == 0) return 0;
+  const uint64_t* src = ms.X;
+  int nS = U;
+  if (U > B) {
+    const uint64_t cut = find_cut(ms.X, U, B, kSortMax, ms.cnt, ms.iscan, ms.red);
+    if (tid == 0) ms.cntS = 0;
     __syncthreads();
-    block_bitonic_desc(ms.X, P);
-    return U < B ? U : B;
-  }
-  // Narrow a value range [lo, hi] until every element >= its cut fits the
-  // sort buffer; `need` elements are still wanted from inside the range and
-  // `above` elements lie above it.
-  uint64_t mx = 0, mn = ~0ull;
-  for (int i = tid; i < U; i += kBlock) {
-    const uint64_t x = ms.X[i];
-    mx = x > mx ? x : mx;
-    mn = x < mn ? x : mn;
-  }
-  uint64_t hi = block_max_u64(mx, ms.red);
-  uint64_t lo = block_min_u64(mn, ms.red);
-  int need = B, above = 0;
-  uint64_t cut = lo;
-  for (;;) {
-    const uint64_t diff = hi - lo;
-    const int bits = diff == 0 ? 0 : 64 - __clzll((long long)diff);
-    const int shift = bits > 8 ? bits - 8 : 0;
-    for (int i = tid; i < 256; i += kBlock) ms.hist[i] = 0u;
-    __syncthreads();
-    for (int i = tid; i < U; i += kBlock) {
-      const uint64_t x = ms.X[i];
-      if (x >= lo && x <= hi) atomicAdd(&ms.hist[(int)((x - lo) >> shift)], 1u);
-    }
-    __syncthreads();
-    // Find the bin where the running count from the top reaches `need`.
-    int cstar = 0, cum_above = 0, cum_at = 0;
-    if (tid < kWave) {
-      // one wave: 4 bins per lane, suffix sums from the top
-      const int b0 = 255 - 4 * tid;  // lane 0 holds bins 255..252
-      int v[4], s = 0;
-      for (int q = 0; q < 4; ++q) {
-        v[q] = (int)ms.hist[b0 - q];
-        s += v[q];
-      }
-      int incl = s;
-      for (int off = 1; off < kWave; off <<= 1) {
-        const int y = __shfl_up(incl, off);
-        if (tid >= off) incl += y;
-      }
-      int run = incl - s;  // elements in bins above this lane's group
-      int found = -1, fa = 0, fat = 0;
-      for (int q = 0; q < 4; ++q) {
-        if (found < 0 && run + v[q] >= need) {
-          found = b0 - q;
-          fa = run;
-          fat = run + v[q];
-        }
-        run += v[q];
-      }
-      const uint64_t bal = __ballot(found >= 0);
-      const int first = bal ? __ffsll((long long)bal) - 1 : 0;
-      cstar = __shfl(found, first);
-      cum_above = __shfl(fa, first);
-      cum_at = __shfl(fat, first);
-      if (tid == 0) {
-        ms.iscan[0] = cstar;
-        ms.iscan[1] = cum_above;
-        ms.iscan[2] = cum_at;
+    for (int i0 = 0; i0 < U; i0 += kBlock) {
+      const int i = i0 + tid;
+      const uint64_t x = i < U ? ms.X[i] : 0ull;
+      const bool p = x >= cut && x != 0ull;
+      const uint64_t bal = __ballot(p);
+      if (bal) {
+        int b0 = 0;
+        if (lane == 0) b0 = atomicAdd(&ms.cntS, __popcll(bal));
+        b0 = __shfl(b0, 0);
+        const int pos = b0 + __popcll(bal & lanemask_lt());
+        if (p && pos < kSortMax) ms.S[pos] = x;
       }
     }
     __syncthreads();
-    cstar = ms.iscan[0];
-    cum_above = ms.iscan[1];
-    cum_at = ms.iscan[2];
-    __syncthreads();
-    const uint64_t bin_lo = lo + ((uint64_t)cstar << shift);
-    if (above + cum_at <= kSortMax || shift == 0) {
-      cut = bin_lo;
-      break;
-    }
-    above += cum_above;
-    need -= cum_above;
-    lo = bin_lo;
-    const uint64_t width = (shift >= 64) ? ~0ull : (((uint64_t)1 << shift) - 1);
-    hi = (hi - lo > width) ? lo + width : hi;
+    nS = ms.cntS < kSortMax ? ms.cntS : kSortMax;
+    src = ms.S;
   }
-  // Gather everything >= cut, sort it, keep the first B.
-  if (tid == 0) ms.cntS = 0;
-  __syncthreads();
-  for (int i = tid; i < U; i += kBlock) {
-    const uint64_t x = ms.X[i];
-    if (x >= cut) {
-      const int p = atomicAdd(&ms.cntS, 1);
-      if (p < kSortMax) ms.S[p] = x;
-    }
-  }
-  __syncthreads();
-  const int nS = ms.cntS < kSortMax ? ms.cntS : kSortMax;
-  const int P = pow2_ceil(nS < 2 ? 2 : nS);
-  for (int i = nS + tid; i < P; i += kBlock) ms.S[i] = 0ull;
-  __syncthreads();
-  block_bitonic_desc(ms.S, P);
-  const int keep = nS < B ? nS : B;
-  for (int i = tid; i < keep; i += kBlock) ms.X[i] = ms.S[i];
-  __syncthreads();
-  return keep;
+  // X is free now: its upper part is the scatter buffer, its head the output.
+  bucket_sort_desc(src, nS, ms.X + kSortMax, ms.X, ms.cnt, ms.iscan, ms.red);
+  return nS < B ? nS : B;
 }
 
 template <class Src>
@@ -423,44 +433,134 @@ __global__ __launch_bounds__(kBlock) void merge_candidates(Src src0, int64_t n, 
   __shared__ MergeShared ms;
   __shared__ typename Src::Shared sh;
   __shared__ uint64_t sT[kMaxGrid];
-  __shared__ int sOff[kMaxGrid];
-  __shared__ int sCnt[kMaxGrid];
   const int t = blockIdx.x;
   const int tid = threadIdx.x;
   const Src src = bind_theta(src0, t);
   const size_t slot0 = (size_t)t * G;
 
-  // Offsets of the lists (G <= kMaxGrid <= kBlock), then one flat, coalesced
-  // copy of every list slot that holds an entry.
-  int c = tid < G ? (int)counts[slot0 + tid] : 0;
-  int total = 0;
-  const int off = block_exclusive_scan(c, ms.iscan, &total);
-  if (tid < G) {
-    sOff[tid] = off;
-    sCnt[tid] = c;
-    sT[tid] = bounds[slot0 + tid];
-  }
-  __syncthreads();
+  // One round trip: every list slot (G x M, empty slots hold 0) and the
+  // completeness bounds.
+  constexpr int kR = (kMergeCap + kBlock - 1) / kBlock;
   const uint64_t* lists_t = lists + slot0 * (size_t)M;
-  for (int idx = tid; idx < G * M; idx += kBlock) {
-    const int w = idx / M, i = idx - w * M;
-    if (i < sCnt[w]) ms.X[sOff[w] + i] = lists_t[idx];
+  const int GM = G * M;
+  const uint64_t Tw = tid < G ? bounds[slot0 + tid] : 0ull;
+  uint64_t v[kR];
+#pragma unroll
+  for (int r = 0; r < kR; ++r) {
+    const int idx = tid + r * kBlock;
+    v[r] = idx < GM ? lists_t[idx] : 0ull;
+  }
+  if (tid < G) sT[tid] = Tw;
+  // Exact range and count of the candidates (registers -> wave -> LDS)
+  // while the slots go to LDS and the histogram is cleared.
+  const int lane = tid & (kWave - 1), wv = tid / kWave;
+  uint64_t mx = 0, mn = ~0ull;
+  int nz = 0;
+#pragma unroll
+  for (int r = 0; r < kR; ++r) {
+    const int idx = tid + r * kBlock;
+    if (idx < GM) ms.X[idx] = v[r];
+    if (v[r] != 0ull) {
+      mx = v[r] > mx ? v[r] : mx;
+      mn = v[r] < mn ? v[r] : mn;
+      ++nz;
+    }
+  }
+  mx = wave_max_u64(mx);
+  mn = wave_min_u64(mn);
+  nz = wave_incl_scan_add(nz);
+  for (int i = tid; i < 4096; i += kBlock) ms.cnt[i] = 0u;
+  if (lane == kWave - 1) {
+    ms.wmax[wv] = mx;
+    ms.wmin[wv] = mn;
+    ms.iscan[wv] = nz;
   }
   __syncthreads();
-  int U = topb_inplace(ms, total, B);
+  int total = 0;
+#pragma unroll
+  for (int i = 0; i < kWavesPerBlock; ++i) total += ms.iscan[i];
+  int U = 0;
+  if (total > 0) {
+    uint64_t hi = 0, lo = ~0ull;
+#pragma unroll
+    for (int i = 0; i < kWavesPerBlock; ++i) {
+      hi = ms.wmax[i] > hi ? ms.wmax[i] : hi;
+      lo = ms.wmin[i] < lo ? ms.wmin[i] : lo;
+    }
+    const uint64_t diff = hi - lo;
+    const int bits = diff == 0 ? 0 : 64 - __clzll((long long)diff);
+    const int shift = bits > 12 ? bits - 12 : 0;
+#pragma unroll
+    for (int r = 0; r < kR; ++r)
+      if (v[r] != 0ull) atomicAdd(&ms.cnt[(int)((v[r] - lo) >> shift)], 1u);
+    __syncthreads();
+    // Bucket offsets from the top; the bucket where the running count
+    // reaches min(B, total) is the cut.
+    const int want = B < total ? B : total;
+    uint32_t cb[4];
+    int s4 = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      cb[q] = ms.cnt[4095 - 4 * tid - q];
+      s4 += (int)cb[q];
+    }
+    int tot = 0;
+    int run = block_exclusive_scan(s4, ms.iscan, &tot);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int b = 4095 - 4 * tid - q;
+      ms.cnt[b] = (uint32_t)run;  // bucket start, used as a cursor
+      if (run < want && run + (int)cb[q] >= want) {
+        ms.cut_bin = b;
+        ms.cut_cnt = run + (int)cb[q];
+      }
+      run += (int)cb[q];
+    }
+    __syncthreads();
+    const int cstar = ms.cut_bin, cum_at = ms.cut_cnt;
+    if (cum_at <= kSortMax) {
+#pragma unroll
+      for (int r = 0; r < kR; ++r) {
+        if (v[r] != 0ull) {
+          const int b = (int)((v[r] - lo) >> shift);
+          if (b >= cstar) ms.S[atomicAdd(&ms.cnt[b], 1u)] = v[r];
+        }
+      }
+      __syncthreads();
+      // ms.cnt[b] is now the end of bucket b, and the end of bucket b+1 is
+      // its start: rank each element inside its bucket.
+      for (int i = tid; i < cum_at; i += kBlock) {
+        const uint64_t x = ms.S[i];
+        const int b = (int)((x - lo) >> shift);
+        const int start = b == 4095 ? 0 : (int)ms.cnt[b + 1];
+        const int end = (int)ms.cnt[b];
+        int rank = 0;
+        for (int j = start; j < end; ++j) rank += ms.S[j] > x;
+        ms.X[start + rank] = x;
+      }
+      __syncthreads();
+      U = want;
+    } else {
+      U = select_top(ms, GM, B);  // X holds all G x M slots; empty slots are 0
+    }
+  }
   uint64_t tau = (U >= B) ? ms.X[B - 1] : 0ull;
 
-  // Re-read shares whose lists could miss top-B members.
+  // Re-read shares whose lists could miss top-B members (rare).
   bool staged = false;
-  for (int w = 0; w < G; ++w) {
+  const uint64_t thr0 = tau > 1ull ? tau : 1ull;
+  const int any_risk = __syncthreads_or(tid < G && sT[tid] > thr0);
+  for (int w = 0; any_risk && w < G; ++w) {
     const uint64_t thr = tau > 1ull ? tau : 1ull;
     if (!(sT[w] > thr)) continue;
     if (!staged) {
-      src.stage(sh, t);
+      typename Src::Stage st;
+      src.stage_load(st);
+      src.stage_store(sh, st, t);
       __syncthreads();
       staged = true;
     }
-    const uint64_t Tw = sT[w];
+    const uint64_t Tcut = sT[w];
     const int64_t nchunks = (n + kChunk - 1) / kChunk;
     // All chunks of share w: c = w + G * lc, lc = 0, 1, ...; a chunk per wave,
     // 4 requests per lane.
@@ -468,7 +568,7 @@ __global__ __launch_bounds__(kBlock) void merge_candidates(Src src0, int64_t n, 
       const int64_t first_c = (int64_t)w + (int64_t)G * lc0;
       if (first_c >= nchunks) break;
       if (U + kBlock * 4 > kMergeCap) {
-        U = topb_inplace(ms, U, B);
+        U = select_top(ms, U, B);
         tau = (U >= B) ? ms.X[B - 1] : 0ull;
       }
       if (tid == 0) ms.cntX = U;
@@ -477,14 +577,17 @@ __global__ __launch_bounds__(kBlock) void merge_candidates(Src src0, int64_t n, 
       const int64_t cidx = (int64_t)w + (int64_t)G * (lc0 + wv);
       const int64_t b0 = cidx < nchunks ? cidx * kChunk + (int64_t)lane * 4 : n;
       const typename Src::Raw r = src.load4(b0, n);
-      uint64_t k4[4];
-      src.keys4(r, b0, sh, k4);
+      uint32_t k4[4];
+      src.keys4(r, sh, k4);
       const uint64_t lowb = tau > 1ull ? tau : 1ull;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        if (b0 + e < n && k4[e] >= lowb && k4[e] < Tw) {
-          const int p = atomicAdd(&ms.cntX, 1);
-          ms.X[p] = k4[e];
+        if (k4[e] != 0u && b0 + e < n) {
+          const uint64_t x = make_comp(k4[e], (uint32_t)(b0 + e));
+          if (x >= lowb && x < Tcut) {
+            const int p = atomicAdd(&ms.cntX, 1);
+            ms.X[p] = x;
+          }
         }
       }
       __syncthreads();
@@ -492,9 +595,7 @@ __global__ __launch_bounds__(kBlock) void merge_candidates(Src src0, int64_t n, 
       __syncthreads();
     }
   }
-  if (staged) {
-    U = topb_inplace(ms, U, B);
-  }
+  if (staged) U = select_top(ms, U, B);
 
   // Publish.
   const int sel = U < B ? U : B;
@@ -557,7 +658,7 @@ static void carve(const SelectPlan& p, void* ws, uint64_t** lists, uint32_t** co
 hipError_t launch_step(const int32_t* len, const float* arrival, int64_t n, float now,
                        const ewsjf_queue_table* table, const ewsjf_theta* theta, int32_t n_theta,
                        const ewsjf_cost& cost, int32_t B, int32_t* tomb_len, int32_t* ids, float* top,
-                       int32_t* n_sel, void* ws, hipStream_t stream) {
+                       int32_t* n_sel, void* ws, hipStream_t stream, hipEvent_t* marks) {
   const SelectPlan p = plan_select(n, n_theta, B);
   uint64_t* lists;
   uint32_t* counts;
@@ -570,13 +671,18 @@ hipError_t launch_step(const int32_t* len, const float* arrival, int64_t n, floa
   src.theta = theta;
   src.now = now;
   src.cost = CostF{(float)cost.c0, (float)cost.c1, (float)cost.c2};
+  if (marks != nullptr && hipEventRecord(marks[0], stream) != hipSuccess) return hipErrorInvalidValue;
   hipLaunchKernelGGL(local_candidates<PoolSource>, dim3(p.G, n_theta), dim3(kBlock), 0, stream, src, n, p.G,
                      p.m, p.M, lists, counts, bounds);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (marks != nullptr && hipEventRecord(marks[1], stream) != hipSuccess) return hipErrorInvalidValue;
   hipLaunchKernelGGL(merge_candidates<PoolSource>, dim3(n_theta), dim3(kBlock), 0, stream, src, n, p.G, p.M,
                      B, lists, counts, bounds, ids, top, n_sel, tomb_len);
-  return hipGetLastError();
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (marks != nullptr && hipEventRecord(marks[2], stream) != hipSuccess) return hipErrorInvalidValue;
+  return hipSuccess;
 }
 
 hipError_t launch_select(const float* score, int64_t n, int32_t n_theta, int32_t B, int32_t* ids, float* top,
