@@ -12,7 +12,8 @@ sits in HBM; `--rotate` distinct copies (10 x 32 MiB by default, more than
 the 256 MiB Infinity Cache) are stepped in turn so each step reads HBM.
 Steps run from a captured HIP graph (chunks of up to 50 steps) so host
 launch cost does not bound the loop; an eager pass with per-kernel events
-gives the streaming kernel's own duration for the roofline figure.
+gives each kernel's own duration (start/end events bound to the kernel's
+dispatch) for the roofline figure.
 
 Prints one JSON line.  Flags: --gpus (only 1 is supported), --steps,
 --warmup, --rotate, --no-cpu (skip the oracle baseline).
@@ -109,6 +110,8 @@ def main() -> int:
     ap.add_argument("--rotate", type=int, default=10)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="run one device copy of this many MiB first (counter calibration under rocprofv3)")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -127,6 +130,17 @@ def main() -> int:
     torch.cuda.set_device(0)
     dev = torch.device("cuda:0")
     hip = Hip()
+
+    if args.copy_probe_mib > 0:
+        # A plain copy of known size: its FETCH_SIZE / WRITE_SIZE counters
+        # calibrate the streaming kernel's counter readings.
+        a = torch.empty(args.copy_probe_mib << 20, dtype=torch.uint8, device=dev)
+        b = torch.empty_like(a)
+        a.fill_(1)
+        torch.cuda.synchronize()
+        b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
 
     pool = W.config(2)
     n, B = pool.n, pool.B
@@ -179,20 +193,24 @@ def main() -> int:
             raise L.EwsjfError(st, "ewsjf_step")
 
     # ---- eager pass with per-kernel events (streaming kernel duration) -----
+    # A spin kernel holds the stream until every step of the pass is
+    # enqueued, so the event intervals see device execution only, not host
+    # launch latency.
     s_eager = vp(stream.cuda_stream)
     for i in range(args.warmup):
         step(i, s_eager)
     torch.cuda.synchronize()
     K = args.steps
-    marks = [(hip.event(), hip.event(), hip.event()) for _ in range(K)]
-    ev_arr = [(vp * 3)(*m) for m in marks]
+    marks = [(hip.event(), hip.event(), hip.event(), hip.event()) for _ in range(K)]
+    ev_arr = [(vp * 4)(*m) for m in marks]
+    torch.cuda._sleep(int(2.4e9 * (0.02 + 3e-5 * K)))  # ~20 ms + 30 us per step of GPU clock cycles
     rt.hipEventRecord(e0, s_eager)
     for i in range(K):
         step(i, s_eager, ev_arr[i])
     rt.hipEventRecord(e1, s_eager)
     eager_ms = hip.elapsed_ms(e0, e1) / K
     k1 = [hip.elapsed_ms(m[0], m[1]) for m in marks]
-    k2 = [hip.elapsed_ms(m[1], m[2]) for m in marks]
+    k2 = [hip.elapsed_ms(m[2], m[3]) for m in marks]
     k1_ms = float(np.mean(k1))
     k2_ms = float(np.mean(k2))
     eager_ids = ids.clone()

@@ -199,9 +199,10 @@ ewsjf_status ewsjf_step(int32_t* len, const float* arrival, int64_t n, float now
                         int32_t flags, int32_t* ids, float* top, int32_t* n_sel, void* ws, size_t ws_bytes,
                         hipStream_t stream);
 
-/* ewsjf_step that also records three caller-created events on `stream`:
- * marks[0] before the streaming (route + score + local candidate) kernel,
- * marks[1] between it and the merge kernel, marks[2] after the merge.  For
+/* ewsjf_step that also times its two kernels with four caller-created events
+ * (hipEventCreate, timing enabled): marks[0]/marks[1] take the start/end of
+ * the streaming kernel (routing, scoring and per-workgroup candidates),
+ * marks[2]/marks[3] the start/end of the merge kernel (exact top-B).  For
  * per-phase timing by a monitor; marks == NULL behaves as ewsjf_step. */
 ewsjf_status ewsjf_step_timed(int32_t* len, const float* arrival, int64_t n, float now, const void* table,
                               const ewsjf_theta* theta, int32_t n_theta, const ewsjf_cost* cost, int32_t B,

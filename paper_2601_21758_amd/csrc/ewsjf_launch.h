@@ -21,8 +21,8 @@ struct SelectPlan {
 
 SelectPlan plan_select(int64_t n, int32_t n_theta, int32_t B);
 
-// marks (optional, may be NULL): three events recorded before the streaming
-// kernel, between the two kernels and after the merge kernel.
+// marks (optional, may be NULL): four events taking the start and end
+// timestamps of the streaming kernel and of the merge kernel.
 hipError_t launch_step(const int32_t* len, const float* arrival, int64_t n, float now,
                        const ewsjf_queue_table* table, const ewsjf_theta* theta, int32_t n_theta,
                        const ewsjf_cost& cost, int32_t B, int32_t* tomb_len, int32_t* ids, float* top,

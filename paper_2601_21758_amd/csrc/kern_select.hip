@@ -20,6 +20,7 @@
 //
 // The composite key (score key << 32 | ~id) is unique per request, so the
 // order (score desc, id asc) is total and the admitted set is unique.
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include "ewsjf_device.h"
@@ -103,6 +104,14 @@ struct PoolSource {
     return r;
   }
 
+  // All four requests in range: one 16-byte streaming load per array.
+  __device__ __forceinline__ Raw load4_full(int64_t base) const {
+    Raw r;
+    r.l = __builtin_nontemporal_load(reinterpret_cast<const i32x4*>(len + base));
+    r.a = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(arrival + base));
+    return r;
+  }
+
   __device__ __forceinline__ uint32_t key1(int b, float a, const Shared& sh) const {
     const int L = sh.L;
     const int bc = b < 0 ? 0 : (b < L ? b : L);
@@ -146,6 +155,13 @@ struct ScoreSource {
       if (base + 1 < nn) r.s.y = row_[base + 1];
       if (base + 2 < nn) r.s.z = row_[base + 2];
     }
+    return r;
+  }
+
+  __device__ __forceinline__ Raw load4_full(int64_t base) const {
+    Raw r;
+    if (vec_) r.s = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(row_ + base));
+    else r.s = f32x4{row_[base + 0], row_[base + 1], row_[base + 2], row_[base + 3]};
     return r;
   }
 
@@ -195,16 +211,20 @@ struct ListShared {
 
 // Chunk c of workgroup w at local index lc is c = w + G * lc.  Wave v of the
 // block takes local indices lc = v + kWavesPerBlock * (j + kChunksPerPass * pass).
+// The chunk index is wave-uniform, so full chunks take an unguarded path.
 template <class Src>
 __device__ __forceinline__ void load_pass(const Src& src, int64_t n, int64_t nchunks, int G, int pass,
-                                          typename Src::Raw raw[kChunksPerPass], int64_t base[kChunksPerPass]) {
-  const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
+                                          typename Src::Raw raw[kChunksPerPass], int64_t chunk[kChunksPerPass]) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wv = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
+  const int64_t full = n / kChunk;
 #pragma unroll
   for (int j = 0; j < kChunksPerPass; ++j) {
     const int64_t lc = (int64_t)wv + kWavesPerBlock * ((int64_t)j + (int64_t)kChunksPerPass * pass);
     const int64_t c = (int64_t)blockIdx.x + (int64_t)G * lc;
-    base[j] = c < nchunks ? c * kChunk + (int64_t)lane * 4 : n;  // n = past the end
-    raw[j] = src.load4(base[j], n);
+    chunk[j] = c;
+    if (c < full) raw[j] = src.load4_full(c * kChunk + (int64_t)lane * 4);
+    else raw[j] = src.load4(c < nchunks ? c * kChunk + (int64_t)lane * 4 : n, n);
   }
 }
 
@@ -228,8 +248,8 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
   typename Src::Stage st;
   src.stage_load(st);
   typename Src::Raw raw[kChunksPerPass];
-  int64_t base[kChunksPerPass];
-  if (passes > 0) load_pass(src, n, nchunks, G, 0, raw, base);
+  int64_t chunk[kChunksPerPass];
+  if (passes > 0) load_pass(src, n, nchunks, G, 0, raw, chunk);
   src.stage_store(sh, st, t);
   if (threadIdx.x == 0) {
     ls.cnt = 0;
@@ -244,14 +264,20 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
   // entries below it are dropped at the end.
   uint32_t my_bar = 0;  // this wave's largest bar over the passes
   for (int pass = 0; pass < passes; ++pass) {
-    if (pass > 0) load_pass(src, n, nchunks, G, pass, raw, base);
+    if (pass > 0) load_pass(src, n, nchunks, G, pass, raw, chunk);
+    // The bar comes from the first kChunksPerPass-1 chunks, so it is ready
+    // while the last chunk is still in flight; every element (the last
+    // chunk's too) at or above it is emitted.
     uint32_t key[kElemsPerLane];
 #pragma unroll
-    for (int j = 0; j < kChunksPerPass; ++j) src.keys4(raw[j], sh, key + 4 * j);
+    for (int j = 0; j < kChunksPerPass - 1; ++j) src.keys4(raw[j], sh, key + 4 * j);
     uint32_t lmax = 0;
 #pragma unroll
-    for (int e = 0; e < kElemsPerLane; ++e) lmax = key[e] > lmax ? key[e] : lmax;
+    for (int e = 0; e < 4 * (kChunksPerPass - 1); ++e) lmax = key[e] > lmax ? key[e] : lmax;
     const uint32_t bar = wave_mth_largest_u32(lmax, m);
+    src.keys4(raw[kChunksPerPass - 1], sh, key + 4 * (kChunksPerPass - 1));
+#pragma unroll
+    for (int e = 4 * (kChunksPerPass - 1); e < kElemsPerLane; ++e) lmax = key[e] > lmax ? key[e] : lmax;
     const uint32_t wbar = bar > my_bar ? bar : my_bar;
     my_bar = wbar;
     if (__ballot(lmax >= wbar && lmax != 0u)) {
@@ -265,7 +291,8 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
           b0 = __shfl(b0, 0);
           const int pos = b0 + __popcll(bal & lanemask_lt());
           if (p) {
-            if (pos < kListCap) ls.list[pos] = make_comp(key[e], (uint32_t)(base[e / 4] + (e & 3)));
+            if (pos < kListCap)
+              ls.list[pos] = make_comp(key[e], (uint32_t)(chunk[e / 4] * kChunk + lane * 4 + (e & 3)));
             else ls.ovf = 1;
           }
         }
@@ -671,18 +698,24 @@ hipError_t launch_step(const int32_t* len, const float* arrival, int64_t n, floa
   src.theta = theta;
   src.now = now;
   src.cost = CostF{(float)cost.c0, (float)cost.c1, (float)cost.c2};
-  if (marks != nullptr && hipEventRecord(marks[0], stream) != hipSuccess) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(local_candidates<PoolSource>, dim3(p.G, n_theta), dim3(kBlock), 0, stream, src, n, p.G,
-                     p.m, p.M, lists, counts, bounds);
+  if (marks == nullptr) {
+    hipLaunchKernelGGL(local_candidates<PoolSource>, dim3(p.G, n_theta), dim3(kBlock), 0, stream, src, n, p.G,
+                       p.m, p.M, lists, counts, bounds);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(merge_candidates<PoolSource>, dim3(n_theta), dim3(kBlock), 0, stream, src, n, p.G, p.M,
+                       B, lists, counts, bounds, ids, top, n_sel, tomb_len);
+    return hipGetLastError();
+  }
+  // The events take the start and end timestamps of each kernel's own
+  // dispatch.
+  hipExtLaunchKernelGGL(local_candidates<PoolSource>, dim3(p.G, n_theta), dim3(kBlock), 0, stream, marks[0],
+                        marks[1], 0, src, n, p.G, p.m, p.M, lists, counts, bounds);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (marks != nullptr && hipEventRecord(marks[1], stream) != hipSuccess) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(merge_candidates<PoolSource>, dim3(n_theta), dim3(kBlock), 0, stream, src, n, p.G, p.M,
-                     B, lists, counts, bounds, ids, top, n_sel, tomb_len);
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  if (marks != nullptr && hipEventRecord(marks[2], stream) != hipSuccess) return hipErrorInvalidValue;
-  return hipSuccess;
+  hipExtLaunchKernelGGL(merge_candidates<PoolSource>, dim3(n_theta), dim3(kBlock), 0, stream, marks[2], marks[3],
+                        0, src, n, p.G, p.M, B, lists, counts, bounds, ids, top, n_sel, tomb_len);
+  return hipGetLastError();
 }
 
 hipError_t launch_select(const float* score, int64_t n, int32_t n_theta, int32_t B, int32_t* ids, float* top,
