@@ -27,6 +27,22 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ i32x4 load_i32x4(const int32_t* p) { return *reinterpret_cast<const i32x4*>(p); }
 __device__ __forceinline__ f32x4 load_f32x4(const float* p) { return *reinterpret_cast<const f32x4*>(p); }
 
+// Buffer-resource loads of one 256-element chunk: the resource covers only the
+// chunk's in-range part, so lanes past the end of the array read zeros
+// instead of faulting, and every chunk costs exactly one load instruction
+// per array (no branches, so the wait counters track each chunk).
+constexpr int kBufferWord3 = 0x00020000;  // raw buffer, 32-bit data (gfx9 family)
+constexpr int kCachePolicyNT = 2;         // streaming (non-temporal) hint
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t chunk_rsrc(const void* chunk_base, int64_t remaining_elems) {
+  const int64_t r = remaining_elems < 0 ? 0 : (remaining_elems > kChunk ? kChunk : remaining_elems);
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(chunk_base), (short)0, (int)(r * 4), kBufferWord3);
+}
+
+__device__ __forceinline__ i32x4 chunk_load_i32x4(__amdgpu_buffer_rsrc_t rs, int lane) {
+  return __builtin_amdgcn_raw_buffer_load_b128(rs, lane * 16, 0, kCachePolicyNT);
+}
+
 // Per-queue scoring constants derived from one parameter vector:
 // w_base, w_urg, w_fair * ln 2 (so the fairness term uses log2), and q + 1.
 struct QParams {

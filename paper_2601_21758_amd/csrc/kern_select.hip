@@ -56,30 +56,34 @@ struct PoolSource {
   };
   struct Stage {
     i32x4 v[kLutPerThread];
+    double mean;
   };
 
+  // Branch-free on purpose: every load is issued unconditionally (the lookup
+  // table and the mean array are read whole, indices clamped into them), so
+  // the LDS stores in stage_store wait only for these loads and not for the
+  // pool loads issued after them.
   __device__ __forceinline__ void stage_load(Stage& st) const {
-    const int nvec = (table->max_len + 1 + 15) / 16;
     const i32x4* src = reinterpret_cast<const i32x4*>(table->lut);
 #pragma unroll
     for (int r = 0; r < kLutPerThread; ++r) {
       const int i = threadIdx.x + r * kBlock;
-      st.v[r] = i < nvec ? src[i] : i32x4{0, 0, 0, 0};
+      st.v[r] = src[i < kLutVecs ? i : kLutVecs - 1];
     }
+    st.mean = table->mean[threadIdx.x & (EWSJF_MAX_QUEUES - 1)];
   }
 
   __device__ __forceinline__ void stage_store(Shared& sh, const Stage& st, int t) const {
-    const int nvec = (table->max_len + 1 + 15) / 16;
     i32x4* dst = reinterpret_cast<i32x4*>(sh.lut);
 #pragma unroll
     for (int r = 0; r < kLutPerThread; ++r) {
       const int i = threadIdx.x + r * kBlock;
-      if (i < nvec) dst[i] = st.v[r];
+      if (r + 1 < kLutPerThread || i < kLutVecs) dst[i] = st.v[r];
     }
     const int k = table->k;
     if ((int)threadIdx.x < k) {
       const int q = threadIdx.x;
-      const double m = table->mean[q];
+      const double m = st.mean;
       const ewsjf_theta th = theta[t];
       const double wb = (double)th.a_base * m + (double)th.b_base;
       const double wu = (double)th.a_urg * m + (double)th.b_urg;
@@ -104,11 +108,13 @@ struct PoolSource {
     return r;
   }
 
-  // All four requests in range: one 16-byte streaming load per array.
-  __device__ __forceinline__ Raw load4_full(int64_t base) const {
+  // The 4 requests of this lane in chunk c (zeros past the end of the pool).
+  __device__ __forceinline__ Raw load_chunk(int64_t c, int64_t n, int lane) const {
+    const int64_t first = c * kChunk;
     Raw r;
-    r.l = __builtin_nontemporal_load(reinterpret_cast<const i32x4*>(len + base));
-    r.a = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(arrival + base));
+    r.l = chunk_load_i32x4(chunk_rsrc(len + first, n - first), lane);
+    const i32x4 a = chunk_load_i32x4(chunk_rsrc(arrival + first, n - first), lane);
+    r.a = __builtin_bit_cast(f32x4, a);
     return r;
   }
 
@@ -158,10 +164,18 @@ struct ScoreSource {
     return r;
   }
 
-  __device__ __forceinline__ Raw load4_full(int64_t base) const {
+  // A chunk beyond the row's end reads zeros, which are marked empty below.
+  __device__ __forceinline__ Raw load_chunk(int64_t c, int64_t nn, int lane) const {
+    const int64_t first = c * kChunk;
     Raw r;
-    if (vec_) r.s = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(row_ + base));
-    else r.s = f32x4{row_[base + 0], row_[base + 1], row_[base + 2], row_[base + 3]};
+    const i32x4 v = chunk_load_i32x4(chunk_rsrc(row_ + first, nn - first), lane);
+    r.s = __builtin_bit_cast(f32x4, v);
+    const int64_t i0 = first + 4 * lane;
+    const float nan = __builtin_nanf("");
+    if (i0 + 0 >= nn) r.s.x = nan;
+    if (i0 + 1 >= nn) r.s.y = nan;
+    if (i0 + 2 >= nn) r.s.z = nan;
+    if (i0 + 3 >= nn) r.s.w = nan;
     return r;
   }
 
@@ -217,14 +231,12 @@ __device__ __forceinline__ void load_pass(const Src& src, int64_t n, int64_t nch
                                           typename Src::Raw raw[kChunksPerPass], int64_t chunk[kChunksPerPass]) {
   const int lane = threadIdx.x & (kWave - 1);
   const int wv = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
-  const int64_t full = n / kChunk;
 #pragma unroll
   for (int j = 0; j < kChunksPerPass; ++j) {
     const int64_t lc = (int64_t)wv + kWavesPerBlock * ((int64_t)j + (int64_t)kChunksPerPass * pass);
     const int64_t c = (int64_t)blockIdx.x + (int64_t)G * lc;
     chunk[j] = c;
-    if (c < full) raw[j] = src.load4_full(c * kChunk + (int64_t)lane * 4);
-    else raw[j] = src.load4(c < nchunks ? c * kChunk + (int64_t)lane * 4 : n, n);
+    raw[j] = src.load_chunk(c, n, lane);
   }
 }
 
@@ -249,7 +261,9 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
   src.stage_load(st);
   typename Src::Raw raw[kChunksPerPass];
   int64_t chunk[kChunksPerPass];
-  if (passes > 0) load_pass(src, n, nchunks, G, 0, raw, chunk);
+  // Unconditional: chunks past the end of the pool read as empty, and a
+  // branch here would make the LDS stores below wait for every load.
+  load_pass(src, n, nchunks, G, 0, raw, chunk);
   src.stage_store(sh, st, t);
   if (threadIdx.x == 0) {
     ls.cnt = 0;
@@ -280,21 +294,27 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
     for (int e = 4 * (kChunksPerPass - 1); e < kElemsPerLane; ++e) lmax = key[e] > lmax ? key[e] : lmax;
     const uint32_t wbar = bar > my_bar ? bar : my_bar;
     my_bar = wbar;
-    if (__ballot(lmax >= wbar && lmax != 0u)) {
+    // One LDS atomic per wave: each lane counts its qualifying elements, a
+    // wave prefix sum gives every lane its offset, lane 63 reserves the
+    // wave's total.
+    uint32_t mask = 0;
+#pragma unroll
+    for (int e = 0; e < kElemsPerLane; ++e) mask |= (key[e] != 0u && key[e] >= wbar) ? (1u << e) : 0u;
+    const int mine = __builtin_popcount(mask);
+    const int incl = wave_incl_scan_add(mine);
+    int wbase = 0;
+    if (lane == kWave - 1 && incl > 0) wbase = atomicAdd(&ls.cnt, incl);
+    wbase = __shfl(wbase, kWave - 1);
+    if (mask) {
+      int pos = wbase + incl - mine;
 #pragma unroll
       for (int e = 0; e < kElemsPerLane; ++e) {
-        const bool p = key[e] != 0u && key[e] >= wbar;
-        const uint64_t bal = __ballot(p);
-        if (bal) {
-          int b0 = 0;
-          if (lane == 0) b0 = atomicAdd(&ls.cnt, __popcll(bal));
-          b0 = __shfl(b0, 0);
-          const int pos = b0 + __popcll(bal & lanemask_lt());
-          if (p) {
-            if (pos < kListCap)
-              ls.list[pos] = make_comp(key[e], (uint32_t)(chunk[e / 4] * kChunk + lane * 4 + (e & 3)));
-            else ls.ovf = 1;
-          }
+        if (mask & (1u << e)) {
+          if (pos < kListCap)
+            ls.list[pos] = make_comp(key[e], (uint32_t)(chunk[e / 4] * kChunk + lane * 4 + (e & 3)));
+          else
+            ls.ovf = 1;
+          ++pos;
         }
       }
     }
