@@ -16,6 +16,7 @@ constexpr int kChunksPerPass = 4;            // chunks a wave holds in registers
 constexpr int kElemsPerLane = 4 * kChunksPerPass;
 constexpr int kMaxGrid = 256;                // streaming workgroups (one per CU)
 constexpr int kListCap = 1024;               // per-workgroup candidate list in LDS
+constexpr int kWaveCap = kListCap / (kBlock / kWave);  // one region of the list per wave
 constexpr int kMergeCap = 9088;              // merge kernel candidate capacity (LDS, >= 2 * kSortMax)
 constexpr int kSortMax = 4096;               // largest bitonic sort in LDS
 constexpr int kLutBytes = EWSJF_MAX_LEN + 16;
@@ -43,11 +44,23 @@ __device__ __forceinline__ i32x4 chunk_load_i32x4(__amdgpu_buffer_rsrc_t rs, int
   return __builtin_amdgcn_raw_buffer_load_b128(rs, lane * 16, 0, kCachePolicyNT);
 }
 
-// Per-queue scoring constants derived from one parameter vector:
-// w_base, w_urg, w_fair * ln 2 (so the fairness term uses log2), and q + 1.
-struct QParams {
-  float wb, wu, wf2, qn;
+// Per-queue scoring constants derived from one parameter vector, each already
+// multiplied by the queue's density factor q + 1: (q+1) w_base, (q+1) w_urg
+// and (q+1) w_fair ln 2 (so the fairness term takes a log2).  16 bytes, so a
+// lookup is one LDS read.
+struct alignas(16) QParams {
+  float wb, wu, wf2, pad;
 };
+
+// The weights are affine in the queue's mean length (Section 4.1); they and the
+// (q + 1) factor are formed in double and rounded once.
+__device__ __forceinline__ QParams make_qparams(const ewsjf_theta& th, double mean, int q) {
+  const double f = (double)(q + 1);
+  const double wb = ((double)th.a_base * mean + (double)th.b_base) * f;
+  const double wu = ((double)th.a_urg * mean + (double)th.b_urg) * f;
+  const double wf = ((double)th.a_fair * mean + (double)th.b_fair) * f * 0.69314718055994530942;
+  return QParams{(float)wb, (float)wu, (float)wf, 0.0f};
+}
 
 // ---------------------------------------------------------------------------
 // Order-preserving keys.  A float score maps to a 32-bit unsigned key whose
@@ -100,19 +113,6 @@ __device__ __forceinline__ int wave_sum_i32(int x) {
 __device__ __forceinline__ uint64_t lanemask_lt() {
   const int lane = threadIdx.x & (kWave - 1);
   return lane == 0 ? 0ull : (~0ull >> (64 - lane));
-}
-
-// The m-th largest of the 64 lane values (distinct values; ties removed
-// together), or 0 when fewer than m distinct non-zero values exist.
-__device__ __forceinline__ uint32_t wave_mth_largest_u32(uint32_t x, int m) {
-  uint32_t t = 0;
-  for (int r = 0; r < m; ++r) {
-    const uint32_t mx = wave_max_u32(x);
-    t = mx;
-    if (mx == 0u) break;
-    if (x == mx) x = 0u;
-  }
-  return t;
 }
 
 // Block-wide reductions over kBlock threads using a 16-entry LDS scratch.
@@ -195,6 +195,36 @@ __device__ __forceinline__ uint32_t xor_lane_u32(uint32_t x) {
   } else {
     return (uint32_t)__shfl_xor(v, 32);
   }
+}
+
+// Bar of a wave over its lane values x (0 = no element): the lanes form
+// 2^lg groups of 64 >> lg consecutive lanes; the bar is the smallest group
+// maximum over the groups holding an element (0 when no lane holds one).  At
+// least one element per such group is >= the bar.  Six butterfly max steps:
+// the steps inside a group take the group maximum, then the values are
+// negated (so 0 stays 0 and the smallest nonzero maximum becomes the largest)
+// and the remaining steps take the maximum across groups.
+__device__ __forceinline__ uint32_t wave_group_bar(uint32_t x, int lg) {
+  const int s = 6 - lg;  // steps that stay inside a group
+  if (s == 0) x = 0u - x;
+  x = max(x, xor_lane_u32<1>(x));
+  if (s == 1) x = 0u - x;
+  x = max(x, xor_lane_u32<2>(x));
+  if (s == 2) x = 0u - x;
+  x = max(x, xor_lane_u32<4>(x));
+  if (s == 3) x = 0u - x;
+  x = max(x, xor_lane_u32<8>(x));
+  if (s == 4) x = 0u - x;
+  x = max(x, xor_lane_u32<16>(x));
+  if (s == 5) x = 0u - x;
+  x = max(x, xor_lane_u32<32>(x));
+  if (s == 6) x = 0u - x;
+  return 0u - x;
+}
+
+// Number of lanes below this one whose bit is set in the wave mask sm.
+__device__ __forceinline__ int lanes_below(uint64_t sm) {
+  return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(sm >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)sm, 0u));
 }
 
 template <int J>
@@ -473,7 +503,7 @@ __device__ __forceinline__ float phi_f32(int b, float arrival, float now, const 
   const float C = __builtin_fmaf(__builtin_fmaf(c.c2, fb, c.c1), fb, c.c0);
   const float lg = __builtin_amdgcn_logf(bp1);  // log2(b + 1)
   const float num = __builtin_fmaf(p.wf2 * lg, C, __builtin_fmaf(p.wb, C, p.wu * W));
-  return p.qn * num * __builtin_amdgcn_rcpf(bp1 * C);
+  return num * __builtin_amdgcn_rcpf(bp1 * C);
 }
 
 // Order-preserving key of a score computed in registers: NaN -> -inf,
@@ -496,18 +526,7 @@ __device__ inline void stage_policy(const ewsjf_queue_table* tab, const ewsjf_th
   const int nvec = (L + 1 + 15) / 16;
   for (int i = threadIdx.x; i < nvec; i += blockDim.x) dst[i] = src[i];
   if (theta != nullptr) {
-    for (int q = threadIdx.x; q < k; q += blockDim.x) {
-      const double m = tab->mean[q];
-      const double wb = (double)theta->a_base * m + (double)theta->b_base;
-      const double wu = (double)theta->a_urg * m + (double)theta->b_urg;
-      const double wf = (double)theta->a_fair * m + (double)theta->b_fair;
-      QParams p;
-      p.wb = (float)wb;
-      p.wu = (float)wu;
-      p.wf2 = (float)(wf * 0.69314718055994530942);
-      p.qn = (float)(q + 1);
-      qp[q] = p;
-    }
+    for (int q = threadIdx.x; q < k; q += blockDim.x) qp[q] = make_qparams(*theta, tab->mean[q], q);
   }
 }
 

@@ -13,7 +13,7 @@ namespace ewsjf {
 // Launch geometry and workspace layout of the two-kernel top-B selection.
 struct SelectPlan {
   int G = 1;        // streaming workgroups
-  int m = 4;        // per-wave order statistic used as the candidate bar
+  int lg = 2;       // log2 of the lane groups per wave that set the candidate bar
   int M = 16;       // list entries kept per workgroup
   int n_theta = 1;
   size_t lists_bytes = 0, counts_bytes = 0, bounds_bytes = 0, ws_bytes = 0;

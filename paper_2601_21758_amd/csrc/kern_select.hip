@@ -57,13 +57,15 @@ struct PoolSource {
   struct Stage {
     i32x4 v[kLutPerThread];
     double mean;
+    ewsjf_theta th;
+    int k, L;
   };
 
   // Branch-free on purpose: every load is issued unconditionally (the lookup
-  // table and the mean array are read whole, indices clamped into them), so
-  // the LDS stores in stage_store wait only for these loads and not for the
-  // pool loads issued after them.
-  __device__ __forceinline__ void stage_load(Stage& st) const {
+  // table and the mean array are read whole, indices clamped into them), and
+  // the table's scalars are read here too, so the LDS stores in stage_store
+  // wait only for these loads and never for the pool loads issued after them.
+  __device__ __forceinline__ void stage_load(Stage& st, int t) const {
     const i32x4* src = reinterpret_cast<const i32x4*>(table->lut);
 #pragma unroll
     for (int r = 0; r < kLutPerThread; ++r) {
@@ -71,26 +73,20 @@ struct PoolSource {
       st.v[r] = src[i < kLutVecs ? i : kLutVecs - 1];
     }
     st.mean = table->mean[threadIdx.x & (EWSJF_MAX_QUEUES - 1)];
+    st.th = theta[t];
+    st.k = table->k;
+    st.L = table->max_len;
   }
 
-  __device__ __forceinline__ void stage_store(Shared& sh, const Stage& st, int t) const {
+  __device__ __forceinline__ void stage_store(Shared& sh, const Stage& st) const {
     i32x4* dst = reinterpret_cast<i32x4*>(sh.lut);
 #pragma unroll
     for (int r = 0; r < kLutPerThread; ++r) {
       const int i = threadIdx.x + r * kBlock;
       if (r + 1 < kLutPerThread || i < kLutVecs) dst[i] = st.v[r];
     }
-    const int k = table->k;
-    if ((int)threadIdx.x < k) {
-      const int q = threadIdx.x;
-      const double m = st.mean;
-      const ewsjf_theta th = theta[t];
-      const double wb = (double)th.a_base * m + (double)th.b_base;
-      const double wu = (double)th.a_urg * m + (double)th.b_urg;
-      const double wf = (double)th.a_fair * m + (double)th.b_fair;
-      sh.qp[q] = QParams{(float)wb, (float)wu, (float)(wf * 0.69314718055994530942), (float)(q + 1)};
-    }
-    if (threadIdx.x == 0) sh.L = table->max_len;
+    if ((int)threadIdx.x < st.k) sh.qp[threadIdx.x] = make_qparams(st.th, st.mean, threadIdx.x);
+    if (threadIdx.x == 0) sh.L = st.L;
   }
 
   __device__ __forceinline__ Raw load4(int64_t base, int64_t n) const {
@@ -119,8 +115,7 @@ struct PoolSource {
   }
 
   __device__ __forceinline__ uint32_t key1(int b, float a, const Shared& sh) const {
-    const int L = sh.L;
-    const int bc = b < 0 ? 0 : (b < L ? b : L);
+    const int bc = min(max(b, 0), sh.L);
     const float phi = phi_f32(b, a, now, sh.qp[sh.lut[bc]], cost);
     return b > 0 ? ukey_fast(phi) : 0u;
   }
@@ -145,8 +140,8 @@ struct ScoreSource {
   };
   struct Stage {};
 
-  __device__ __forceinline__ void stage_load(Stage&) const {}
-  __device__ __forceinline__ void stage_store(Shared&, const Stage&, int) const {}
+  __device__ __forceinline__ void stage_load(Stage&, int) const {}
+  __device__ __forceinline__ void stage_store(Shared&, const Stage&) const {}
 
   __device__ __forceinline__ Raw load4(int64_t base, int64_t nn) const {
     Raw r;
@@ -212,36 +207,39 @@ __device__ __forceinline__ ScoreSource bind_theta<ScoreSource>(const ScoreSource
 // Per-workgroup candidate list.
 // ---------------------------------------------------------------------------
 struct ListShared {
-  uint64_t list[kListCap];
+  uint64_t list[kListCap];  // kWavesPerBlock regions of kWaveCap entries
   uint64_t list2[kListCap];
   uint32_t hist[256];
   uint64_t red[kWavesPerBlock];
   int iscan[kWavesPerBlock];
   uint32_t bar[kWavesPerBlock];
-  int cnt;
+  int wcnt[kWavesPerBlock];
   int ovf;
   int nout;
 };
+static_assert(kWaveCap == kWave, "the final filter maps one region slot to one lane");
 
 // Chunk c of workgroup w at local index lc is c = w + G * lc.  Wave v of the
 // block takes local indices lc = v + kWavesPerBlock * (j + kChunksPerPass * pass).
-// The chunk index is wave-uniform, so full chunks take an unguarded path.
-template <class Src>
-__device__ __forceinline__ void load_pass(const Src& src, int64_t n, int64_t nchunks, int G, int pass,
-                                          typename Src::Raw raw[kChunksPerPass], int64_t chunk[kChunksPerPass]) {
-  const int lane = threadIdx.x & (kWave - 1);
+// Chunks past the end of the pool read as empty (bounded buffer loads), so
+// the loads are issued without a branch.
+__device__ __forceinline__ int64_t chunk_of(int G, int pass, int j) {
   const int wv = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
-#pragma unroll
-  for (int j = 0; j < kChunksPerPass; ++j) {
-    const int64_t lc = (int64_t)wv + kWavesPerBlock * ((int64_t)j + (int64_t)kChunksPerPass * pass);
-    const int64_t c = (int64_t)blockIdx.x + (int64_t)G * lc;
-    chunk[j] = c;
-    raw[j] = src.load_chunk(c, n, lane);
-  }
+  const int64_t lc = (int64_t)wv + kWavesPerBlock * ((int64_t)j + (int64_t)kChunksPerPass * pass);
+  return (int64_t)blockIdx.x + (int64_t)G * lc;
 }
 
 template <class Src>
-__global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, int G, int m, int M,
+__device__ __forceinline__ void load_one(const Src& src, int64_t n, int G, int pass, int j, typename Src::Raw& raw) {
+  raw = src.load_chunk(chunk_of(G, pass, j), n, threadIdx.x & (kWave - 1));
+}
+
+// Keeps the compiler from moving memory operations or arithmetic across this
+// point, so the load/score interleaving below stays as written.
+__device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
+
+template <class Src>
+__global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, int G, int lg, int M,
                                                            uint64_t* __restrict__ lists,
                                                            uint32_t* __restrict__ counts,
                                                            uint64_t* __restrict__ bounds) {
@@ -254,90 +252,104 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
   const int64_t my_chunks = nchunks > blockIdx.x ? (nchunks - blockIdx.x + G - 1) / G : 0;
   const int passes = (int)((my_chunks + kWavesPerBlock * kChunksPerPass - 1) / (kWavesPerBlock * kChunksPerPass));
 
-  // Table loads first, then the pool loads, then the table goes to LDS: the
-  // LDS stores wait only for the (older) table loads, so scoring of the
-  // first chunks starts while the rest of the pool is still streaming in.
+  // A wave stalls at a vector load while the compute unit's memory pipeline
+  // is full, so a wave that issued all of its loads before scoring would
+  // score only once nearly the whole stream had arrived.  Instead each wave
+  // keeps two chunks in flight and scores one chunk per chunk it issues.
+  // The tables go first; the barrier before scoring then waits only for
+  // them and for the first two chunk loads of every wave.
   typename Src::Stage st;
-  src.stage_load(st);
+  src.stage_load(st, t);
+  // The compute unit serves a workgroup's loads roughly in issue order; this
+  // barrier (which does not wait for the loads) puts every wave's table loads
+  // ahead of every wave's pool loads, so the table lands after one latency.
+  __builtin_amdgcn_s_barrier();
   typename Src::Raw raw[kChunksPerPass];
-  int64_t chunk[kChunksPerPass];
-  // Unconditional: chunks past the end of the pool read as empty, and a
-  // branch here would make the LDS stores below wait for every load.
-  load_pass(src, n, nchunks, G, 0, raw, chunk);
-  src.stage_store(sh, st, t);
+  load_one(src, n, G, 0, 0, raw[0]);
+  load_one(src, n, G, 0, 1, raw[1]);
+  src.stage_store(sh, st);
   if (threadIdx.x == 0) {
-    ls.cnt = 0;
     ls.ovf = 0;
     ls.nout = 0;
   }
   __syncthreads();
 
-  // Each wave emits, as soon as its own keys are ready, every element whose
-  // key is >= its bar (the m-th largest lane maximum of the wave).  The
-  // workgroup's completeness bound is the largest bar of any wave and pass;
-  // entries below it are dropped at the end.
+  // Each wave writes every element whose key is >= its bar into its own
+  // region of the list.  The bar (wave_group_bar over the lane maxima of the
+  // first three chunks) leaves at least 2^lg elements of the wave at or
+  // above it.  The workgroup's completeness bound is the largest bar of any
+  // wave and pass; entries below it are dropped at the end.
+  static_assert(kChunksPerPass == 4, "the pipeline below is written for 4 chunks per pass");
+  uint64_t* const region = ls.list + wv * kWaveCap;
   uint32_t my_bar = 0;  // this wave's largest bar over the passes
+  int wcnt = 0;         // entries of this wave's region (wave-uniform)
+  bool wovf = false;    // the region overflowed: elements were lost
   for (int pass = 0; pass < passes; ++pass) {
-    if (pass > 0) load_pass(src, n, nchunks, G, pass, raw, chunk);
-    // The bar comes from the first kChunksPerPass-1 chunks, so it is ready
-    // while the last chunk is still in flight; every element (the last
-    // chunk's too) at or above it is emitted.
     uint32_t key[kElemsPerLane];
-#pragma unroll
-    for (int j = 0; j < kChunksPerPass - 1; ++j) src.keys4(raw[j], sh, key + 4 * j);
+    sched_fence();
+    load_one(src, n, G, pass, 2, raw[2]);
+    sched_fence();
+    src.keys4(raw[0], sh, key + 0);
+    sched_fence();
+    load_one(src, n, G, pass, 3, raw[3]);
+    sched_fence();
+    src.keys4(raw[1], sh, key + 4);
+    src.keys4(raw[2], sh, key + 8);
+    // The bar comes from the first three chunks, so it is ready while the
+    // last chunk is still in flight; every element (the last chunk's too)
+    // at or above it is written.
     uint32_t lmax = 0;
 #pragma unroll
-    for (int e = 0; e < 4 * (kChunksPerPass - 1); ++e) lmax = key[e] > lmax ? key[e] : lmax;
-    const uint32_t bar = wave_mth_largest_u32(lmax, m);
-    src.keys4(raw[kChunksPerPass - 1], sh, key + 4 * (kChunksPerPass - 1));
+    for (int e = 0; e < 12; ++e) lmax = key[e] > lmax ? key[e] : lmax;
+    const uint32_t bar = wave_group_bar(lmax, lg);
+    src.keys4(raw[3], sh, key + 12);
+    sched_fence();
+    // The next pass's first two chunks (empty after the last pass): without
+    // a branch, so waits on the loads above keep their exact counts.
+    load_one(src, n, G, pass + 1, 0, raw[0]);
+    load_one(src, n, G, pass + 1, 1, raw[1]);
+    sched_fence();
+    my_bar = bar > my_bar ? bar : my_bar;
+    // Per element slot: one compare; the wave's mask of qualifying lanes
+    // gives each lane its position, and the wave-uniform count advances.
+    const uint32_t thr = my_bar > 1u ? my_bar : 1u;
 #pragma unroll
-    for (int e = 4 * (kChunksPerPass - 1); e < kElemsPerLane; ++e) lmax = key[e] > lmax ? key[e] : lmax;
-    const uint32_t wbar = bar > my_bar ? bar : my_bar;
-    my_bar = wbar;
-    // One LDS atomic per wave: each lane counts its qualifying elements, a
-    // wave prefix sum gives every lane its offset, lane 63 reserves the
-    // wave's total.
-    uint32_t mask = 0;
-#pragma unroll
-    for (int e = 0; e < kElemsPerLane; ++e) mask |= (key[e] != 0u && key[e] >= wbar) ? (1u << e) : 0u;
-    const int mine = __builtin_popcount(mask);
-    const int incl = wave_incl_scan_add(mine);
-    int wbase = 0;
-    if (lane == kWave - 1 && incl > 0) wbase = atomicAdd(&ls.cnt, incl);
-    wbase = __shfl(wbase, kWave - 1);
-    if (mask) {
-      int pos = wbase + incl - mine;
-#pragma unroll
-      for (int e = 0; e < kElemsPerLane; ++e) {
-        if (mask & (1u << e)) {
-          if (pos < kListCap)
-            ls.list[pos] = make_comp(key[e], (uint32_t)(chunk[e / 4] * kChunk + lane * 4 + (e & 3)));
-          else
-            ls.ovf = 1;
-          ++pos;
-        }
+    for (int e = 0; e < kElemsPerLane; ++e) {
+      const bool p = key[e] >= thr;
+      const uint64_t sm = __ballot(p);
+      if (sm != 0ull) {
+        const int pos = wcnt + lanes_below(sm);
+        if (p && pos < kWaveCap)
+          region[pos] = make_comp(key[e], (uint32_t)(chunk_of(G, pass, e / 4) * kChunk + lane * 4 + (e & 3)));
+        wcnt += __popcll(sm);
       }
     }
+    if (wcnt > kWaveCap) {
+      wovf = true;
+      wcnt = kWaveCap;
+    }
     if (passes > 1) {
-      // Keep the list bounded between passes: drop entries below the
-      // workgroup's running bar.
+      // Keep the regions bounded between passes: drop entries below the
+      // largest bar published so far (never above the final bound, since
+      // every bar only grows).
       if (lane == 0) ls.bar[wv] = my_bar;
       __syncthreads();
       uint32_t tb = 0;
 #pragma unroll
       for (int i = 0; i < kWavesPerBlock; ++i) tb = ls.bar[i] > tb ? ls.bar[i] : tb;
-      const int cnt = ls.cnt < kListCap ? ls.cnt : kListCap;
       const uint64_t lowc = (uint64_t)tb << 32;
-      const uint64_t mine = (int)threadIdx.x < cnt ? ls.list[threadIdx.x] : 0ull;
-      const int flag = mine >= lowc && mine != 0ull;
-      int total = 0;
-      const int pos = block_exclusive_scan(flag, ls.iscan, &total);
-      if (flag) ls.list[pos] = mine;
-      if (threadIdx.x == 0) ls.cnt = total;
-      __syncthreads();
+      const uint64_t x = lane < wcnt ? region[lane] : 0ull;
+      const bool keep = x >= lowc && x != 0ull;
+      const uint64_t km = __ballot(keep);
+      if (keep) region[lanes_below(km)] = x;
+      wcnt = __popcll(km);
     }
   }
-  if (lane == 0) ls.bar[wv] = my_bar;
+  if (lane == 0) {
+    ls.bar[wv] = my_bar;
+    ls.wcnt[wv] = wcnt;
+    if (wovf) ls.ovf = 1;
+  }
   __syncthreads();
 
   // Publish into the workgroup's M fixed slots (unused slots hold 0).
@@ -355,10 +367,9 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
 #pragma unroll
   for (int i = 0; i < kWavesPerBlock; ++i) T_bar = ls.bar[i] > T_bar ? ls.bar[i] : T_bar;
   const uint64_t lowc = (uint64_t)T_bar << 32;
-  const int raw_cnt = ls.cnt;
   // Entries >= lowc are exactly the share's elements >= lowc.
   {
-    const uint64_t x = (int)threadIdx.x < raw_cnt ? ls.list[threadIdx.x] : 0ull;
+    const uint64_t x = lane < ls.wcnt[wv] ? ls.list[threadIdx.x] : 0ull;
     const bool keep = x >= lowc && x != 0ull;
     const uint64_t bal = __ballot(keep);
     if (bal) {
@@ -602,8 +613,8 @@ __global__ __launch_bounds__(kBlock) void merge_candidates(Src src0, int64_t n, 
     if (!(sT[w] > thr)) continue;
     if (!staged) {
       typename Src::Stage st;
-      src.stage_load(st);
-      src.stage_store(sh, st, t);
+      src.stage_load(st, t);
+      src.stage_store(sh, st);
       __syncthreads();
       staged = true;
     }
@@ -675,10 +686,14 @@ SelectPlan plan_select(int64_t n, int32_t n_theta, int32_t B) {
   if (G > kMaxGrid) G = kMaxGrid;
   p.G = (int)G;
   const int per = (int)((B + p.G - 1) / p.G);
+  // Each wave leaves at least 2^lg elements at or above its bar: the largest
+  // power of two <= 5/4 of the workgroup's even share of the B, within [4, 64].
   int m = (5 * per + 3) / 4;
   if (m < 4) m = 4;
   if (m > 64) m = 64;
-  p.m = m;
+  int lg = 0;
+  while ((2 << lg) <= m) ++lg;
+  p.lg = lg;
   int M = pow2_ceil(8 * per);
   if (M < 16) M = 16;
   const int cap = kMergeCap / p.G;
@@ -720,7 +735,7 @@ hipError_t launch_step(const int32_t* len, const float* arrival, int64_t n, floa
   src.cost = CostF{(float)cost.c0, (float)cost.c1, (float)cost.c2};
   if (marks == nullptr) {
     hipLaunchKernelGGL(local_candidates<PoolSource>, dim3(p.G, n_theta), dim3(kBlock), 0, stream, src, n, p.G,
-                       p.m, p.M, lists, counts, bounds);
+                       p.lg, p.M, lists, counts, bounds);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(merge_candidates<PoolSource>, dim3(n_theta), dim3(kBlock), 0, stream, src, n, p.G, p.M,
@@ -730,7 +745,7 @@ hipError_t launch_step(const int32_t* len, const float* arrival, int64_t n, floa
   // The events take the start and end timestamps of each kernel's own
   // dispatch.
   hipExtLaunchKernelGGL(local_candidates<PoolSource>, dim3(p.G, n_theta), dim3(kBlock), 0, stream, marks[0],
-                        marks[1], 0, src, n, p.G, p.m, p.M, lists, counts, bounds);
+                        marks[1], 0, src, n, p.G, p.lg, p.M, lists, counts, bounds);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipExtLaunchKernelGGL(merge_candidates<PoolSource>, dim3(n_theta), dim3(kBlock), 0, stream, marks[2], marks[3],
@@ -749,7 +764,7 @@ hipError_t launch_select(const float* score, int64_t n, int32_t n_theta, int32_t
   src.score = score;
   src.n = n;
   hipLaunchKernelGGL(local_candidates<ScoreSource>, dim3(p.G, n_theta), dim3(kBlock), 0, stream, src, n, p.G,
-                     p.m, p.M, lists, counts, bounds);
+                     p.lg, p.M, lists, counts, bounds);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(merge_candidates<ScoreSource>, dim3(n_theta), dim3(kBlock), 0, stream, src, n, p.G, p.M,
