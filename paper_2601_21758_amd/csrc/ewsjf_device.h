@@ -17,6 +17,8 @@ constexpr int kElemsPerLane = 4 * kChunksPerPass;
 constexpr int kMaxGrid = 256;                // streaming workgroups (one per CU)
 constexpr int kListCap = 1024;               // per-workgroup candidate list in LDS
 constexpr int kWaveCap = kListCap / (kBlock / kWave);  // one region of the list per wave
+constexpr int kStageWaves = 4;                // waves that stage the per-workgroup tables
+constexpr int kStageThreads = kStageWaves * kWave;
 constexpr int kMergeCap = 9088;              // merge kernel candidate capacity (LDS, >= 2 * kSortMax)
 constexpr int kSortMax = 4096;               // largest bitonic sort in LDS
 constexpr int kLutBytes = EWSJF_MAX_LEN + 16;
@@ -225,6 +227,18 @@ __device__ __forceinline__ uint32_t wave_group_bar(uint32_t x, int lg) {
 // Number of lanes below this one whose bit is set in the wave mask sm.
 __device__ __forceinline__ int lanes_below(uint64_t sm) {
   return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(sm >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)sm, 0u));
+}
+
+// xor_lane_u32 for a wave-uniform distance j in {1, 2, 4, 8, 16, 32}.
+__device__ __forceinline__ uint32_t xor_lane_u32_dyn(uint32_t x, int j) {
+  switch (j) {
+    case 1: return xor_lane_u32<1>(x);
+    case 2: return xor_lane_u32<2>(x);
+    case 4: return xor_lane_u32<4>(x);
+    case 8: return xor_lane_u32<8>(x);
+    case 16: return xor_lane_u32<16>(x);
+    default: return xor_lane_u32<32>(x);
+  }
 }
 
 template <int J>

@@ -42,8 +42,8 @@ struct PoolSource {
   float now;
   CostF cost;
 
-  static constexpr int kLutVecs = kLutBytes / 16;                       // 2049
-  static constexpr int kLutPerThread = (kLutVecs + kBlock - 1) / kBlock;  // 3
+  static constexpr int kLutVecs = kLutBytes / 16;                                     // 2049
+  static constexpr int kLutPerThread = (kLutVecs + kStageThreads - 1) / kStageThreads;  // 9
 
   struct Raw {
     i32x4 l;
@@ -61,18 +61,19 @@ struct PoolSource {
     int k, L;
   };
 
-  // Branch-free on purpose: every load is issued unconditionally (the lookup
-  // table and the mean array are read whole, indices clamped into them), and
-  // the table's scalars are read here too, so the LDS stores in stage_store
-  // wait only for these loads and never for the pool loads issued after them.
+  // Run by the first kStageThreads threads.  Branch-free on purpose: every
+  // load is issued unconditionally (the lookup table and the mean array are
+  // read whole, indices clamped into them), and the table's scalars are read
+  // here too, so the LDS stores in stage_store wait only for these loads.
   __device__ __forceinline__ void stage_load(Stage& st, int t) const {
     const i32x4* src = reinterpret_cast<const i32x4*>(table->lut);
 #pragma unroll
     for (int r = 0; r < kLutPerThread; ++r) {
-      const int i = threadIdx.x + r * kBlock;
+      const int i = threadIdx.x + r * kStageThreads;
       st.v[r] = src[i < kLutVecs ? i : kLutVecs - 1];
     }
-    st.mean = table->mean[threadIdx.x & (EWSJF_MAX_QUEUES - 1)];
+    static_assert(EWSJF_MAX_QUEUES == kStageThreads, "one mean per staging thread");
+    st.mean = table->mean[threadIdx.x];
     st.th = theta[t];
     st.k = table->k;
     st.L = table->max_len;
@@ -82,7 +83,7 @@ struct PoolSource {
     i32x4* dst = reinterpret_cast<i32x4*>(sh.lut);
 #pragma unroll
     for (int r = 0; r < kLutPerThread; ++r) {
-      const int i = threadIdx.x + r * kBlock;
+      const int i = threadIdx.x + r * kStageThreads;
       if (r + 1 < kLutPerThread || i < kLutVecs) dst[i] = st.v[r];
     }
     if ((int)threadIdx.x < st.k) sh.qp[threadIdx.x] = make_qparams(st.th, st.mean, threadIdx.x);
@@ -256,18 +257,20 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
   // is full, so a wave that issued all of its loads before scoring would
   // score only once nearly the whole stream had arrived.  Instead each wave
   // keeps two chunks in flight and scores one chunk per chunk it issues.
-  // The tables go first; the barrier before scoring then waits only for
-  // them and for the first two chunk loads of every wave.
+  // The tables go first (loaded by the first kStageWaves waves); the
+  // barrier before scoring then waits only for them and for the first two
+  // chunk loads of every wave.
+  const bool stager = wv < kStageWaves;  // wave-uniform
   typename Src::Stage st;
-  src.stage_load(st, t);
+  if (stager) src.stage_load(st, t);
   // The compute unit serves a workgroup's loads roughly in issue order; this
-  // barrier (which does not wait for the loads) puts every wave's table loads
-  // ahead of every wave's pool loads, so the table lands after one latency.
+  // barrier (which does not wait for the loads) puts every table load ahead
+  // of every pool load, so the table lands after one latency.
   __builtin_amdgcn_s_barrier();
   typename Src::Raw raw[kChunksPerPass];
   load_one(src, n, G, 0, 0, raw[0]);
   load_one(src, n, G, 0, 1, raw[1]);
-  src.stage_store(sh, st);
+  if (stager) src.stage_store(sh, st);
   if (threadIdx.x == 0) {
     ls.ovf = 0;
     ls.nout = 0;
@@ -390,40 +393,28 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
     return;
   }
   // Keep exactly the M largest: every element >= the M-th largest is listed.
-  if (cnt <= 256) {
-    // rank counting over a short list
-    if ((int)threadIdx.x < cnt) {
-      const uint64_t x = ls.list2[threadIdx.x];
-      int rank = 0;
-      for (int j = 0; j < cnt; ++j) rank += ls.list2[j] > x;
-      if (rank < M) out_list[rank] = x;
-      if (rank == M - 1) {
-        counts[slot] = (uint32_t)M;
-        bounds[slot] = x > lowc ? x : lowc;
-      }
-    }
-    return;
+  // Each element's rank (the number of larger entries; composites are
+  // distinct, so ranks are 0..cnt-1) is counted by tpe consecutive lanes,
+  // each over a slice of the list, and summed with lane exchanges.
+  int tpe = 1;
+  while (tpe < kWave && 2 * tpe * cnt <= kBlock) tpe *= 2;
+  const int e = threadIdx.x / tpe, part = threadIdx.x & (tpe - 1);
+  const int per = (cnt + tpe - 1) / tpe;
+  uint64_t x = 0;
+  int rank = 0;
+  if (e < cnt) {
+    x = ls.list2[e];
+    const int j0 = part * per, j1 = min(cnt, j0 + per);
+#pragma unroll 8
+    for (int j = j0; j < j1; ++j) rank += ls.list2[j] > x;
   }
-  const uint64_t cut = find_cut(ls.list2, cnt, M, 0, ls.hist, ls.iscan, ls.red);
-  if (threadIdx.x == 0) ls.nout = 0;
-  __syncthreads();
-  for (int i0 = 0; i0 < cnt; i0 += kBlock) {
-    const int i = i0 + (int)threadIdx.x;
-    const uint64_t x = i < cnt ? ls.list2[i] : 0ull;
-    const bool p = x >= cut && x != 0ull;
-    const uint64_t bal = __ballot(p);
-    if (bal) {
-      int b0 = 0;
-      if (lane == 0) b0 = atomicAdd(&ls.nout, __popcll(bal));
-      b0 = __shfl(b0, 0);
-      if (p) out_list[b0 + __popcll(bal & lanemask_lt())] = x;
+  for (int o = 1; o < tpe; o <<= 1) rank += (int)xor_lane_u32_dyn((uint32_t)rank, o);
+  if (e < cnt && part == 0) {
+    if (rank < M) out_list[rank] = x;
+    if (rank == M - 1) {
+      counts[slot] = (uint32_t)M;
+      bounds[slot] = x > lowc ? x : lowc;
     }
-  }
-  __syncthreads();
-  for (int i = ls.nout + (int)threadIdx.x; i < M; i += kBlock) out_list[i] = 0ull;
-  if (threadIdx.x == 0) {
-    counts[slot] = (uint32_t)ls.nout;
-    bounds[slot] = cut > lowc ? cut : lowc;
   }
 }
 
@@ -439,6 +430,7 @@ struct MergeShared {
   uint64_t wmax[kWavesPerBlock];
   uint64_t wmin[kWavesPerBlock];
   int iscan[kWavesPerBlock];
+  int wtot[kWavesPerBlock];
   int cntX;
   int cntS;
   int cut_bin;
@@ -497,54 +489,51 @@ __global__ __launch_bounds__(kBlock) void merge_candidates(Src src0, int64_t n, 
   const size_t slot0 = (size_t)t * G;
 
   // One round trip: every list slot (G x M, empty slots hold 0) and the
-  // completeness bounds.
+  // completeness bounds, as bounded buffer loads (no branches, so the waits
+  // below are exact).
   constexpr int kR = (kMergeCap + kBlock - 1) / kBlock;
-  const uint64_t* lists_t = lists + slot0 * (size_t)M;
+  const int lane = tid & (kWave - 1), wv = tid / kWave;
   const int GM = G * M;
+  const __amdgpu_buffer_rsrc_t lrs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint64_t*>(lists + slot0 * (size_t)M), (short)0, GM * 8, kBufferWord3);
   const uint64_t Tw = tid < G ? bounds[slot0 + tid] : 0ull;
   uint64_t v[kR];
 #pragma unroll
   for (int r = 0; r < kR; ++r) {
-    const int idx = tid + r * kBlock;
-    v[r] = idx < GM ? lists_t[idx] : 0ull;
+    const auto w = __builtin_amdgcn_raw_buffer_load_b64(lrs, (tid + r * kBlock) * 8, 0, kCachePolicyNT);
+    v[r] = ((uint64_t)w[1] << 32) | w[0];
   }
   if (tid < G) sT[tid] = Tw;
   // Exact range and count of the candidates (registers -> wave -> LDS)
   // while the slots go to LDS and the histogram is cleared.
-  const int lane = tid & (kWave - 1), wv = tid / kWave;
   uint64_t mx = 0, mn = ~0ull;
   int nz = 0;
 #pragma unroll
   for (int r = 0; r < kR; ++r) {
     const int idx = tid + r * kBlock;
     if (idx < GM) ms.X[idx] = v[r];
-    if (v[r] != 0ull) {
-      mx = v[r] > mx ? v[r] : mx;
-      mn = v[r] < mn ? v[r] : mn;
-      ++nz;
-    }
+    mx = v[r] > mx ? v[r] : mx;
+    mn = (v[r] != 0ull && v[r] < mn) ? v[r] : mn;
+    nz += v[r] != 0ull;
   }
   mx = wave_max_u64(mx);
   mn = wave_min_u64(mn);
-  nz = wave_incl_scan_add(nz);
+  nz = (int)__ockl_wfred_add_u32((uint32_t)nz);
   for (int i = tid; i < 4096; i += kBlock) ms.cnt[i] = 0u;
-  if (lane == kWave - 1) {
+  if (lane == 0) {
     ms.wmax[wv] = mx;
     ms.wmin[wv] = mn;
     ms.iscan[wv] = nz;
   }
   __syncthreads();
-  int total = 0;
-#pragma unroll
-  for (int i = 0; i < kWavesPerBlock; ++i) total += ms.iscan[i];
+  // Every wave reduces the kWavesPerBlock partials itself, one per lane.
+  static_assert(kWavesPerBlock <= kWave, "one partial per lane");
+  const bool pl = lane < kWavesPerBlock;
+  const int total = (int)__ockl_wfred_add_u32(pl ? (uint32_t)ms.iscan[lane] : 0u);
   int U = 0;
   if (total > 0) {
-    uint64_t hi = 0, lo = ~0ull;
-#pragma unroll
-    for (int i = 0; i < kWavesPerBlock; ++i) {
-      hi = ms.wmax[i] > hi ? ms.wmax[i] : hi;
-      lo = ms.wmin[i] < lo ? ms.wmin[i] : lo;
-    }
+    const uint64_t hi = wave_max_u64(pl ? ms.wmax[lane] : 0ull);
+    const uint64_t lo = wave_min_u64(pl ? ms.wmin[lane] : ~0ull);
     const uint64_t diff = hi - lo;
     const int bits = diff == 0 ? 0 : 64 - __clzll((long long)diff);
     const int shift = bits > 12 ? bits - 12 : 0;
@@ -552,8 +541,8 @@ __global__ __launch_bounds__(kBlock) void merge_candidates(Src src0, int64_t n, 
     for (int r = 0; r < kR; ++r)
       if (v[r] != 0ull) atomicAdd(&ms.cnt[(int)((v[r] - lo) >> shift)], 1u);
     __syncthreads();
-    // Bucket offsets from the top; the bucket where the running count
-    // reaches min(B, total) is the cut.
+    // Bucket offsets from the top: this thread's 4 buckets, a wave scan, then
+    // the waves' totals (one per lane) for the offset of this wave.
     const int want = B < total ? B : total;
     uint32_t cb[4];
     int s4 = 0;
@@ -562,8 +551,13 @@ __global__ __launch_bounds__(kBlock) void merge_candidates(Src src0, int64_t n, 
       cb[q] = ms.cnt[4095 - 4 * tid - q];
       s4 += (int)cb[q];
     }
-    int tot = 0;
-    int run = block_exclusive_scan(s4, ms.iscan, &tot);
+    const int incl = wave_incl_scan_add(s4);
+    if (lane == kWave - 1) ms.wtot[wv] = incl;
+    __syncthreads();
+    const int wt = pl ? ms.wtot[lane] : 0;
+    const int wincl = wave_incl_scan_add(wt);
+    const int before = __builtin_amdgcn_readlane(wincl - wt, wv);  // totals of the waves before this one
+    int run = before + incl - s4;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int b = 4095 - 4 * tid - q;
@@ -607,14 +601,20 @@ __global__ __launch_bounds__(kBlock) void merge_candidates(Src src0, int64_t n, 
   // Re-read shares whose lists could miss top-B members (rare).
   bool staged = false;
   const uint64_t thr0 = tau > 1ull ? tau : 1ull;
-  const int any_risk = __syncthreads_or(tid < G && sT[tid] > thr0);
+  // Every wave reads all G bounds itself, so the answer is uniform across
+  // the block without a barrier.
+  bool risk_lane = false;
+  for (int w = lane; w < G; w += kWave) risk_lane |= sT[w] > thr0;
+  const bool any_risk = __ballot(risk_lane) != 0ull;
   for (int w = 0; any_risk && w < G; ++w) {
     const uint64_t thr = tau > 1ull ? tau : 1ull;
     if (!(sT[w] > thr)) continue;
     if (!staged) {
-      typename Src::Stage st;
-      src.stage_load(st, t);
-      src.stage_store(sh, st);
+      if (tid < kStageThreads) {
+        typename Src::Stage st;
+        src.stage_load(st, t);
+        src.stage_store(sh, st);
+      }
       __syncthreads();
       staged = true;
     }
