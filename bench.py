@@ -15,8 +15,17 @@ launch cost does not bound the loop; an eager pass with per-kernel events
 gives each kernel's own duration (start/end events bound to the kernel's
 dispatch) for the roofline figure.
 
+Two more workloads ride along in the same JSON line (skip them with
+--no-extra): "batched_theta" -- one 1,048,576-request pool scored and
+selected under 256 parameter vectors per step (top-256 each); "streaming"
+-- 10,000 steps of the streaming scheduler (1,048,576-slot ring, 4,096
+arrivals and 512 admissions per step, Refine-and-Prune over the last
+65,536 arrivals every 100 steps on a side stream), per-step device latency
+p50/p99 over steps 100..9,999.
+
 Prints one JSON line.  Flags: --gpus (only 1 is supported), --steps,
---warmup, --rotate, --no-cpu (skip the oracle baseline).
+--warmup, --rotate, --no-cpu (skip the oracle baseline), --no-extra,
+--stream-steps.
 """
 from __future__ import annotations
 
@@ -102,6 +111,107 @@ def cpu_baseline(pool, table_ref, budget_s: float):
                       f"{pool.n:,}-request pool, single thread, {el:.1f} s"}, res
 
 
+def batched_theta_bench(hip, steps: int = 20):
+    """Config-3 shape: 256 parameter vectors over one 1M pool, top-256 each."""
+    import numpy as np
+    import torch
+
+    from paper_2601_21758_amd import _lib as L
+    from paper_2601_21758_amd import ewsjf as E
+    from paper_2601_21758_amd import workloads as W
+    dev = torch.device("cuda:0")
+    pool = W.config(3)
+    n, B, nt = pool.n, pool.B, pool.theta.shape[0]
+    length = torch.from_numpy(pool.length).to(dev)
+    arrival = torch.from_numpy(pool.arrival).to(dev)
+    theta = torch.from_numpy(pool.theta).to(dev)
+    table = E.partition(torch.from_numpy(pool.window).to(dev),
+                        E.params(init_queues=pool.init_queues, max_queues=pool.max_queues))
+    out = E._outs(nt, B, dev, None)
+    ws = E.Workspace(dev)
+    for _ in range(3):
+        E.step(length, arrival, pool.now, table, theta, B, pool.cost, out=out, ws=ws)
+    torch.cuda.synchronize()
+    ws_buf = ws.get(E.workspace_bytes(L.OP_STEP, n, nt, B))
+    marks = [(hip.event(), hip.event(), hip.event(), hip.event()) for _ in range(steps)]
+    vp = C.c_void_p
+    s = vp(torch.cuda.current_stream().cuda_stream)
+    c = E.cost(*pool.cost)
+    torch.cuda._sleep(int(2.4e9 * 0.02))
+    e0, e1 = hip.event(), hip.event()
+    hip.rt.hipEventRecord(e0, s)
+    for i in range(steps):
+        ev = (vp * 4)(*marks[i])
+        st = L.lib().ewsjf_step_timed(vp(length.data_ptr()), vp(arrival.data_ptr()), n, float(pool.now),
+                                      vp(table.data_ptr()), vp(theta.data_ptr()), nt, C.byref(c), B, 0,
+                                      vp(out[0].data_ptr()), vp(out[1].data_ptr()), vp(out[2].data_ptr()),
+                                      vp(ws_buf.data_ptr()), ws_buf.numel(), s, ev)
+        if st != 0:
+            raise L.EwsjfError(st, "ewsjf_step_timed")
+    hip.rt.hipEventRecord(e1, s)
+    ms = hip.elapsed_ms(e0, e1) / steps
+    k1 = float(np.mean([hip.elapsed_ms(m[0], m[1]) for m in marks]))
+    k2 = float(np.mean([hip.elapsed_ms(m[2], m[3]) for m in marks]))
+    return {"workload": "batched_theta_1m: 1,048,576 requests (3-mode lognormal mix), 64-queue policy, "
+                        "256 parameter vectors drawn in the stated ranges, top B=256 per vector",
+            "ms_per_step": ms, "request_theta_pairs_per_s": n * nt / (ms * 1e-3),
+            "kernels_ms": {"local_candidates": k1, "merge_candidates": k2}, "steps": steps,
+            "input_sha256": pool.digest()[:16]}
+
+
+def streaming_bench(steps: int):
+    """Config-4 shape: per-step device latency of the streaming scheduler."""
+    import numpy as np
+    import torch
+
+    from paper_2601_21758_amd import ewsjf as E
+    from paper_2601_21758_amd import workloads as W
+    from paper_2601_21758_amd.streaming import StreamingScheduler
+    dev = torch.device("cuda:0")
+    sw = W.Streaming(steps=steps)
+    L0, A0 = sw.initial_fill()
+    per = sw.per_step
+    lens = np.empty((steps, per), np.int32)
+    arrs = np.empty((steps, per), np.float32)
+    for i in range(steps):
+        lens[i], arrs[i] = sw.arrivals(i)
+    nows = arrs[:, -1].astype(np.float64)
+    dl = torch.from_numpy(lens).to(dev)
+    da = torch.from_numpy(arrs).to(dev)
+    prm = E.params(init_queues=sw.K, max_queues=sw.K)
+    sched = StreamingScheduler(sw.capacity, sw.window_size, sw.B, prm, sw.theta[0], sw.cost, device=dev)
+    sched.fill(L0, A0)
+    torch.cuda.synchronize()
+    block = 100
+    lat = np.zeros(steps)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(block)]
+    for b0 in range(0, steps, block):
+        nb = min(block, steps - b0)
+        torch.cuda._sleep(int(2.4e9 * 0.03))  # hold the stream while the block is enqueued
+        for j in range(nb):
+            i = b0 + j
+            ev[j][0].record()
+            sched.insert(dl[i], da[i])
+            if i % sw.rp_every == 0:
+                sched.launch_repartition()
+            sched.step(float(nows[i]), tombstone=True)
+            ev[j][1].record()
+        torch.cuda.synchronize()
+        for j in range(nb):
+            lat[b0 + j] = ev[j][0].elapsed_time(ev[j][1]) * 1e3
+    steady = lat[100:] if steps > 100 else lat
+    rp = lat[101::sw.rp_every] if steps > 101 else np.zeros(0)
+    return {"workload": "streaming_drift_1m: 1,048,576-slot ring, 4,096 arrivals and B=512 admissions per step, "
+                        "64-queue Refine-and-Prune over the last 65,536 arrivals every 100 steps (side stream, "
+                        "effective the next step), short-request weight drifting 0.9 -> 0.3",
+            "steps": steps, "p50_us": float(np.percentile(steady, 50)), "p99_us": float(np.percentile(steady, 99)),
+            "mean_us": float(steady.mean()), "max_us": float(steady.max()),
+            "after_repartition_p50_us": float(np.median(rp)) if rp.size else None,
+            "latency": "device time from the step's first insert copy to the end of its admission, "
+                       "steps 100.. (steps before 100 are warm-up)",
+            "slowest_steps": [[int(i), float(lat[i])] for i in np.argsort(lat)[::-1][:8]]}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -110,6 +220,8 @@ def main() -> int:
     ap.add_argument("--rotate", type=int, default=10)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--no-extra", action="store_true", help="skip the batched-theta and streaming workloads")
+    ap.add_argument("--stream-steps", type=int, default=10000)
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="run one device copy of this many MiB first (counter calibration under rocprofv3)")
     args = ap.parse_args()
@@ -266,6 +378,9 @@ def main() -> int:
         "eager_ms_per_step": eager_ms, "graph_matches_eager": graph_ok,
         "partition_ms": partition_ms,
     }
+    if not args.no_extra:
+        out["batched_theta"] = batched_theta_bench(hip)
+        out["streaming"] = streaming_bench(args.stream_steps)
     if not args.no_cpu:
         import oracle
         ref_table = oracle.partition(pool.window, init_queues=pool.init_queues, max_queues=pool.max_queues)

@@ -157,6 +157,24 @@ __device__ __forceinline__ int wave_incl_scan_add(int v) {
 
 // Exclusive prefix sum over kBlock threads; returns this thread's prefix and
 // writes the total to *total.  scratch holds >= kWavesPerBlock ints.
+// The same over a block of nthreads threads (a multiple of kWave).
+__device__ __forceinline__ int block_exclusive_scan_n(int x, int* scratch, int* total, int nthreads) {
+  const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
+  const int nw = nthreads / kWave;
+  const int incl = wave_incl_scan_add(x);
+  if (lane == kWave - 1) scratch[wv] = incl;
+  __syncthreads();
+  int wave_base = 0, sum = 0;
+  for (int i = 0; i < nw; ++i) {
+    const int si = scratch[i];
+    wave_base += i < wv ? si : 0;
+    sum += si;
+  }
+  __syncthreads();
+  *total = sum;
+  return wave_base + incl - x;
+}
+
 __device__ __forceinline__ int block_exclusive_scan(int x, int* scratch, int* total) {
   const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
   const int incl = wave_incl_scan_add(x);

@@ -34,8 +34,19 @@ namespace {
 constexpr int kHistPerBlock = 16384;   // window entries per histogram workgroup
 constexpr int kMaxHistBlocks = 64;
 constexpr int kKmeansBlocks = 256;
-constexpr int kLeafLds = 4096;         // Stage-3 leaves kept in LDS
+constexpr int kLeafLds = 2048;         // Stage-3 leaves kept in LDS
+constexpr uint64_t kInfBits = 0x7FF0000000000000ull;  // +inf as binary64 bits
 constexpr int kBinsPerThread = EWSJF_MAX_LEN / kBlock;  // 32
+
+// A Stage-3 leaf with its neighbours' links and the density and mean of the
+// leaf after it (so one merge needs two rounds of LDS reads).  48 bytes.
+struct alignas(16) Leaf {
+  int64_t n, S;
+  double rho, mean;      // n / (hi - lo + 1), S / n
+  double rho_n, mean_n;  // the same of the next leaf (unused when nxt < 0)
+  int32_t lo, hi;
+  int32_t nxt, prv;      // -1: none; prv == -2 marks a merged-away leaf
+};
 
 struct PartWs {
   uint32_t* partial;  // [Gh][L+1]
@@ -51,10 +62,8 @@ struct PartWs {
   int64_t* gS;
   int32_t* glo;
   int32_t* ghi;
-  double* gU;
-  int32_t* gnext;
-  int32_t* gprev;
-  int32_t* galive;
+  Leaf* grec;         // [L] Stage-3 records when the leaves exceed LDS
+  uint64_t* gU;       // [L]
   int Gh;
 };
 
@@ -90,16 +99,14 @@ PartWs carve_part(void* ws, int64_t n, int L) {
   w.gS = reinterpret_cast<int64_t*>(take((size_t)L * 8));
   w.glo = reinterpret_cast<int32_t*>(take((size_t)L * 4));
   w.ghi = reinterpret_cast<int32_t*>(take((size_t)L * 4));
-  w.gU = reinterpret_cast<double*>(take((size_t)L * 8));
-  w.gnext = reinterpret_cast<int32_t*>(take((size_t)L * 4));
-  w.gprev = reinterpret_cast<int32_t*>(take((size_t)L * 4));
-  w.galive = reinterpret_cast<int32_t*>(take((size_t)L * 4));
+  w.grec = reinterpret_cast<Leaf*>(take((size_t)L * sizeof(Leaf)));
+  w.gU = reinterpret_cast<uint64_t*>(take((size_t)L * 8));
   return w;
 }
 
 size_t carve_size(int64_t n, int L) {
   PartWs w = carve_part(nullptr, n, L);
-  return reinterpret_cast<size_t>(w.galive) + up256((size_t)L * 4);
+  return reinterpret_cast<size_t>(w.gU) + up256((size_t)L * 8);
 }
 
 // ---------------------------------------------------------------------------
@@ -288,6 +295,15 @@ __device__ __forceinline__ double utility(int64_t na, int64_t Sa, int32_t loa, i
   return (rho_a + rho_b) / (fabs(m_b - m_a) + eps);
 }
 
+// The same expression on per-leaf densities and means computed once (the
+// division results are identical to recomputing them).
+__device__ __forceinline__ double utility_cached(double rho_a, double m_a, double rho_b, double m_b, double eps) {
+  return (rho_a + rho_b) / (fabs(m_b - m_a) + eps);
+}
+
+__device__ __forceinline__ uint64_t dbits(double x) { return (uint64_t)__double_as_longlong(x); }
+
+
 struct ArgMin {
   double u;
   int i;
@@ -324,13 +340,6 @@ struct RpShared {
       uint16_t v[EWSJF_MAX_LEN];
       uint8_t start[EWSJF_MAX_LEN];
     } a;
-    struct {
-      int64_t n[kLeafLds];
-      int64_t S[kLeafLds];
-      int32_t lo[kLeafLds];
-      int32_t hi[kLeafLds];
-      double U[kLeafLds];
-    } b;
   } u;
   int64_t scr64[kWavesPerBlock];
   double su[kWavesPerBlock];
@@ -377,6 +386,23 @@ __device__ void segment_carries(RpShared& sm, int V, int j0, int* carry_s, int* 
   __syncthreads();
   *carry_s = cs;
   *carry_e = ce < V ? ce : V;
+}
+
+// The queue table from k queue aggregates in length order.
+template <class N, class Lo>
+__device__ void write_queues(ewsjf_queue_table* tab, int k, const N* n, const N* S, const Lo* lo, const Lo* hi,
+                             int tid, int nthreads) {
+  for (int i = tid; i < k; i += nthreads) {
+    const int64_t cn = n[i], cs = S[i];
+    const int32_t l = lo[i], h = hi[i];
+    if (i > 0) tab->bounds[i - 1] = l;
+    tab->lo[i] = l;
+    tab->hi[i] = h;
+    tab->count[i] = cn;
+    tab->sum[i] = cs;
+    tab->mean[i] = (double)cs / (double)cn;
+  }
+  if (tid == 0) tab->k = k;
 }
 
 __global__ __launch_bounds__(kBlock) void rp_refine_prune(PartWs w, ewsjf_partition_params p, int64_t n_window,
@@ -493,161 +519,8 @@ __global__ __launch_bounds__(kBlock) void rp_refine_prune(PartWs w, ewsjf_partit
   __threadfence();
   __syncthreads();
   const int n_leaves = nl;
-  bool in_lds = false;
-
-  // ---- Stage 3, global-memory phase while the leaves exceed the LDS arrays ---
-  if (nl > p.max_queues && nl > kLeafLds) {
-    volatile double* gU = w.gU;
-    volatile int64_t* gn = w.gn;
-    volatile int64_t* gS = w.gS;
-    volatile int32_t* glo = w.glo;
-    volatile int32_t* ghi = w.ghi;
-    volatile int32_t* gnext = w.gnext;
-    volatile int32_t* gprev = w.gprev;
-    volatile int32_t* galive = w.galive;
-    const int nl0 = nl;
-    for (int i = tid; i < nl0; i += kBlock) {
-      gnext[i] = i + 1 < nl0 ? i + 1 : -1;
-      gprev[i] = i - 1;
-      galive[i] = 1;
-      gU[i] = i + 1 < nl0 ? utility(gn[i], gS[i], glo[i], ghi[i], gn[i + 1], gS[i + 1], glo[i + 1], ghi[i + 1], p.eps)
-                          : inf;
-    }
-    __threadfence();
-    __syncthreads();
-    int alive = nl0;
-    while (alive > p.max_queues && alive > kLeafLds) {
-      ArgMin x{inf, 0x7fffffff};
-      for (int i = tid; i < nl0; i += kBlock) x = argmin_pick(x, ArgMin{gU[i], i});
-      const ArgMin best = block_argmin(x, sm.su, sm.si);
-      if (tid == 0) {
-        const int a = best.i;
-        const int b = gnext[a];
-        gn[a] = gn[a] + gn[b];
-        gS[a] = gS[a] + gS[b];
-        ghi[a] = ghi[b];
-        const int c = gnext[b];
-        gnext[a] = c;
-        if (c >= 0) gprev[c] = a;
-        galive[b] = 0;
-        gU[b] = inf;
-        gU[a] = c >= 0 ? utility(gn[a], gS[a], glo[a], ghi[a], gn[c], gS[c], glo[c], ghi[c], p.eps) : inf;
-        const int pr = gprev[a];
-        if (pr >= 0) gU[pr] = utility(gn[pr], gS[pr], glo[pr], ghi[pr], gn[a], gS[a], glo[a], ghi[a], p.eps);
-      }
-      __threadfence();
-      __syncthreads();
-      --alive;
-    }
-    // Survivors, in index (= length) order, go straight into the LDS arrays.
-    const int per = (nl0 + kBlock - 1) / kBlock;
-    const int i0 = tid * per;
-    int cnt = 0;
-    for (int q = 0; q < per; ++q)
-      if (i0 + q < nl0) cnt += galive[i0 + q];
-    int tot = 0;
-    int pos = block_exclusive_scan(cnt, sm.iscr, &tot);
-    __syncthreads();  // the LDS union switches from the Stage-2 view to the leaf view
-    for (int q = 0; q < per; ++q) {
-      const int i = i0 + q;
-      if (i < nl0 && galive[i]) {
-        sm.u.b.n[pos] = gn[i];
-        sm.u.b.S[pos] = gS[i];
-        sm.u.b.lo[pos] = glo[i];
-        sm.u.b.hi[pos] = ghi[i];
-        ++pos;
-      }
-    }
-    nl = tot;
-    in_lds = true;
-    __syncthreads();
-  }
-
-  // ---- Stage 3 in LDS ----------------------------------------------------------
-  if (nl > p.max_queues) {
-    if (!in_lds) {
-      __syncthreads();
-      for (int i = tid; i < nl; i += kBlock) {
-        sm.u.b.n[i] = w.gn[i];
-        sm.u.b.S[i] = w.gS[i];
-        sm.u.b.lo[i] = w.glo[i];
-        sm.u.b.hi[i] = w.ghi[i];
-      }
-      in_lds = true;
-      __syncthreads();
-    }
-    for (int i = tid; i < nl; i += kBlock)
-      sm.u.b.U[i] = i + 1 < nl ? utility(sm.u.b.n[i], sm.u.b.S[i], sm.u.b.lo[i], sm.u.b.hi[i], sm.u.b.n[i + 1],
-                                         sm.u.b.S[i + 1], sm.u.b.lo[i + 1], sm.u.b.hi[i + 1], p.eps)
-                               : inf;
-    __syncthreads();
-    while (nl > p.max_queues) {
-      ArgMin x{inf, 0x7fffffff};
-      for (int i = tid; i < nl - 1; i += kBlock) x = argmin_pick(x, ArgMin{sm.u.b.U[i], i});
-      const ArgMin best = block_argmin(x, sm.su, sm.si);
-      const int a = best.i;
-      // remove entry a+1: shift a+2.. left by one (two phases through registers)
-      int64_t tn[kLeafLds / kBlock], tS[kLeafLds / kBlock];
-      int32_t tlo[kLeafLds / kBlock], thi[kLeafLds / kBlock];
-      double tU[kLeafLds / kBlock];
-      int cntq = 0;
-      for (int i = a + 1 + tid; i < nl - 1; i += kBlock) {
-        tn[cntq] = sm.u.b.n[i + 1];
-        tS[cntq] = sm.u.b.S[i + 1];
-        tlo[cntq] = sm.u.b.lo[i + 1];
-        thi[cntq] = sm.u.b.hi[i + 1];
-        tU[cntq] = sm.u.b.U[i + 1];
-        ++cntq;
-      }
-      const int64_t nb = sm.u.b.n[a + 1], Sb = sm.u.b.S[a + 1];
-      const int32_t hib = sm.u.b.hi[a + 1];
-      __syncthreads();
-      cntq = 0;
-      for (int i = a + 1 + tid; i < nl - 1; i += kBlock) {
-        sm.u.b.n[i] = tn[cntq];
-        sm.u.b.S[i] = tS[cntq];
-        sm.u.b.lo[i] = tlo[cntq];
-        sm.u.b.hi[i] = thi[cntq];
-        sm.u.b.U[i] = tU[cntq];
-        ++cntq;
-      }
-      if (tid == 0) {
-        sm.u.b.n[a] += nb;
-        sm.u.b.S[a] += Sb;
-        sm.u.b.hi[a] = hib;
-      }
-      --nl;
-      __syncthreads();
-      if (tid == 0) {
-        if (a + 1 < nl)
-          sm.u.b.U[a] = utility(sm.u.b.n[a], sm.u.b.S[a], sm.u.b.lo[a], sm.u.b.hi[a], sm.u.b.n[a + 1],
-                                sm.u.b.S[a + 1], sm.u.b.lo[a + 1], sm.u.b.hi[a + 1], p.eps);
-        else
-          sm.u.b.U[a] = inf;
-        if (a > 0)
-          sm.u.b.U[a - 1] = utility(sm.u.b.n[a - 1], sm.u.b.S[a - 1], sm.u.b.lo[a - 1], sm.u.b.hi[a - 1],
-                                    sm.u.b.n[a], sm.u.b.S[a], sm.u.b.lo[a], sm.u.b.hi[a], p.eps);
-      }
-      __syncthreads();
-    }
-  }
-
-  // ---- Queue table ------------------------------------------------------------
-  const int k = nl;
-  for (int i = tid; i < k; i += kBlock) {
-    const int64_t cn = in_lds ? sm.u.b.n[i] : w.gn[i];
-    const int64_t cs = in_lds ? sm.u.b.S[i] : w.gS[i];
-    const int32_t lo = in_lds ? sm.u.b.lo[i] : w.glo[i];
-    const int32_t hi = in_lds ? sm.u.b.hi[i] : w.ghi[i];
-    if (i > 0) tab->bounds[i - 1] = lo;
-    tab->lo[i] = lo;
-    tab->hi[i] = hi;
-    tab->count[i] = cn;
-    tab->sum[i] = cs;
-    tab->mean[i] = (double)cs / (double)cn;
-  }
   if (tid == 0) {
-    tab->k = k;
+    w.meta[3] = n_leaves;
     tab->max_len = L;
     tab->n_distinct = V;
     tab->n_coarse = n_coarse;
@@ -655,9 +528,190 @@ __global__ __launch_bounds__(kBlock) void rp_refine_prune(PartWs w, ewsjf_partit
     tab->reserved0 = 0;
     tab->n_window = n_window;
   }
+  // Within the queue budget: the leaves are the queues.  Otherwise Stage 3
+  // (rp_merge) writes them.
+  if (nl <= p.max_queues) write_queues(tab, nl, w.gn, w.gS, w.glo, w.ghi, tid, kBlock);
 }
 
 }  // namespace
+
+// ---------------------------------------------------------------------------
+// Stage 3: greedy merge of the adjacent pair with the smallest utility until
+// at most max_queues remain (Section 4.2, "Stage 3", Eq. 3).
+//
+// The merge is sequential (each merge changes its neighbours' utilities), so
+// one wave runs it.  Leaves keep their index (a linked list replaces
+// shifting), and lane l caches the minimum utility over the pairs it owns
+// (left-leaf indices [l*P, l*P + P)).  A merge costs a two-step wave
+// reduction for the global minimum, two rounds of record reads and a rescan
+// by the few lanes whose pairs changed.  Utilities are non-negative binary64
+// values, so their bit patterns order like the values; ties go to the smaller
+// leaf index, which is the smaller position in the list.  The records live in
+// LDS, or in the workspace when there are more leaves than LDS holds.
+// ---------------------------------------------------------------------------
+constexpr int kMergeThreads = 256;
+
+template <bool kInLds>
+__device__ __forceinline__ void stage3(Leaf* rec, uint64_t* U, const PartWs& w, int nl0,
+                                       const ewsjf_partition_params& p, ewsjf_queue_table* tab, int* iscr) {
+  const int tid = threadIdx.x;
+  for (int i = tid; i < nl0; i += kMergeThreads) {
+    Leaf r;
+    r.n = w.gn[i];
+    r.S = w.gS[i];
+    r.lo = w.glo[i];
+    r.hi = w.ghi[i];
+    r.rho = (double)r.n / (double)((int64_t)r.hi - (int64_t)r.lo + 1);
+    r.mean = (double)r.S / (double)r.n;
+    r.nxt = i + 1 < nl0 ? i + 1 : -1;
+    r.prv = i - 1;
+    r.rho_n = r.mean_n = 0.0;
+    if (i + 1 < nl0) {
+      const int64_t n1 = w.gn[i + 1], S1 = w.gS[i + 1];
+      r.rho_n = (double)n1 / (double)((int64_t)w.ghi[i + 1] - (int64_t)w.glo[i + 1] + 1);
+      r.mean_n = (double)S1 / (double)n1;
+    }
+    rec[i] = r;
+    U[i] = i + 1 < nl0 ? dbits(utility_cached(r.rho, r.mean, r.rho_n, r.mean_n, p.eps)) : kInfBits;
+  }
+  __syncthreads();
+  if (tid < kWave) {
+    const int lane = tid;
+    const int P = (nl0 + kWave - 1) / kWave;
+    // This lane's minimum (first index on ties) over its P slots.
+    auto scan_own = [&](uint64_t& mu, int& mi) {
+      mu = kInfBits + 1;  // above every utility, +inf included
+      mi = 0x7fffffff;
+#pragma unroll 8
+      for (int q = 0; q < P; ++q) {
+        const int i = lane * P + q;
+        const uint64_t u = i < nl0 ? U[i] : ~0ull;
+        if (u < mu) {
+          mu = u;
+          mi = i;
+        }
+      }
+    };
+    uint64_t lane_u;
+    int lane_i;
+    scan_own(lane_u, lane_i);
+    // Lane `owner`'s minimum recomputed by the whole wave, one slot per lane
+    // (P <= kWave when the records are in LDS).
+    auto rescan = [&](int owner) {
+      if constexpr (kInLds) {
+        const int i = owner * P + lane;
+        const uint64_t u = (lane < P && i < nl0) ? U[i] : ~0ull;
+        const uint64_t m = wave_min_u64(u);
+        const uint64_t bal = __ballot(u == m);
+        if (lane == owner) {
+          lane_u = m == ~0ull ? kInfBits + 1 : m;
+          lane_i = m == ~0ull ? 0x7fffffff : owner * P + (int)__builtin_ctzll(bal);
+        }
+      } else {
+        if (lane == owner) scan_own(lane_u, lane_i);
+      }
+    };
+    for (int alive = nl0; alive > p.max_queues; --alive) {
+      const uint64_t mu = wave_min_u64(lane_u);
+      const uint64_t bal = __ballot(lane_u == mu);
+      const int a = __builtin_amdgcn_readlane(lane_i, (int)__builtin_ctzll(bal));
+      const int b = rec[a].nxt, pr = rec[a].prv;
+      const int64_t na = rec[a].n + rec[b].n;
+      const int64_t Sa = rec[a].S + rec[b].S;
+      const int32_t hia = rec[b].hi;
+      const int c = rec[b].nxt;
+      const double rho_c = rec[b].rho_n, mean_c = rec[b].mean_n;
+      const double rho_a = (double)na / (double)((int64_t)hia - (int64_t)rec[a].lo + 1);
+      const double m_a = (double)Sa / (double)na;
+      const uint64_t Ua = c >= 0 ? dbits(utility_cached(rho_a, m_a, rho_c, mean_c, p.eps)) : kInfBits;
+      const uint64_t Upr = pr >= 0 ? dbits(utility_cached(rec[pr].rho, rec[pr].mean, rho_a, m_a, p.eps)) : kInfBits;
+      if (lane == 0) {
+        rec[a].n = na;
+        rec[a].S = Sa;
+        rec[a].hi = hia;
+        rec[a].rho = rho_a;
+        rec[a].mean = m_a;
+        rec[a].rho_n = rho_c;
+        rec[a].mean_n = mean_c;
+        rec[a].nxt = c;
+        rec[b].prv = -2;
+        if (c >= 0) rec[c].prv = a;
+        if (pr >= 0) {
+          rec[pr].rho_n = rho_a;
+          rec[pr].mean_n = m_a;
+          U[pr] = Upr;
+        }
+        U[b] = kInfBits;
+        U[a] = Ua;
+      }
+      // Lane 0's stores before anyone's next reads: LDS serves one wave in
+      // order; the workspace needs a fence.
+      if constexpr (!kInLds) __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+      // Cached minima that may be stale: a's owner (its minimum was a, now
+      // Ua), b's owner if its minimum was b (now removed), pr's owner if its
+      // minimum was pr (now Upr).  A value that improves a minimum is taken
+      // directly; otherwise the owner's slots are rescanned.
+      const int oa = a / P, ob = b / P, op = pr >= 0 ? pr / P : -1;
+      const bool lower_a = Ua < mu;  // still the global minimum: a keeps it
+      bool stale = false;
+      if (lane == oa) {
+        if (lower_a) lane_u = Ua;  // lane_i == a already
+        else stale = true;
+      }
+      if (lane == ob && lane_i == b) stale = true;
+      if (lane == op) {
+        if (Upr < lane_u || (Upr == lane_u && pr < lane_i)) {
+          lane_u = Upr;
+          lane_i = pr;
+        } else if (lane_i == pr) {
+          stale = true;
+        }
+      }
+      uint64_t todo = __ballot(stale);
+      while (todo != 0ull) {
+        const int owner = (int)__builtin_ctzll(todo);
+        todo &= todo - 1;
+        rescan(owner);
+      }
+    }
+  }
+  __syncthreads();
+  // Survivors in index (= length) order are the queues.
+  const int per = (nl0 + kMergeThreads - 1) / kMergeThreads;
+  const int i0 = tid * per;
+  int cnt = 0;
+  for (int q = 0; q < per; ++q)
+    if (i0 + q < nl0 && rec[i0 + q].prv != -2) ++cnt;
+  int tot = 0;
+  int pos = block_exclusive_scan_n(cnt, iscr, &tot, kMergeThreads);
+  for (int q = 0; q < per; ++q) {
+    const int i = i0 + q;
+    if (i < nl0 && rec[i].prv != -2) {
+      const Leaf& r = rec[i];
+      if (pos > 0) tab->bounds[pos - 1] = r.lo;
+      tab->lo[pos] = r.lo;
+      tab->hi[pos] = r.hi;
+      tab->count[pos] = r.n;
+      tab->sum[pos] = r.S;
+      tab->mean[pos] = (double)r.S / (double)r.n;
+      ++pos;
+    }
+  }
+  if (tid == 0) tab->k = tot;
+}
+
+__global__ __launch_bounds__(kMergeThreads) void rp_merge(PartWs w, ewsjf_partition_params p,
+                                                          ewsjf_queue_table* tab) {
+  __shared__ Leaf srec[kLeafLds];
+  __shared__ uint64_t sU[kLeafLds];
+  __shared__ int iscr[kMergeThreads / kWave];
+  const int nl = w.meta[3];
+  if (nl <= p.max_queues) return;  // rp_refine_prune wrote the queues
+  if (nl <= kLeafLds)
+    stage3<true>(srec, sU, w, nl, p, tab, iscr);
+  else
+    stage3<false>(w.grec, w.gU, w, nl, p, tab, iscr);
+}
 
 size_t partition_ws_bytes(int64_t n_window, const ewsjf_partition_params& p) {
   return carve_size(n_window, p.max_len);
@@ -675,6 +729,7 @@ hipError_t launch_partition(const int32_t* window, int64_t n_window, const ewsjf
     hipLaunchKernelGGL(rp_kmeans3_pick, dim3(1), dim3(64), 0, stream, w, kKmeansBlocks);
   }
   hipLaunchKernelGGL(rp_refine_prune, dim3(1), dim3(kBlock), 0, stream, w, p, n_window, table);
+  hipLaunchKernelGGL(rp_merge, dim3(1), dim3(kMergeThreads), 0, stream, w, p, table);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   return launch_build_lut(table, stream);

@@ -1,0 +1,121 @@
+"""Streaming harness: ring insertion, eviction, tombstones, Refine-and-Prune
+every rp_every steps on the sliding window with a one-step hand-over, checked
+in lockstep against the oracle (both sides apply the oracle's admitted set so
+an allowed near-tie difference cannot make the states diverge)."""
+import os
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+
+from paper_2601_21758_amd import workloads as W  # noqa: E402
+from paper_2601_21758_amd.streaming import StreamingScheduler  # noqa: E402
+from parity_util import check_admission, check_table  # noqa: E402
+from streaming_ref import OracleStream  # noqa: E402
+
+
+# ---- host-side logic (CPU) ------------------------------------------------------
+def test_ring_copy_wraps():
+    dst = torch.zeros(10, dtype=torch.int32)
+    StreamingScheduler._ring_copy(dst, 7, torch.arange(1, 6, dtype=torch.int32), 10)
+    assert dst.tolist() == [4, 5, 0, 0, 0, 0, 0, 1, 2, 3]
+    StreamingScheduler._ring_copy(dst, 2, torch.arange(6, 9, dtype=torch.int32), 10)
+    assert dst.tolist() == [4, 5, 6, 7, 8, 0, 0, 1, 2, 3]
+
+
+def test_reference_ring_and_window_follow_the_generator():
+    s = W.Streaming(seed=4, capacity=1 << 12, per_step=256, steps=40, window=1024, rp_every=10, B=32)
+    ref = OracleStream(s.capacity, s.window_size, s.B, 16, 16, s.theta, s.cost)
+    L0, A0 = s.initial_fill()
+    ref.fill(L0, A0)
+    assert np.array_equal(np.sort(ref.win), np.sort(L0[-1024:]))
+    history = [L0]
+    for step in range(40):
+        L, A = s.arrivals(step)
+        ref.insert(L, A)
+        history.append(L)
+        # the request with id = slot holds the latest arrival written there
+        assert np.array_equal(ref.len[s.slots(step)], L)
+        # the window is the multiset of the last `window` arrival lengths
+        last = np.concatenate(history)[-1024:]
+        assert np.array_equal(np.sort(ref.win), np.sort(last))
+
+
+def test_constructor_rejects_window_larger_than_ring():
+    from paper_2601_21758_amd import ewsjf
+    with pytest.raises(ValueError):
+        StreamingScheduler(100, 200, 8, ewsjf.params(), W.THETA_MID, device="cpu")
+
+
+# ---- lockstep parity on the GPU ---------------------------------------------------
+def _lockstep(capacity, per_step, steps, window, rp_every, B, K, label, tombstone_check_every=0):
+    from paper_2601_21758_amd import ewsjf
+    s = W.Streaming(seed=4, capacity=capacity, per_step=per_step, steps=steps, window=window, rp_every=rp_every,
+                    B=B, K=K)
+    prm = ewsjf.params(init_queues=K, max_queues=K)
+    gpu = StreamingScheduler(capacity, window, B, prm, s.theta[0], s.cost)
+    ref = OracleStream(capacity, window, B, K, K, s.theta, s.cost)
+    L0, A0 = s.initial_fill()
+    gpu.fill(L0, A0)
+    ref.fill(L0, A0)
+    check_table(ewsjf.read_table(gpu.table()), ref.table)
+    near = 0
+    for step in range(steps):
+        L, A = s.arrivals(step)
+        gpu.insert(torch.from_numpy(L).cuda(), torch.from_numpy(A).cuda())
+        ref.insert(L, A)
+        now = float(A[-1])
+        if step % rp_every == 0:
+            gpu.launch_repartition()
+            rt = ref.repartition()
+        tomb = tombstone_check_every and step % tombstone_check_every == 0
+        ids, top, nsel = gpu.step(now, tombstone=bool(tomb))
+        rids, rtop, rnsel, rsc = ref.step(now)
+        torch.cuda.synchronize()
+        gi = ids.cpu().numpy()[0]
+        near += check_admission(gi, top.cpu().numpy()[0], nsel.cpu().numpy()[0], rids, rtop, rnsel, rsc)
+        if step % rp_every == 0:
+            check_table(ewsjf.read_table(gpu.table()), rt)
+        if tomb:
+            # the step tombstoned its own admitted set; restore the slots the
+            # oracle did not admit (near-ties only) before applying the oracle's
+            glen = gpu.len.cpu().numpy()
+            assert np.all(glen[gi[:int(nsel[0])]] == 0)
+            extra = np.setdiff1d(gi[:int(nsel[0])], rids[:rnsel])
+            if extra.size:
+                gpu.len[torch.from_numpy(extra.astype(np.int64)).cuda()] = torch.from_numpy(ref.len[extra]).cuda()
+        gpu.apply_tombstones(rids[:rnsel])
+        ref.tombstone(rids[:rnsel])
+        if step % 50 == 0 or step == steps - 1:
+            assert np.array_equal(gpu.len.cpu().numpy(), ref.len), f"{label}: ring lengths diverged at step {step}"
+            print(f"{label}: step {step} ok (near-tie differences so far {near})", flush=True)
+    assert np.array_equal(gpu.arr.cpu().numpy(), ref.arr)
+    return near
+
+
+@pytest.mark.gpu
+def test_streaming_lockstep_small():
+    _lockstep(capacity=1 << 14, per_step=512, steps=120, window=4096, rp_every=10, B=64, K=16, label="small",
+              tombstone_check_every=7)
+
+
+@pytest.mark.gpu
+def test_streaming_lockstep_ring_wraps_many_times():
+    # 24 steps of 1024 into a 4096-slot ring: every slot is overwritten six
+    # times, evicting pending requests
+    _lockstep(capacity=4096, per_step=1024, steps=24, window=2048, rp_every=5, B=128, K=8, label="wrap",
+              tombstone_check_every=3)
+
+
+@pytest.mark.gpu
+def test_streaming_lockstep_full_size_prefix():
+    # the streaming workload at full size (1,048,576-slot ring, 4,096 arrivals
+    # and 512 admissions per step, 65,536-length window, 64 queues): the first
+    # 101 steps, so two hand-overs (steps 0 and 100) are covered
+    _lockstep(capacity=1 << 20, per_step=4096, steps=101, window=65536, rp_every=100, B=512, K=64, label="full",
+              tombstone_check_every=25)
