@@ -289,14 +289,18 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
   bool wovf = false;    // the region overflowed: elements were lost
   for (int pass = 0; pass < passes; ++pass) {
     uint32_t key[kElemsPerLane];
-    sched_fence();
-    load_one(src, n, G, pass, 2, raw[2]);
+    // A wave stalls at a load while the memory pipeline is full, so it
+    // scores a chunk that has arrived before it issues the next load; the
+    // other waves keep the pipeline full meanwhile.
     sched_fence();
     src.keys4(raw[0], sh, key + 0);
     sched_fence();
-    load_one(src, n, G, pass, 3, raw[3]);
+    load_one(src, n, G, pass, 2, raw[2]);
     sched_fence();
     src.keys4(raw[1], sh, key + 4);
+    sched_fence();
+    load_one(src, n, G, pass, 3, raw[3]);
+    sched_fence();
     src.keys4(raw[2], sh, key + 8);
     // The bar comes from the first three chunks, so it is ready while the
     // last chunk is still in flight; every element (the last chunk's too)
@@ -396,8 +400,10 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
   // Each element's rank (the number of larger entries; composites are
   // distinct, so ranks are 0..cnt-1) is counted by tpe consecutive lanes,
   // each over a slice of the list, and summed with lane exchanges.
+  // Short lists (the common case) take one lane per element: no exchanges.
   int tpe = 1;
-  while (tpe < kWave && 2 * tpe * cnt <= kBlock) tpe *= 2;
+  if (cnt > 128)
+    while (tpe < kWave && 2 * tpe * cnt <= kBlock) tpe *= 2;
   const int e = threadIdx.x / tpe, part = threadIdx.x & (tpe - 1);
   const int per = (cnt + tpe - 1) / tpe;
   uint64_t x = 0;
@@ -694,7 +700,7 @@ SelectPlan plan_select(int64_t n, int32_t n_theta, int32_t B) {
   int lg = 0;
   while ((2 << lg) <= m) ++lg;
   p.lg = lg;
-  int M = pow2_ceil(8 * per);
+  int M = pow2_ceil(4 * per);
   if (M < 16) M = 16;
   const int cap = kMergeCap / p.G;
   if (M > cap) M = cap;
