@@ -8,7 +8,7 @@
  *                    -> contiguous queue intervals (Section 4.2, Stages 1-3,
  *                    Eq. 2 split test, Eq. 3 scheduling utility).
  *   ewsjf_route      Dynamic Queue Routing: each request -> the one queue whose
- *                    interval holds its prompt length (Section 3.3 Dispatcher;
+ *                    interval holds its prompt length (Section 3.2 Dispatcher;
  *                    Section 5, deterministic routing over contiguous,
  *                    non-overlapping intervals).
  *   ewsjf_score      Density-Weighted Scoring Phi(r, q) of every request

@@ -14,7 +14,7 @@
 //     lengths into contiguous queue intervals (Section 4.2, Stages 1-3,
 //     Eq. 2 and Eq. 3).
 //   * Dynamic Queue Routing of each request to the one interval containing
-//     its prompt length (Section 3.3 "Dispatcher"; Section 5 "Stability and
+//     its prompt length (Section 3.2 "Dispatcher"; Section 5 "Stability and
 //     Correctness").
 //   * Density-Weighted Scoring Phi(r, q) (Eq. 1 / Eq. 4) with the affine
 //     context-aware weights of the meta-policy (Section 4.1, Section 4.4.1).
@@ -257,7 +257,7 @@ bool params_ok(int64_t n, int32_t init_mode, int32_t init_queues, int32_t max_qu
   return true;
 }
 
-// Route one prompt length (Section 3.3 "Dispatcher").  The queues form a
+// Route one prompt length (Section 3.2 "Dispatcher").  The queues form a
 // contiguous cover of the length axis: bounds[i] is the smallest window
 // length of queue i+1, queue 0 extends down to 1 and the last queue up
 // without limit, so each length b >= 1 lies in exactly one interval.

@@ -8,7 +8,7 @@
 namespace ewsjf {
 
 // lut[b] = number of bounds <= b, i.e. the queue holding length b (contiguous
-// cover of the length axis; Section 3.3 Dispatcher).
+// cover of the length axis; Section 3.2 Dispatcher).
 __global__ void build_lut_kernel(ewsjf_queue_table* tab) {
   const int L = tab->max_len;
   const int nb = tab->k - 1;
