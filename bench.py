@@ -209,6 +209,7 @@ def streaming_bench(steps: int):
             "after_repartition_p50_us": float(np.median(rp)) if rp.size else None,
             "latency": "device time from the step's first insert copy to the end of its admission, "
                        "steps 100.. (steps before 100 are warm-up)",
+            "percentiles_us": {str(q): float(np.percentile(steady, q)) for q in (10, 25, 50, 75, 90, 95, 99)},
             "slowest_steps": [[int(i), float(lat[i])] for i in np.argsort(lat)[::-1][:8]]}
 
 

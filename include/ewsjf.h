@@ -18,6 +18,8 @@
  *   ewsjf_select     Top-B admission: the B admissible requests with the highest
  *                    score, ties to the lowest request id.
  *   ewsjf_step       route + score + select fused into one pass over the pool.
+ *   ewsjf_ring_insert  new requests into a ring pool and the partition window
+ *                    (the streaming scheduler's per-step update).
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -208,6 +210,21 @@ ewsjf_status ewsjf_step_timed(int32_t* len, const float* arrival, int64_t n, flo
                               const ewsjf_theta* theta, int32_t n_theta, const ewsjf_cost* cost, int32_t B,
                               int32_t flags, int32_t* ids, float* top, int32_t* n_sel, void* ws, size_t ws_bytes,
                               hipStream_t stream, hipEvent_t* marks);
+
+/* Streaming pool update: the tactical loop admits from a pool that new
+ * requests keep joining (Section 3.2), and the strategic loop partitions a
+ * window of the most recent request lengths (Section 3.1; Section 4.2).  One
+ * launch writes n new requests into ring slots (pos + i) mod capacity
+ * (ring_len, ring_arrival), overwriting whatever those slots held, and their
+ * lengths into window slots (wpos + i) mod window_cap.
+ * ring_len, ring_arrival: device [capacity]; window: device int32 [window_cap]
+ * (may be NULL with window_cap == 0); new_len, new_arrival: device [n].
+ * 0 <= pos < capacity, 0 <= wpos < max(window_cap, 1), n <= capacity and
+ * n <= window_cap when a window is given; otherwise EWSJF_ERR_ARG.  The new
+ * arrays must not overlap the ring or the window.  No alignment requirement. */
+ewsjf_status ewsjf_ring_insert(int32_t* ring_len, float* ring_arrival, int64_t capacity, int64_t pos,
+                               int32_t* window, int64_t window_cap, int64_t wpos, const int32_t* new_len,
+                               const float* new_arrival, int64_t n, hipStream_t stream);
 
 /* Human-readable name of a status code (static storage). */
 const char* ewsjf_status_string(ewsjf_status s);

@@ -19,8 +19,8 @@ STEP_TOMBSTONE = 1
 OP_PARTITION, OP_SELECT, OP_STEP = 0, 1, 2
 
 EXPORTED = ("ewsjf_queue_table_bytes", "ewsjf_workspace_bytes", "ewsjf_table_upload", "ewsjf_partition",
-            "ewsjf_route", "ewsjf_score", "ewsjf_select", "ewsjf_step", "ewsjf_step_timed", "ewsjf_status_string",
-            "ewsjf_version")
+            "ewsjf_route", "ewsjf_score", "ewsjf_select", "ewsjf_step", "ewsjf_step_timed", "ewsjf_ring_insert",
+            "ewsjf_status_string", "ewsjf_version")
 
 
 class PartitionParams(C.Structure):
@@ -78,6 +78,8 @@ def lib():
         L.ewsjf_step_timed.argtypes = [vp, vp, i64, f32, vp, vp, i32, C.POINTER(Cost), i32, i32, vp, vp, vp, vp, sz,
                                        vp, vp]
         L.ewsjf_step_timed.restype = C.c_int
+        L.ewsjf_ring_insert.argtypes = [vp, vp, i64, i64, vp, i64, i64, vp, vp, i64, vp]
+        L.ewsjf_ring_insert.restype = C.c_int
         L.ewsjf_status_string.argtypes = [C.c_int]
         L.ewsjf_status_string.restype = C.c_char_p
         L.ewsjf_version.argtypes = []

@@ -127,6 +127,23 @@ ewsjf_status ewsjf_partition(const int32_t* window, int64_t n_window, const ewsj
       ewsjf::launch_partition(window, n_window, *p, static_cast<ewsjf_queue_table*>(table), ws, stream));
 }
 
+ewsjf_status ewsjf_ring_insert(int32_t* ring_len, float* ring_arrival, int64_t capacity, int64_t pos,
+                               int32_t* window, int64_t window_cap, int64_t wpos, const int32_t* new_len,
+                               const float* new_arrival, int64_t n, hipStream_t stream) {
+  if (n > 0 && (ring_len == nullptr || ring_arrival == nullptr || new_len == nullptr || new_arrival == nullptr))
+    return EWSJF_ERR_NULL;
+  if (window_cap > 0 && window == nullptr) return EWSJF_ERR_NULL;
+  if (capacity < 1 || capacity > kMaxN || pos < 0 || pos >= capacity || n < 0 || n > capacity) return EWSJF_ERR_ARG;
+  if (window_cap < 0 || window_cap > kMaxN || wpos < 0 || (window_cap > 0 && (wpos >= window_cap || n > window_cap)) ||
+      (window_cap == 0 && wpos != 0))
+    return EWSJF_ERR_ARG;
+  if (n == 0) return EWSJF_OK;
+  const ewsjf_status ds = check_device();
+  if (ds != EWSJF_OK) return ds;
+  return launched(ewsjf::launch_ring_insert(ring_len, ring_arrival, capacity, pos, window, window_cap, wpos, new_len,
+                                            new_arrival, n, stream));
+}
+
 ewsjf_status ewsjf_route(const int32_t* len, int64_t n, const void* table, int32_t* qid, hipStream_t stream) {
   if (table == nullptr || (n > 0 && (len == nullptr || qid == nullptr))) return EWSJF_ERR_NULL;
   if (n < 0 || n > kMaxN) return EWSJF_ERR_ARG;

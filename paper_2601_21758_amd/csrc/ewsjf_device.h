@@ -17,6 +17,7 @@ constexpr int kElemsPerLane = 4 * kChunksPerPass;
 constexpr int kMaxGrid = 256;                // streaming workgroups (one per CU)
 constexpr int kListCap = 1024;               // per-workgroup candidate list in LDS
 constexpr int kWaveCap = kListCap / (kBlock / kWave);  // one region of the list per wave
+constexpr int kOverCap = 128;                // overflow entries kept per workgroup
 constexpr int kStageWaves = 4;                // waves that stage the per-workgroup tables
 constexpr int kStageThreads = kStageWaves * kWave;
 constexpr int kMergeCap = 9088;              // merge kernel candidate capacity (LDS, >= 2 * kSortMax)
@@ -240,6 +241,21 @@ __device__ __forceinline__ uint32_t wave_group_bar(uint32_t x, int lg) {
   x = max(x, xor_lane_u32<32>(x));
   if (s == 6) x = 0u - x;
   return 0u - x;
+}
+
+// The k-th largest (k >= 1) of the wave's kElemsPerLane * 64 keys (0 when
+// fewer than k keys are nonzero): the largest v with at least k keys >= v,
+// found bit by bit from the top with wave-wide counts.
+__device__ inline uint32_t wave_kth_largest(const uint32_t* key, int k) {
+  uint32_t prefix = 0;
+  for (int bit = 31; bit >= 0; --bit) {
+    const uint32_t cand = prefix | (1u << bit);
+    uint32_t c = 0;
+#pragma unroll
+    for (int e = 0; e < kElemsPerLane; ++e) c += key[e] >= cand ? 1u : 0u;
+    if ((int)__ockl_wfred_add_u32(c) >= k) prefix = cand;
+  }
+  return prefix;
 }
 
 // Number of lanes below this one whose bit is set in the wave mask sm.

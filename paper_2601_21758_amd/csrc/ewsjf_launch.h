@@ -16,7 +16,20 @@ struct SelectPlan {
   int lg = 2;       // log2 of the lane groups per wave that set the candidate bar
   int M = 16;       // list entries kept per workgroup
   int n_theta = 1;
-  size_t lists_bytes = 0, counts_bytes = 0, bounds_bytes = 0, ws_bytes = 0;
+  size_t lists_bytes = 0, counts_bytes = 0, bounds_bytes = 0;
+  size_t over_bytes = 0, over_cnt_bytes = 0, bounds2_bytes = 0;
+  size_t ws_bytes = 0;
+};
+
+// Per-workgroup candidate buffers in the step/select workspace, indexed by
+// slot = theta * G + workgroup.
+struct CandBufs {
+  uint64_t* lists;     // [slot][M]: the M largest composites (0 = empty)
+  uint32_t* counts;    // [slot]
+  uint64_t* bounds;    // [slot]: every composite >= bound of the share is in its M slots
+  uint64_t* over;      // [slot][kOverCap]: the next entries below the M slots
+  uint32_t* over_cnt;  // [slot]
+  uint64_t* bounds2;   // [slot]: every composite >= bound2 is in the slots or the overflow
 };
 
 SelectPlan plan_select(int64_t n, int32_t n_theta, int32_t B);
@@ -40,6 +53,9 @@ hipError_t launch_score(const int32_t* len, const float* arrival, int64_t n, flo
 
 // Builds the routing lut of a device table whose header and bounds are set.
 hipError_t launch_build_lut(ewsjf_queue_table* table, hipStream_t stream);
+hipError_t launch_ring_insert(int32_t* ring_len, float* ring_arrival, int64_t capacity, int64_t pos, int32_t* window,
+                              int64_t window_cap, int64_t wpos, const int32_t* new_len, const float* new_arrival,
+                              int64_t n, hipStream_t stream);
 
 // Refine-and-Prune.
 size_t partition_ws_bytes(int64_t n_window, const ewsjf_partition_params& p);

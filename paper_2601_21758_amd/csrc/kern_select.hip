@@ -240,10 +240,7 @@ __device__ __forceinline__ void load_one(const Src& src, int64_t n, int G, int p
 __device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
 
 template <class Src>
-__global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, int G, int lg, int M,
-                                                           uint64_t* __restrict__ lists,
-                                                           uint32_t* __restrict__ counts,
-                                                           uint64_t* __restrict__ bounds) {
+__global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, int G, int lg, int M, CandBufs cb) {
   __shared__ typename Src::Shared sh;
   __shared__ ListShared ls;
   const int t = blockIdx.y;
@@ -319,16 +316,35 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
     my_bar = bar > my_bar ? bar : my_bar;
     // Per element slot: one compare; the wave's mask of qualifying lanes
     // gives each lane its position, and the wave-uniform count advances.
-    const uint32_t thr = my_bar > 1u ? my_bar : 1u;
+    const int wcnt0 = wcnt;
+    auto emit = [&](uint32_t thr) {
 #pragma unroll
-    for (int e = 0; e < kElemsPerLane; ++e) {
-      const bool p = key[e] >= thr;
-      const uint64_t sm = __ballot(p);
-      if (sm != 0ull) {
-        const int pos = wcnt + lanes_below(sm);
-        if (p && pos < kWaveCap)
-          region[pos] = make_comp(key[e], (uint32_t)(chunk_of(G, pass, e / 4) * kChunk + lane * 4 + (e & 3)));
-        wcnt += __popcll(sm);
+      for (int e = 0; e < kElemsPerLane; ++e) {
+        const bool p = key[e] >= thr;
+        const uint64_t sm = __ballot(p);
+        if (sm != 0ull) {
+          const int pos = wcnt + lanes_below(sm);
+          if (p && pos < kWaveCap)
+            region[pos] = make_comp(key[e], (uint32_t)(chunk_of(G, pass, e / 4) * kChunk + lane * 4 + (e & 3)));
+          wcnt += __popcll(sm);
+        }
+      }
+    };
+    emit(my_bar > 1u ? my_bar : 1u);
+    if (wcnt > kWaveCap) {
+      // Too many keys at or above the bar (data whose high keys cluster in
+      // this wave): raise the bar just above the (room)-th largest key, so
+      // fewer than `room` keys qualify, and emit again.  Only equal keys
+      // beyond the room can still overflow (then the list is marked
+      // incomplete and the merge re-reads the share).
+      const int room = kWaveCap - wcnt0;
+      if (room > 0) {
+        const uint32_t kth = wave_kth_largest(key, room);
+        if (kth != 0xFFFFFFFFu) {
+          my_bar = kth + 1u > my_bar ? kth + 1u : my_bar;
+          wcnt = wcnt0;
+          emit(my_bar);
+        }
       }
     }
     if (wcnt > kWaveCap) {
@@ -361,12 +377,15 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
 
   // Publish into the workgroup's M fixed slots (unused slots hold 0).
   const size_t slot = (size_t)t * G + blockIdx.x;
-  uint64_t* out_list = lists + slot * (size_t)M;
+  uint64_t* out_list = cb.lists + slot * (size_t)M;
+  uint64_t* over_list = cb.over + slot * (size_t)kOverCap;
   if (ls.ovf != 0) {
     for (int i = threadIdx.x; i < M; i += kBlock) out_list[i] = 0ull;
     if (threadIdx.x == 0) {
-      counts[slot] = 0u;
-      bounds[slot] = ~0ull;  // nothing guaranteed: the merge re-reads this share
+      cb.counts[slot] = 0u;
+      cb.bounds[slot] = ~0ull;  // nothing guaranteed: the merge re-reads this share
+      cb.bounds2[slot] = ~0ull;
+      cb.over_cnt[slot] = 0u;
     }
     return;
   }
@@ -391,8 +410,10 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
   if (cnt <= M) {
     for (int i = threadIdx.x; i < M; i += kBlock) out_list[i] = i < cnt ? ls.list2[i] : 0ull;
     if (threadIdx.x == 0) {
-      counts[slot] = (uint32_t)cnt;
-      bounds[slot] = lowc;
+      cb.counts[slot] = (uint32_t)cnt;
+      cb.bounds[slot] = lowc;
+      cb.bounds2[slot] = lowc;
+      cb.over_cnt[slot] = 0u;
     }
     return;
   }
@@ -415,13 +436,20 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
     for (int j = j0; j < j1; ++j) rank += ls.list2[j] > x;
   }
   for (int o = 1; o < tpe; o <<= 1) rank += (int)xor_lane_u32_dyn((uint32_t)rank, o);
+  // The entries ranked below the M slots go to the overflow list (up to
+  // kOverCap of them), which the merge reads before it would re-read the
+  // share from the pool.
+  const int listed = min(cnt, M + kOverCap);
   if (e < cnt && part == 0) {
     if (rank < M) out_list[rank] = x;
+    else if (rank < listed) over_list[rank - M] = x;
     if (rank == M - 1) {
-      counts[slot] = (uint32_t)M;
-      bounds[slot] = x > lowc ? x : lowc;
+      cb.counts[slot] = (uint32_t)M;
+      cb.bounds[slot] = x > lowc ? x : lowc;
     }
+    if (rank == listed - 1) cb.bounds2[slot] = (cnt <= M + kOverCap || x < lowc) ? lowc : x;
   }
+  if (threadIdx.x == 0) cb.over_cnt[slot] = (uint32_t)(listed - M);
 }
 
 // ---------------------------------------------------------------------------
@@ -479,16 +507,66 @@ __device__ inline int select_top(MergeShared& ms, int U, int B) {
   return nS < B ? nS : B;
 }
 
+// Count of entries greater than v in the descending array a[0..len).
+__device__ __forceinline__ int count_greater_desc(const uint64_t* a, int len, uint64_t v) {
+  int lo = 0, hi = len;
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (a[mid] > v)
+      lo = mid + 1;
+    else
+      hi = mid;
+  }
+  return lo;
+}
+
+// X[0..U0) holds the current top entries sorted descending, S[0..k) new
+// entries (distinct from them).  Leaves the top min(B, U0 + k) of both
+// sorted in X and returns that count.  A short S is sorted by rank counting
+// and merged by binary searches; a long one goes through select_top.
+constexpr int kMergeNewRank = 512;
+__device__ inline int merge_new(MergeShared& ms, int U0, int k, int B) {
+  const int tid = threadIdx.x;
+  if (k == 0) return U0;
+  if (k > kMergeNewRank || U0 + k > kMergeCap) {
+    for (int i = tid; i < k; i += kBlock) ms.X[U0 + i] = ms.S[i];
+    __syncthreads();
+    return select_top(ms, U0 + k, B);
+  }
+  for (int e = tid; e < k; e += kBlock) {
+    const uint64_t y = ms.S[e];
+    int r = 0;
+#pragma unroll 8
+    for (int j = 0; j < k; ++j) r += ms.S[j] > y;
+    ms.X[U0 + r] = y;
+  }
+  __syncthreads();
+  const int total = U0 + k < B ? U0 + k : B;
+  const uint64_t* N = ms.X + U0;
+  for (int i = tid; i < U0; i += kBlock) {
+    const uint64_t x = ms.X[i];
+    const int r = i + count_greater_desc(N, k, x);
+    if (r < total) ms.S[r] = x;
+  }
+  for (int j = tid; j < k; j += kBlock) {
+    const uint64_t y = N[j];
+    const int r = j + count_greater_desc(ms.X, U0, y);
+    if (r < total) ms.S[r] = y;
+  }
+  __syncthreads();
+  for (int i = tid; i < total; i += kBlock) ms.X[i] = ms.S[i];
+  __syncthreads();
+  return total;
+}
+
 template <class Src>
-__global__ __launch_bounds__(kBlock) void merge_candidates(Src src0, int64_t n, int G, int M, int B,
-                                                           const uint64_t* __restrict__ lists,
-                                                           const uint32_t* __restrict__ counts,
-                                                           const uint64_t* __restrict__ bounds,
+__global__ __launch_bounds__(kBlock) void merge_candidates(Src src0, int64_t n, int G, int M, int B, CandBufs cb,
                                                            int32_t* __restrict__ ids, float* __restrict__ top,
                                                            int32_t* __restrict__ n_sel, int32_t* tomb_len) {
   __shared__ MergeShared ms;
   __shared__ typename Src::Shared sh;
   __shared__ uint64_t sT[kMaxGrid];
+  __shared__ uint64_t sT2[kMaxGrid];
   const int t = blockIdx.x;
   const int tid = threadIdx.x;
   const Src src = bind_theta(src0, t);
@@ -501,15 +579,19 @@ __global__ __launch_bounds__(kBlock) void merge_candidates(Src src0, int64_t n, 
   const int lane = tid & (kWave - 1), wv = tid / kWave;
   const int GM = G * M;
   const __amdgpu_buffer_rsrc_t lrs = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint64_t*>(lists + slot0 * (size_t)M), (short)0, GM * 8, kBufferWord3);
-  const uint64_t Tw = tid < G ? bounds[slot0 + tid] : 0ull;
+      cb.lists + slot0 * (size_t)M, (short)0, GM * 8, kBufferWord3);
+  const uint64_t Tw = tid < G ? cb.bounds[slot0 + tid] : 0ull;
+  const uint64_t Tw2 = tid < G ? cb.bounds2[slot0 + tid] : 0ull;
   uint64_t v[kR];
 #pragma unroll
   for (int r = 0; r < kR; ++r) {
     const auto w = __builtin_amdgcn_raw_buffer_load_b64(lrs, (tid + r * kBlock) * 8, 0, kCachePolicyNT);
     v[r] = ((uint64_t)w[1] << 32) | w[0];
   }
-  if (tid < G) sT[tid] = Tw;
+  if (tid < G) {
+    sT[tid] = Tw;
+    sT2[tid] = Tw2;
+  }
   // Exact range and count of the candidates (registers -> wave -> LDS)
   // while the slots go to LDS and the histogram is cleared.
   uint64_t mx = 0, mn = ~0ull;
@@ -604,62 +686,79 @@ __global__ __launch_bounds__(kBlock) void merge_candidates(Src src0, int64_t n, 
   }
   uint64_t tau = (U >= B) ? ms.X[B - 1] : 0ull;
 
-  // Re-read shares whose lists could miss top-B members (rare).
+  // Shares whose slots could miss top-B members (rare), largest bound first:
+  // each adds its entries in [cut, bound) -- from its overflow list when that
+  // reaches down to the cut, else re-read from the pool -- and the cut is
+  // raised right away, so later shares often drop out.  X[0..U) is sorted.
   bool staged = false;
-  const uint64_t thr0 = tau > 1ull ? tau : 1ull;
-  // Every wave reads all G bounds itself, so the answer is uniform across
-  // the block without a barrier.
-  bool risk_lane = false;
-  for (int w = lane; w < G; w += kWave) risk_lane |= sT[w] > thr0;
-  const bool any_risk = __ballot(risk_lane) != 0ull;
-  for (int w = 0; any_risk && w < G; ++w) {
+  for (;;) {
     const uint64_t thr = tau > 1ull ? tau : 1ull;
-    if (!(sT[w] > thr)) continue;
-    if (!staged) {
-      if (tid < kStageThreads) {
-        typename Src::Stage st;
-        src.stage_load(st, t);
-        src.stage_store(sh, st);
+    // The share with the largest bound; every wave finds it from LDS itself,
+    // so the decision is uniform without a barrier.
+    uint64_t bl = 0;
+    int wl = 0x7fffffff;
+    for (int w = lane; w < G; w += kWave)
+      if (sT[w] > bl) {
+        bl = sT[w];
+        wl = w;
+      }
+    const uint64_t best = wave_max_u64(bl);
+    if (best <= thr) break;
+    const int wbest = __builtin_amdgcn_readlane(wl, (int)__builtin_ctzll(__ballot(bl == best)));
+    if (tid == 0) ms.cntS = 0;
+    __syncthreads();
+    if (sT2[wbest] <= thr) {
+      const uint64_t* ov = cb.over + (slot0 + wbest) * (size_t)kOverCap;
+      const int oc = (int)cb.over_cnt[slot0 + wbest];
+      if (tid < oc) {
+        const uint64_t x = ov[tid];
+        if (x >= thr && x < best) ms.S[atomicAdd(&ms.cntS, 1)] = x;
       }
       __syncthreads();
-      staged = true;
-    }
-    const uint64_t Tcut = sT[w];
-    const int64_t nchunks = (n + kChunk - 1) / kChunk;
-    // All chunks of share w: c = w + G * lc, lc = 0, 1, ...; a chunk per wave,
-    // 4 requests per lane.
-    for (int64_t lc0 = 0;; lc0 += kWavesPerBlock) {
-      const int64_t first_c = (int64_t)w + (int64_t)G * lc0;
-      if (first_c >= nchunks) break;
-      if (U + kBlock * 4 > kMergeCap) {
-        U = select_top(ms, U, B);
-        tau = (U >= B) ? ms.X[B - 1] : 0ull;
+      U = merge_new(ms, U, ms.cntS, B);
+    } else {
+      if (!staged) {
+        if (tid < kStageThreads) {
+          typename Src::Stage st;
+          src.stage_load(st, t);
+          src.stage_store(sh, st);
+        }
+        __syncthreads();
+        staged = true;
       }
-      if (tid == 0) ms.cntX = U;
-      __syncthreads();
-      const int lane = tid & (kWave - 1), wv = tid / kWave;
-      const int64_t cidx = (int64_t)w + (int64_t)G * (lc0 + wv);
-      const int64_t b0 = cidx < nchunks ? cidx * kChunk + (int64_t)lane * 4 : n;
-      const typename Src::Raw r = src.load4(b0, n);
-      uint32_t k4[4];
-      src.keys4(r, sh, k4);
-      const uint64_t lowb = tau > 1ull ? tau : 1ull;
+      const int64_t nchunks = (n + kChunk - 1) / kChunk;
+      // All chunks of share wbest: c = wbest + G * lc, lc = 0, 1, ...; a chunk
+      // per wave, 4 requests per lane.
+      for (int64_t lc0 = 0;; lc0 += kWavesPerBlock) {
+        const int64_t first_c = (int64_t)wbest + (int64_t)G * lc0;
+        if (first_c >= nchunks) break;
+        if (lc0 > 0) {  // at most kBlock * 4 = kSortMax new entries per round
+          U = merge_new(ms, U, ms.cntS, B);
+          tau = (U >= B) ? ms.X[B - 1] : 0ull;
+          if (tid == 0) ms.cntS = 0;
+          __syncthreads();
+        }
+        const int64_t cidx = (int64_t)wbest + (int64_t)G * (lc0 + wv);
+        const int64_t b0 = cidx < nchunks ? cidx * kChunk + (int64_t)lane * 4 : n;
+        const typename Src::Raw r = src.load4(b0, n);
+        uint32_t k4[4];
+        src.keys4(r, sh, k4);
+        const uint64_t lowb = tau > 1ull ? tau : 1ull;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        if (k4[e] != 0u && b0 + e < n) {
-          const uint64_t x = make_comp(k4[e], (uint32_t)(b0 + e));
-          if (x >= lowb && x < Tcut) {
-            const int p = atomicAdd(&ms.cntX, 1);
-            ms.X[p] = x;
+        for (int e = 0; e < 4; ++e) {
+          if (k4[e] != 0u && b0 + e < n) {
+            const uint64_t x = make_comp(k4[e], (uint32_t)(b0 + e));
+            if (x >= lowb && x < best) ms.S[atomicAdd(&ms.cntS, 1)] = x;
           }
         }
+        __syncthreads();
       }
-      __syncthreads();
-      U = ms.cntX;
-      __syncthreads();
+      U = merge_new(ms, U, ms.cntS, B);
     }
+    tau = (U >= B) ? ms.X[B - 1] : 0ull;
+    if (tid == 0) sT[wbest] = 0ull;  // done
+    __syncthreads();
   }
-  if (staged) U = select_top(ms, U, B);
 
   // Publish.
   const int sel = U < B ? U : B;
@@ -710,17 +809,32 @@ SelectPlan plan_select(int64_t n, int32_t n_theta, int32_t B) {
   p.lists_bytes = (size_t)n_theta * p.G * p.M * sizeof(uint64_t);
   p.counts_bytes = (size_t)n_theta * p.G * sizeof(uint32_t);
   p.bounds_bytes = (size_t)n_theta * p.G * sizeof(uint64_t);
+  p.over_bytes = (size_t)n_theta * p.G * kOverCap * sizeof(uint64_t);
+  p.over_cnt_bytes = (size_t)n_theta * p.G * sizeof(uint32_t);
+  p.bounds2_bytes = (size_t)n_theta * p.G * sizeof(uint64_t);
   auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
-  p.ws_bytes = up(p.lists_bytes) + up(p.counts_bytes) + up(p.bounds_bytes);
+  p.ws_bytes = up(p.lists_bytes) + up(p.counts_bytes) + up(p.bounds_bytes) + up(p.over_bytes) +
+               up(p.over_cnt_bytes) + up(p.bounds2_bytes);
   return p;
 }
 
-static void carve(const SelectPlan& p, void* ws, uint64_t** lists, uint32_t** counts, uint64_t** bounds) {
+static CandBufs carve(const SelectPlan& p, void* ws) {
   auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
   char* b = static_cast<char*>(ws);
-  *lists = reinterpret_cast<uint64_t*>(b);
-  *counts = reinterpret_cast<uint32_t*>(b + up(p.lists_bytes));
-  *bounds = reinterpret_cast<uint64_t*>(b + up(p.lists_bytes) + up(p.counts_bytes));
+  CandBufs c;
+  size_t o = 0;
+  c.lists = reinterpret_cast<uint64_t*>(b + o);
+  o += up(p.lists_bytes);
+  c.counts = reinterpret_cast<uint32_t*>(b + o);
+  o += up(p.counts_bytes);
+  c.bounds = reinterpret_cast<uint64_t*>(b + o);
+  o += up(p.bounds_bytes);
+  c.over = reinterpret_cast<uint64_t*>(b + o);
+  o += up(p.over_bytes);
+  c.over_cnt = reinterpret_cast<uint32_t*>(b + o);
+  o += up(p.over_cnt_bytes);
+  c.bounds2 = reinterpret_cast<uint64_t*>(b + o);
+  return c;
 }
 
 hipError_t launch_step(const int32_t* len, const float* arrival, int64_t n, float now,
@@ -728,10 +842,7 @@ hipError_t launch_step(const int32_t* len, const float* arrival, int64_t n, floa
                        const ewsjf_cost& cost, int32_t B, int32_t* tomb_len, int32_t* ids, float* top,
                        int32_t* n_sel, void* ws, hipStream_t stream, hipEvent_t* marks) {
   const SelectPlan p = plan_select(n, n_theta, B);
-  uint64_t* lists;
-  uint32_t* counts;
-  uint64_t* bounds;
-  carve(p, ws, &lists, &counts, &bounds);
+  const CandBufs cb = carve(p, ws);
   PoolSource src;
   src.len = len;
   src.arrival = arrival;
@@ -741,40 +852,37 @@ hipError_t launch_step(const int32_t* len, const float* arrival, int64_t n, floa
   src.cost = CostF{(float)cost.c0, (float)cost.c1, (float)cost.c2};
   if (marks == nullptr) {
     hipLaunchKernelGGL(local_candidates<PoolSource>, dim3(p.G, n_theta), dim3(kBlock), 0, stream, src, n, p.G,
-                       p.lg, p.M, lists, counts, bounds);
+                       p.lg, p.M, cb);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(merge_candidates<PoolSource>, dim3(n_theta), dim3(kBlock), 0, stream, src, n, p.G, p.M,
-                       B, lists, counts, bounds, ids, top, n_sel, tomb_len);
+                       B, cb, ids, top, n_sel, tomb_len);
     return hipGetLastError();
   }
   // The events take the start and end timestamps of each kernel's own
   // dispatch.
   hipExtLaunchKernelGGL(local_candidates<PoolSource>, dim3(p.G, n_theta), dim3(kBlock), 0, stream, marks[0],
-                        marks[1], 0, src, n, p.G, p.lg, p.M, lists, counts, bounds);
+                        marks[1], 0, src, n, p.G, p.lg, p.M, cb);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipExtLaunchKernelGGL(merge_candidates<PoolSource>, dim3(n_theta), dim3(kBlock), 0, stream, marks[2], marks[3],
-                        0, src, n, p.G, p.M, B, lists, counts, bounds, ids, top, n_sel, tomb_len);
+                        0, src, n, p.G, p.M, B, cb, ids, top, n_sel, tomb_len);
   return hipGetLastError();
 }
 
 hipError_t launch_select(const float* score, int64_t n, int32_t n_theta, int32_t B, int32_t* ids, float* top,
                          int32_t* n_sel, void* ws, hipStream_t stream) {
   const SelectPlan p = plan_select(n, n_theta, B);
-  uint64_t* lists;
-  uint32_t* counts;
-  uint64_t* bounds;
-  carve(p, ws, &lists, &counts, &bounds);
+  const CandBufs cb = carve(p, ws);
   ScoreSource src;
   src.score = score;
   src.n = n;
   hipLaunchKernelGGL(local_candidates<ScoreSource>, dim3(p.G, n_theta), dim3(kBlock), 0, stream, src, n, p.G,
-                     p.lg, p.M, lists, counts, bounds);
+                     p.lg, p.M, cb);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(merge_candidates<ScoreSource>, dim3(n_theta), dim3(kBlock), 0, stream, src, n, p.G, p.M,
-                     B, lists, counts, bounds, ids, top, n_sel, nullptr);
+                     B, cb, ids, top, n_sel, nullptr);
   return hipGetLastError();
 }
 

@@ -193,3 +193,20 @@ def step(length: torch.Tensor, arrival: torch.Tensor, now: float, table: torch.T
                                int(B), flags, _vp(ids), _vp(top), _vp(nsel), _vp(buf), buf.numel(), _stream(stream)),
             "ewsjf_step")
     return ids, top, nsel
+
+
+def ring_insert(ring_len: torch.Tensor, ring_arrival: torch.Tensor, pos: int, new_len: torch.Tensor,
+                new_arrival: torch.Tensor, window: torch.Tensor | None = None, wpos: int = 0, stream=None) -> None:
+    """Write new requests into ring slots (pos + i) mod capacity and their
+    lengths into window slots (wpos + i) mod len(window), in one launch."""
+    _need(ring_len, torch.int32, "ring_len")
+    _need(ring_arrival, torch.float32, "ring_arrival")
+    _need(new_len, torch.int32, "new_len")
+    _need(new_arrival, torch.float32, "new_arrival")
+    if window is not None:
+        _need(window, torch.int32, "window")
+    wv = _vp(window) if window is not None else C.c_void_p(None)
+    wc = window.numel() if window is not None else 0
+    L.check(L.lib().ewsjf_ring_insert(_vp(ring_len), _vp(ring_arrival), ring_len.numel(), int(pos), wv, wc,
+                                      int(wpos), _vp(new_len), _vp(new_arrival), new_len.numel(), _stream(stream)),
+            "ewsjf_ring_insert")

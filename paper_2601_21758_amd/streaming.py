@@ -10,8 +10,8 @@ takes effect at step s + 1: the paper runs the partitioner off the
 critical path, in the strategic loop (Section 3.1; Section 5), over a window
 of recent requests (Section 4.2).
 
-The ring and window updates are device-to-device copies (memory plumbing);
-every step of the method runs in libewsjf.so's kernels.
+Every step runs in libewsjf.so's kernels: ewsjf_ring_insert, ewsjf_partition
+and ewsjf_step.
 """
 from __future__ import annotations
 
@@ -88,19 +88,9 @@ class StreamingScheduler:
         n = length.numel()
         if arrival.numel() != n or n > self.capacity or n > self.window:
             raise ValueError("one step inserts at most min(capacity, window) arrivals")
-        self._ring_copy(self.len, self.ring_pos, length, self.capacity)
-        self._ring_copy(self.arr, self.ring_pos, arrival, self.capacity)
-        self._ring_copy(self.win, self.win_pos, length, self.window)
+        ewsjf.ring_insert(self.len, self.arr, self.ring_pos, length, arrival, window=self.win, wpos=self.win_pos)
         self.ring_pos = (self.ring_pos + n) % self.capacity
         self.win_pos = (self.win_pos + n) % self.window
-
-    @staticmethod
-    def _ring_copy(dst: torch.Tensor, pos: int, src: torch.Tensor, size: int) -> None:
-        n = src.numel()
-        head = min(n, size - pos)
-        dst[pos:pos + head].copy_(src[:head])
-        if head < n:
-            dst[:n - head].copy_(src[head:])
 
     def launch_repartition(self) -> None:
         """Partition the current window on the side stream; the new table

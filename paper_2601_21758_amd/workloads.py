@@ -219,10 +219,22 @@ def adversarial(kind: str, n: int, seed: int = 0) -> tuple[np.ndarray, np.ndarra
         return l, (rng.random(n) * 60).astype(np.float32), 60.0
     if kind == "future_arrivals":
         return _lengths(rng, n, MIX_TWO), (rng.random(n) * 120).astype(np.float32), 60.0
+    if kind == "oldest_first":
+        # equal lengths and arrivals rising with the id: the scores fall with
+        # the id, so every top request sits in the first few slots
+        return np.full(n, 100, np.int32), np.linspace(0.0, 60.0, n).astype(np.float32), 60.0
+    if kind == "hot_blocks":
+        # a few runs of 300 consecutive slots waited much longer than the rest
+        l = _lengths(rng, n, MIX_TWO)
+        a = (rng.random(n) * 10 + 50).astype(np.float32)
+        for start in rng.integers(0, max(1, n - 300), 6):
+            a[start:start + 300] = (rng.random(min(300, n - start)) * 5).astype(np.float32)
+        return l, a, 60.0
     raise ValueError(kind)
 
 
-ADVERSARIAL_KINDS = ("equal_len", "equal_arrival", "all_equal", "clip_spikes", "tombstones",
+ADVERSARIAL_KINDS = ("equal_len", "equal_arrival", "all_equal", "clip_spikes", "tombstones", "oldest_first",
+                     "hot_blocks",
                      "over_max", "future_arrivals")
 
 

@@ -113,6 +113,26 @@ def test_select_route_score_argument_errors():
     assert lib.ewsjf_score(FAKE, FAKE, 10, 1.0, FAKE, FAKE, 1, C.byref(c), FAKE_MIS, None) == L.ERR_ALIGN
 
 
+def test_ring_insert_argument_errors():
+    lib = L.lib()
+
+    def ins(rl=FAKE, ra=FAKE, cap=100, pos=0, w=FAKE, wc=50, wpos=0, nl=FAKE, na=FAKE, n=10):
+        return lib.ewsjf_ring_insert(rl, ra, cap, pos, w, wc, wpos, nl, na, n, None)
+
+    assert ins(rl=None) == L.ERR_NULL
+    assert ins(na=None) == L.ERR_NULL
+    assert ins(w=None) == L.ERR_NULL            # a window size without a window
+    assert ins(cap=0) == L.ERR_ARG
+    assert ins(pos=100) == L.ERR_ARG            # pos must be a slot
+    assert ins(pos=-1) == L.ERR_ARG
+    assert ins(n=101) == L.ERR_ARG              # more than the ring holds
+    assert ins(n=51) == L.ERR_ARG               # more than the window holds
+    assert ins(wpos=50) == L.ERR_ARG
+    assert ins(w=None, wc=0, wpos=3) == L.ERR_ARG
+    assert ins(n=0) == L.OK                     # nothing to do, no device touched
+    assert ins(rl=None, ra=None, nl=None, na=None, n=0) == L.OK
+
+
 def test_partition_argument_errors():
     lib = L.lib()
     need = lib.ewsjf_workspace_bytes(L.OP_PARTITION, 100, 0, 0, C.byref(_p()))

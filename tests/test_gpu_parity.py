@@ -223,6 +223,18 @@ def test_step_adversarial(E, kind, B):
     check_admission(host(ids)[0], host(top)[0], host(nsel)[0], rids[0], rtop[0], rnsel[0], rs[0])
 
 
+@pytest.mark.parametrize("kind", ["oldest_first", "hot_blocks"])
+def test_step_clustered_on_a_full_grid(E, kind):
+    # 1M requests: 256 workgroups with one chunk per wave, where the top
+    # requests crowd into a few chunks (the merge's recovery path)
+    L, A, now = W.adversarial(kind, 1 << 20, 11)
+    say(f"step clustered {kind} n=1M B=512")
+    t = oracle.partition(np.clip(L, 1, None), init_queues=16, max_queues=16)
+    ids, top, nsel = E.step(dev(L), dev(A), now, upload(E, t), dev(W.THETA_MID), 512)
+    rids, rtop, rnsel, rs = oracle.step(L, A, now, t, W.THETA_MID, 512)
+    check_admission(host(ids)[0], host(top)[0], host(nsel)[0], rids[0], rtop[0], rnsel[0], rs[0])
+
+
 def test_step_small_and_empty_pools(E):
     t = oracle.partition([5, 50, 500], init_queues=2, max_queues=2)
     for n in (0, 1, 3, 4, 5, 63, 255, 257):

@@ -20,12 +20,28 @@ from streaming_ref import OracleStream  # noqa: E402
 
 
 # ---- host-side logic (CPU) ------------------------------------------------------
-def test_ring_copy_wraps():
-    dst = torch.zeros(10, dtype=torch.int32)
-    StreamingScheduler._ring_copy(dst, 7, torch.arange(1, 6, dtype=torch.int32), 10)
-    assert dst.tolist() == [4, 5, 0, 0, 0, 0, 0, 1, 2, 3]
-    StreamingScheduler._ring_copy(dst, 2, torch.arange(6, 9, dtype=torch.int32), 10)
-    assert dst.tolist() == [4, 5, 6, 7, 8, 0, 0, 1, 2, 3]
+@pytest.mark.gpu
+def test_ring_insert_matches_numpy():
+    from paper_2601_21758_amd import ewsjf
+    rng = np.random.default_rng(7)
+    cap, wcap = 1000, 300
+    rl = rng.integers(1, 5000, cap).astype(np.int32)
+    ra = rng.random(cap).astype(np.float32)
+    win = rng.integers(1, 5000, wcap).astype(np.int32)
+    g_rl, g_ra, g_w = (torch.from_numpy(a.copy()).cuda() for a in (rl, ra, win))
+    for pos, wpos, n in [(0, 0, 10), (995, 290, 7), (500, 0, 300), (999, 299, 1), (3, 5, 0)]:
+        nl = rng.integers(1, 5000, n).astype(np.int32)
+        na = rng.random(n).astype(np.float32)
+        ewsjf.ring_insert(g_rl, g_ra, pos, torch.from_numpy(nl).cuda(), torch.from_numpy(na).cuda(), window=g_w,
+                          wpos=wpos)
+        slots = (pos + np.arange(n)) % cap
+        rl[slots] = nl
+        ra[slots] = na
+        win[(wpos + np.arange(n)) % wcap] = nl
+        torch.cuda.synchronize()
+        assert np.array_equal(g_rl.cpu().numpy(), rl)
+        assert np.array_equal(g_ra.cpu().numpy(), ra)
+        assert np.array_equal(g_w.cpu().numpy(), win)
 
 
 def test_reference_ring_and_window_follow_the_generator():
