@@ -213,6 +213,7 @@ struct ListShared {
   uint32_t hist[256];
   uint64_t red[kWavesPerBlock];
   int iscan[kWavesPerBlock];
+  int rank[kShortList];  // ranks of a short list, summed over the waves
   uint32_t bar[kWavesPerBlock];
   int wcnt[kWavesPerBlock];
   int ovf;
@@ -272,6 +273,7 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
     ls.ovf = 0;
     ls.nout = 0;
   }
+  if (threadIdx.x < kShortList) ls.rank[threadIdx.x] = 0;
   __syncthreads();
 
   // Each wave writes every element whose key is >= its bar into its own
@@ -418,10 +420,59 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
     return;
   }
   // Keep exactly the M largest: every element >= the M-th largest is listed.
-  // Each element's rank (the number of larger entries; composites are
-  // distinct, so ranks are 0..cnt-1) is counted by tpe consecutive lanes,
-  // each over a slice of the list, and summed with lane exchanges.
-  // Short lists (the common case) take one lane per element: no exchanges.
+  // Each element's rank is the number of larger entries (composites are
+  // distinct, so ranks are 0..cnt-1).  The entries ranked below the M slots
+  // go to the overflow list (up to kOverCap of them), which the merge reads
+  // before it would re-read the share from the pool.
+  const int listed = min(cnt, M + kOverCap);
+  auto place = [&](uint64_t x, int rank) {
+    if (rank < M) out_list[rank] = x;
+    else if (rank < listed) over_list[rank - M] = x;
+    if (rank == M - 1) {
+      cb.counts[slot] = (uint32_t)M;
+      cb.bounds[slot] = x > lowc ? x : lowc;
+    }
+    if (rank == listed - 1) cb.bounds2[slot] = (cnt <= M + kOverCap || x < lowc) ? lowc : x;
+  };
+  if (cnt <= kShortList) {
+    // The common case: every wave holds all entries (up to 4 per lane),
+    // compares them with its own few (entries w, w + 16, ...) and adds its
+    // counts into LDS, so no wave runs a long serial chain.
+    constexpr int kG = kShortList / kWave;
+    const int ng = (cnt + kWave - 1) / kWave;  // entries per lane in use
+    uint64_t x[kG];
+    int part[kG];
+#pragma unroll
+    for (int g = 0; g < kG; ++g) {
+      x[g] = g < ng && g * kWave + lane < cnt ? ls.list2[g * kWave + lane] : 0ull;
+      part[g] = 0;
+    }
+    // This wave's entries j = wv + 16 i, four reads at a time (an entry past
+    // the list reads as 0, which is never larger).
+    for (int j0 = wv; j0 < cnt; j0 += 4 * kWavesPerBlock) {
+      uint64_t y[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int j = j0 + u * kWavesPerBlock;
+        y[u] = j < cnt ? ls.list2[j] : 0ull;
+      }
+#pragma unroll
+      for (int g = 0; g < kG; ++g)
+        if (g < ng) {
+#pragma unroll
+          for (int u = 0; u < 4; ++u) part[g] += y[u] > x[g];
+        }
+    }
+#pragma unroll
+    for (int g = 0; g < kG; ++g)
+      if (g < ng && g * kWave + lane < cnt && part[g] != 0) atomicAdd(&ls.rank[g * kWave + lane], part[g]);
+    __syncthreads();
+    if (wv < kG && threadIdx.x < cnt) place(ls.list2[threadIdx.x], ls.rank[threadIdx.x]);
+    if (threadIdx.x == 0) cb.over_cnt[slot] = (uint32_t)(listed - M);
+    return;
+  }
+  // Longer lists: tpe consecutive lanes count each element's rank, each over
+  // a slice of the list, and sum with lane exchanges.
   int tpe = 1;
   if (cnt > 128)
     while (tpe < kWave && 2 * tpe * cnt <= kBlock) tpe *= 2;
@@ -436,19 +487,7 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
     for (int j = j0; j < j1; ++j) rank += ls.list2[j] > x;
   }
   for (int o = 1; o < tpe; o <<= 1) rank += (int)xor_lane_u32_dyn((uint32_t)rank, o);
-  // The entries ranked below the M slots go to the overflow list (up to
-  // kOverCap of them), which the merge reads before it would re-read the
-  // share from the pool.
-  const int listed = min(cnt, M + kOverCap);
-  if (e < cnt && part == 0) {
-    if (rank < M) out_list[rank] = x;
-    else if (rank < listed) over_list[rank - M] = x;
-    if (rank == M - 1) {
-      cb.counts[slot] = (uint32_t)M;
-      cb.bounds[slot] = x > lowc ? x : lowc;
-    }
-    if (rank == listed - 1) cb.bounds2[slot] = (cnt <= M + kOverCap || x < lowc) ? lowc : x;
-  }
+  if (e < cnt && part == 0) place(x, rank);
   if (threadIdx.x == 0) cb.over_cnt[slot] = (uint32_t)(listed - M);
 }
 
