@@ -59,6 +59,10 @@ def _declare(L):
     L.oracle_score.restype = None
     L.oracle_select.argtypes = [_p(f32), i64, i32, i32, _p(i32), _p(f32), _p(i32)]
     L.oracle_select.restype = None
+    L.oracle_tactical_step.argtypes = [_p(i32), _p(f32), i64, f32, _p(i32), _p(i32), _p(i64), _p(i64), _p(i32),
+                                       _p(i32), _p(f64), _p(i32), _p(f32), f64, f64, f64, i32, i32, f64,
+                                       _p(i32), _p(i32), _p(i32), _p(f32), _p(i32)]
+    L.oracle_tactical_step.restype = C.c_int
 
 
 def _ptr(a, t):
@@ -205,3 +209,50 @@ def step(length, arrival, now, table: Table, theta, B, cost=(0.01, 1e-4, 0.0)):
     sc = score(length, arrival, now, table, theta, cost)
     ids, top, nsel = select(sc, B)
     return ids, top, nsel, sc
+
+
+@dataclass
+class TacticalResult:
+    ids: np.ndarray         # int32 [n_sel], batch order
+    q_prim: int             # -1 when every queue is empty
+    head_score: np.ndarray  # float32 [k at entry], NaN for empty queues
+    removed: np.ndarray     # bool [k at entry]
+    table: Table            # after this step's removals
+    empty_cnt: np.ndarray   # int32 [k after removals]
+
+
+def tactical_step(length, arrival, now, table: Table, empty_cnt, theta, B, empty_threshold,
+                  cost=(0.01, 1e-4, 0.0), eps=1e-6) -> TacticalResult:
+    """One step of Algorithm 1 (Section 3.2): ArgMax queue, GreedyFill,
+    Backfill from adjacent queues, EmptyThreshold removal."""
+    L = _arr(length, np.int32)
+    A = _arr(arrival, np.float32)
+    k0 = int(table.k)
+    k = np.array([k0], np.int32)
+    bounds = np.zeros(max(1, k0), np.int32)
+    bounds[:k0 - 1] = table.bounds
+    count, ssum = _arr(table.count, np.int64).copy(), _arr(table.sum, np.int64).copy()
+    lo, hi = _arr(table.lo, np.int32).copy(), _arr(table.hi, np.int32).copy()
+    mean = _arr(table.mean, np.float64).copy()
+    ec = _arr(empty_cnt, np.int32).copy()
+    if ec.size != k0:
+        raise ValueError("empty_cnt needs one entry per queue")
+    th = _arr(theta, np.float32).reshape(6)
+    ids = np.zeros(max(1, B), np.int32)
+    nsel = np.zeros(1, np.int32)
+    qp = np.zeros(1, np.int32)
+    hs = np.zeros(k0, np.float32)
+    rm = np.zeros(k0, np.int32)
+    r = lib().oracle_tactical_step(_ptr(L, C.c_int32), _ptr(A, C.c_float), L.size, float(np.float32(now)),
+                                   _ptr(k, C.c_int32), _ptr(bounds, C.c_int32), _ptr(count, C.c_int64),
+                                   _ptr(ssum, C.c_int64), _ptr(lo, C.c_int32), _ptr(hi, C.c_int32),
+                                   _ptr(mean, C.c_double), _ptr(ec, C.c_int32), _ptr(th, C.c_float),
+                                   float(cost[0]), float(cost[1]), float(cost[2]), int(B), int(empty_threshold),
+                                   float(eps), _ptr(ids, C.c_int32), _ptr(nsel, C.c_int32), _ptr(qp, C.c_int32),
+                                   _ptr(hs, C.c_float), _ptr(rm, C.c_int32))
+    if r != 0:
+        raise ValueError("bad tactical-step arguments")
+    k1 = int(k[0])
+    t2 = Table(k1, bounds[:k1 - 1].copy(), count[:k1].copy(), ssum[:k1].copy(), lo[:k1].copy(), hi[:k1].copy(),
+               mean[:k1].copy(), table.n_distinct, table.n_coarse, table.n_leaves)
+    return TacticalResult(ids[:int(nsel[0])].copy(), int(qp[0]), hs, rm.astype(bool), t2, ec[:k1].copy())

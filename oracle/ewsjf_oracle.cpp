@@ -267,6 +267,85 @@ int32_t route_one(int32_t b, const int32_t* bounds, int32_t k) {
   return (int32_t)(std::upper_bound(bounds, bounds + (k - 1), b) - bounds);
 }
 
+
+// ---------------------------------------------------------------------------
+// Algorithm 1 (Section 3.2, "Tactical Loop"): the paper's own batch rule
+// over per-queue FIFOs.
+//
+// Readings (the paper leaves these open):
+//   T1 Each queue is a FIFO of its pending requests in arrival order; equal
+//      arrivals keep request-id order, a NaN arrival counts as +inf and -0
+//      as +0.  peek() is the oldest request.
+//   T2 CalculateScore is Phi (Eq. 1 / Eq. 4) of the head request with the
+//      queue's profile, evaluated exactly as in the per-request scoring
+//      below and rounded once to binary32 (NaN -> -inf).
+//   T3 ArgMax over the non-empty queues; equal scores go to the lower queue
+//      index.
+//   T4 GreedyFill pulls q_prim's requests oldest first until the batch
+//      holds B requests or q_prim is empty.
+//   T5 GetAdjacent(q_prim) = the queues directly below and above q_prim in
+//      length order that are non-empty; Backfill drains them oldest first,
+//      the one with the higher head score first (equal scores: lower index
+//      first), until the batch is full.
+//   T6 empty_cnt counts consecutive steps a queue was empty (a non-empty
+//      step resets it).  Removals are applied after the batch is built
+//      (scores of this step use the queue indices at its start).  The
+//      lowest-index queue past the threshold goes first; it is re-absorbed
+//      by the neighbour whose pair has the lower utility U of Eq. 3 (the
+//      Stage-3 merge rule; equal U: the lower neighbour), aggregates adding
+//      up and the interval spanning both; the merged queue keeps the
+//      absorber's empty_cnt.  The last remaining queue is never removed.
+// ---------------------------------------------------------------------------
+struct FifoKey {
+  float arrival;  // canonical: NaN -> +inf, -0 -> +0
+  int64_t id;
+};
+
+float canonical_arrival(float a) {
+  if (std::isnan(a)) return std::numeric_limits<float>::infinity();
+  if (a == 0.0f) return 0.0f;
+  return a;
+}
+
+bool older(const FifoKey& x, const FifoKey& y) {
+  return x.arrival < y.arrival || (x.arrival == y.arrival && x.id < y.id);
+}
+
+// Density-Weighted Scoring, Eq. 1 / Eq. 4, of one request of queue q:
+//   Phi = qf * ((w_base + w_urg * cs) + w_fair * ln(b + 1))
+//   qf  = q_i / (b + 1) with q_i the 1-based queue index in length order,
+//   cs  = W_t / C_prefill(b), W_t = max(0, now - arrival) seconds,
+//   C_prefill(b) = c0 + c1*b + c2*b*b seconds,
+//   w_x = a_x * mean_q + b_x (the affine meta-policy of Section 4.1 applied
+//   to all three weights), mean_q the queue's window mean length;
+//   th = (a_base, b_base, a_urg, b_urg, a_fair, b_fair).
+// Returned rounded once to binary32, NaN mapped to -inf.
+float phi_key(int32_t len, float arrival, float now, int32_t q, double mean_q, const float* th, double c0,
+              double c1, double c2) {
+  const double m = mean_q;
+  const double w_base = (double)th[0] * m + (double)th[1];
+  const double w_urg = (double)th[2] * m + (double)th[3];
+  const double w_fair = (double)th[4] * m + (double)th[5];
+  double W = (double)now - (double)arrival;
+  if (!(W > 0.0)) W = 0.0;
+  const double b = (double)len;
+  const double C = c0 + c1 * b + c2 * b * b;
+  const double cs = W / C;
+  const double qf = (double)(q + 1) / (b + 1.0);
+  const double phi = qf * ((w_base + w_urg * cs) + w_fair * std::log(b + 1.0));
+  float key = (float)phi;
+  if (std::isnan(key)) key = -std::numeric_limits<float>::infinity();
+  return key;
+}
+
+double utility(const Leaf& a, const Leaf& b, double eps) {
+  const double rho_a = (double)a.n / (double)((int64_t)a.hi - (int64_t)a.lo + 1);
+  const double rho_b = (double)b.n / (double)((int64_t)b.hi - (int64_t)b.lo + 1);
+  const double m_a = (double)a.S / (double)a.n;
+  const double m_b = (double)b.S / (double)b.n;
+  return (rho_a + rho_b) / (std::fabs(m_b - m_a) + eps);
+}
+
 }  // namespace
 
 extern "C" {
@@ -359,17 +438,11 @@ void oracle_route(const int32_t* len, int64_t n, const int32_t* bounds, int32_t 
   for (int64_t i = 0; i < n; ++i) qid[i] = route_one(len[i], bounds, k);
 }
 
-// Density-Weighted Scoring, Eq. 1 / Eq. 4, for every pending request:
-//   Phi = qf * ((w_base + w_urg * cs) + w_fair * ln(b + 1))
-//   qf  = q_i / (b + 1) with q_i the 1-based queue index in length order,
-//   cs  = W_t / C_prefill(b), W_t = max(0, now - arrival) seconds,
-//   C_prefill(b) = c0 + c1*b + c2*b*b seconds,
-//   w_x = a_x * mean_q + b_x (the affine meta-policy of Section 4.1 applied
-//   to all three weights), mean_q the queue's window mean length.
-// theta is [n_theta][6] = (a_base, b_base, a_urg, b_urg, a_fair, b_fair).
-// Output score[t * n + i] is Phi rounded once to binary32; a request whose
-// Phi is NaN gets -inf; an empty slot (len <= 0) gets NaN, which marks it
-// as not admissible.
+// Density-Weighted Scoring (Eq. 1 / Eq. 4, defined in phi_key) for every
+// pending request and parameter vector.  theta is [n_theta][6].  Output
+// score[t * n + i] is Phi rounded once to binary32; a request whose Phi is
+// NaN gets -inf; an empty slot (len <= 0) gets NaN, which marks it as not
+// admissible.
 void oracle_score(const int32_t* len, const float* arrival, int64_t n, float now, int32_t k,
                   const int32_t* bounds, const double* mean, const float* theta, int32_t n_theta,
                   double c0, double c1, double c2, float* score) {
@@ -381,20 +454,7 @@ void oracle_score(const int32_t* len, const float* arrival, int64_t n, float now
         score[(int64_t)t * n + i] = std::numeric_limits<float>::quiet_NaN();
         continue;
       }
-      const double m = mean[q];
-      const double w_base = (double)th[0] * m + (double)th[1];
-      const double w_urg = (double)th[2] * m + (double)th[3];
-      const double w_fair = (double)th[4] * m + (double)th[5];
-      double W = (double)now - (double)arrival[i];
-      if (!(W > 0.0)) W = 0.0;
-      const double b = (double)len[i];
-      const double C = c0 + c1 * b + c2 * b * b;
-      const double cs = W / C;
-      const double qf = (double)(q + 1) / (b + 1.0);
-      const double phi = qf * ((w_base + w_urg * cs) + w_fair * std::log(b + 1.0));
-      float key = (float)phi;
-      if (std::isnan(key)) key = -std::numeric_limits<float>::infinity();
-      score[(int64_t)t * n + i] = key;
+      score[(int64_t)t * n + i] = phi_key(len[i], arrival[i], now, q, mean[q], th, c0, c1, c2);
     }
   }
 }
@@ -428,6 +488,106 @@ void oracle_step(const int32_t* len, const float* arrival, int64_t n, float now,
                  int32_t* n_sel) {
   oracle_score(len, arrival, n, now, k, bounds, mean, theta, n_theta, c0, c1, c2, score_scratch);
   oracle_select(score_scratch, n, n_theta, B, ids, top, n_sel);
+}
+
+
+// One tactical step (Algorithm 1).  The queue table (k, bounds[k-1],
+// count, sum, lo, hi, mean) and empty_cnt[k] are read and updated in place
+// (queues past the empty threshold are removed after the batch is built).
+// Outputs: ids[B] in batch order (-1 after n_sel), head_score[k at entry]
+// (NaN for empty queues), q_prim (-1 when every queue is empty), removed[k
+// at entry] (1 for the queues removed in this step).
+int oracle_tactical_step(const int32_t* len, const float* arrival, int64_t n, float now, int32_t* k_io,
+                         int32_t* bounds, int64_t* count, int64_t* sum, int32_t* lo, int32_t* hi, double* mean,
+                         int32_t* empty_cnt, const float* theta, double c0, double c1, double c2, int32_t B,
+                         int32_t empty_threshold, double eps, int32_t* ids, int32_t* n_sel, int32_t* q_prim,
+                         float* head_score, int32_t* removed) {
+  const int32_t k = *k_io;
+  if (k < 1 || B < 0 || n < 0 || empty_threshold < 0) return kErrArg;
+  // Dispatcher: every pending request joins the FIFO of its queue.
+  std::vector<std::vector<FifoKey>> fifo(k);
+  for (int64_t i = 0; i < n; ++i) {
+    const int32_t q = route_one(len[i], bounds, k);
+    if (q >= 0) fifo[q].push_back({canonical_arrival(arrival[i]), i});
+  }
+  for (auto& f : fifo) std::stable_sort(f.begin(), f.end(), older);
+  // Score Updater: the head of every non-empty queue; empty queues count up.
+  std::vector<bool> marked(k, false);
+  for (int32_t q = 0; q < k; ++q) {
+    removed[q] = 0;
+    if (!fifo[q].empty()) {
+      const int64_t h = fifo[q].front().id;
+      head_score[q] = phi_key(len[h], arrival[h], now, q, mean[q], theta, c0, c1, c2);
+      empty_cnt[q] = 0;
+    } else {
+      head_score[q] = std::numeric_limits<float>::quiet_NaN();
+      empty_cnt[q] += 1;
+      if (empty_cnt[q] > empty_threshold) marked[q] = true;
+    }
+  }
+  // Batch Builder: ArgMax, GreedyFill, Backfill.
+  int32_t prim = -1;
+  for (int32_t q = 0; q < k; ++q)
+    if (!fifo[q].empty() && (prim < 0 || head_score[q] > head_score[prim])) prim = q;
+  *q_prim = prim;
+  int32_t nb = 0;
+  auto drain = [&](int32_t q) {
+    for (const FifoKey& r : fifo[q]) {
+      if (nb >= B) break;
+      ids[nb++] = (int32_t)r.id;
+    }
+  };
+  if (prim >= 0) {
+    drain(prim);
+    if (nb < B) {
+      std::vector<int32_t> adj;
+      if (prim > 0 && !fifo[prim - 1].empty()) adj.push_back(prim - 1);
+      if (prim + 1 < k && !fifo[prim + 1].empty()) adj.push_back(prim + 1);
+      if (adj.size() == 2 && head_score[adj[1]] > head_score[adj[0]]) std::swap(adj[0], adj[1]);
+      for (int32_t q : adj) drain(q);
+    }
+  }
+  *n_sel = nb;
+  for (int32_t r = nb; r < B; ++r) ids[r] = -1;
+  // RemoveQueue, after the batch: re-absorb each marked queue into a neighbour.
+  std::vector<Leaf> qs(k);
+  std::vector<int32_t> cnt(empty_cnt, empty_cnt + k), orig(k);
+  for (int32_t q = 0; q < k; ++q) {
+    qs[q] = {count[q], sum[q], lo[q], hi[q]};
+    orig[q] = q;
+  }
+  for (;;) {
+    int32_t r = -1;
+    for (int32_t q = 0; q < (int32_t)qs.size(); ++q)
+      if (marked[q]) {
+        r = q;
+        break;
+      }
+    if (r < 0 || qs.size() == 1) break;
+    int32_t a;  // absorber
+    if (r == 0) a = 1;
+    else if (r + 1 == (int32_t)qs.size()) a = r - 1;
+    else a = utility(qs[r - 1], qs[r], eps) <= utility(qs[r], qs[r + 1], eps) ? r - 1 : r + 1;
+    Leaf& A = qs[a];
+    A = {A.n + qs[r].n, A.S + qs[r].S, std::min(A.lo, qs[r].lo), std::max(A.hi, qs[r].hi)};
+    removed[orig[r]] = 1;
+    qs.erase(qs.begin() + r);
+    cnt.erase(cnt.begin() + r);
+    orig.erase(orig.begin() + r);
+    marked.erase(marked.begin() + r);
+  }
+  const int32_t k2 = (int32_t)qs.size();
+  *k_io = k2;
+  for (int32_t q = 0; q < k2; ++q) {
+    if (q > 0) bounds[q - 1] = qs[q].lo;
+    count[q] = qs[q].n;
+    sum[q] = qs[q].S;
+    lo[q] = qs[q].lo;
+    hi[q] = qs[q].hi;
+    mean[q] = (double)qs[q].S / (double)qs[q].n;
+    empty_cnt[q] = cnt[q];
+  }
+  return kOk;
 }
 
 }  // extern "C"

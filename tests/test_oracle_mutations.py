@@ -19,7 +19,7 @@ MUTANTS = [
     ("qf_drops_plus_one", "(double)(q + 1) / (b + 1.0)", "(double)(q + 1) / (b)"),
     ("fairness_term_dropped", "+ w_fair * std::log(b + 1.0)", ""),
     ("log_of_b_not_b_plus_1", "std::log(b + 1.0)", "std::log(b)"),
-    ("wait_sign_flipped", "(double)now - (double)arrival[i]", "(double)arrival[i] - (double)now"),
+    ("wait_sign_flipped", "(double)now - (double)arrival;", "(double)arrival - (double)now;"),
     ("cost_drops_linear_term", "c0 + c1 * b + c2 * b * b", "c0 + c2 * b * b"),
     ("compute_score_inverted", "const double cs = W / C;", "const double cs = C / W;"),
     ("urgency_weight_operands_swapped", "(double)th[2] * m + (double)th[3]", "(double)th[3] * m + (double)th[2]"),
@@ -36,6 +36,22 @@ MUTANTS = [
     ("kmeans_wrong_count", "(s2 * s2) / n2", "(s2 * s2) / n1"),
     ("mean_inverted", "mean[i] = (double)q[i].S / (double)q[i].n;", "mean[i] = (double)q[i].n / (double)q[i].S;"),
     ("window_not_clamped", "x = std::min(std::max(x, 1), max_len);", "x = std::max(x, 1);"),
+    # Algorithm 1 (tactical step)
+    ("fifo_newest_first", "return x.arrival < y.arrival || (x.arrival == y.arrival && x.id < y.id);",
+     "return x.arrival > y.arrival || (x.arrival == y.arrival && x.id < y.id);"),
+    ("fifo_tie_prefers_high_id", "(x.arrival == y.arrival && x.id < y.id)", "(x.arrival == y.arrival && x.id > y.id)"),
+    ("argmax_takes_lowest_score", "(prim < 0 || head_score[q] > head_score[prim])",
+     "(prim < 0 || head_score[q] < head_score[prim])"),
+    ("argmax_tie_to_high_index", "(prim < 0 || head_score[q] > head_score[prim])",
+     "(prim < 0 || head_score[q] >= head_score[prim])"),
+    ("backfill_ignores_head_scores", "if (adj.size() == 2 && head_score[adj[1]] > head_score[adj[0]])",
+     "if (false)"),
+    ("backfill_skips_upper_neighbour", "if (prim + 1 < k && !fifo[prim + 1].empty()) adj.push_back(prim + 1);", ""),
+    ("empty_count_never_reset", "      empty_cnt[q] = 0;\n", "\n"),
+    ("empty_threshold_off_by_one", "if (empty_cnt[q] > empty_threshold)", "if (empty_cnt[q] >= empty_threshold)"),
+    ("absorber_highest_utility", "utility(qs[r - 1], qs[r], eps) <= utility(qs[r], qs[r + 1], eps)",
+     "utility(qs[r - 1], qs[r], eps) > utility(qs[r], qs[r + 1], eps)"),
+    ("absorber_drops_counts", "A = {A.n + qs[r].n, A.S + qs[r].S,", "A = {A.n, A.S + qs[r].S,"),
 ]
 
 
@@ -53,7 +69,8 @@ def _run_mutant(args):
                        check=True, capture_output=True)
         env = dict(os.environ, EWSJF_ORACLE_LIB=so)
         r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
-                            os.path.join(ROOT, "tests", "test_oracle_pins.py")],
+                            os.path.join(ROOT, "tests", "test_oracle_pins.py"),
+                            os.path.join(ROOT, "tests", "test_oracle_tactical.py")],
                            cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
         return name, r.returncode
     finally:
