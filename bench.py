@@ -15,8 +15,9 @@ launch cost does not bound the loop; an eager pass with per-kernel events
 gives each kernel's own duration (start/end events bound to the kernel's
 dispatch) for the roofline figure.
 
-Two more workloads ride along in the same JSON line (skip them with
---no-extra): "batched_theta" -- one 1,048,576-request pool scored and
+Three more workloads ride along in the same JSON line (skip them with
+--no-extra): "tactical" -- Algorithm 1's own batch rule on the same 4M pool
+(ewsjf_tactical_step); "batched_theta" -- one 1,048,576-request pool scored and
 selected under 256 parameter vectors per step (top-256 each); "streaming"
 -- 10,000 steps of the streaming scheduler (1,048,576-slot ring, 4,096
 arrivals and 512 admissions per step, Refine-and-Prune over the last
@@ -157,6 +158,61 @@ def batched_theta_bench(hip, steps: int = 20):
             "ms_per_step": ms, "request_theta_pairs_per_s": n * nt / (ms * 1e-3),
             "kernels_ms": {"local_candidates": k1, "merge_candidates": k2}, "steps": steps,
             "input_sha256": pool.digest()[:16]}
+
+
+def tactical_bench(hip, pool, table, lens, arrs, steps: int = 50):
+    """Algorithm 1 (ewsjf_tactical_step) on the 4M pool: head-of-line pass,
+    plan, queue-order selection of B requests, batch assembly.  No removals
+    (threshold above the step count) and no tombstones, so every step sees
+    the same pool state; the pool copies rotate as in the main loop."""
+    import numpy as np
+    import torch
+
+    from paper_2601_21758_amd import _lib as L
+    from paper_2601_21758_amd import ewsjf as E
+    dev = torch.device("cuda:0")
+    n, B = pool.n, pool.B
+    theta = torch.from_numpy(pool.theta).to(dev)
+    ec = E.new_empty_counters(dev)
+    ids = torch.empty(B, dtype=torch.int32, device=dev)
+    small = torch.empty(2, dtype=torch.int32, device=dev)
+    hs = torch.empty(L.MAX_QUEUES, dtype=torch.float32, device=dev)
+    rm = torch.empty(L.MAX_QUEUES, dtype=torch.int32, device=dev)
+    wsb = E.workspace_bytes(L.OP_TACTICAL, n, 1, B)
+    ws = torch.empty(max(256, wsb), dtype=torch.uint8, device=dev)
+    c = E.cost(*pool.cost)
+    vp = C.c_void_p
+    lib = L.lib()
+    s = vp(torch.cuda.current_stream().cuda_stream)
+    nsel_p, qp_p = vp(small.data_ptr()), vp(small.data_ptr() + 4)
+
+    def one(i):
+        r = i % len(lens)
+        st = lib.ewsjf_tactical_step(vp(lens[r].data_ptr()), vp(arrs[r].data_ptr()), n, float(pool.now),
+                                     vp(table.data_ptr()), vp(theta.data_ptr()), C.byref(c), B, 1 << 30,
+                                     vp(ec.data_ptr()), 1e-6, 0, vp(ids.data_ptr()), nsel_p, qp_p,
+                                     vp(hs.data_ptr()), vp(rm.data_ptr()), vp(ws.data_ptr()), wsb, s)
+        if st != 0:
+            raise L.EwsjfError(st, "ewsjf_tactical_step")
+
+    for i in range(5):
+        one(i)
+    torch.cuda.synchronize()
+    torch.cuda._sleep(int(2.4e9 * (0.02 + 1e-4 * steps)))
+    e0, e1 = hip.event(), hip.event()
+    hip.rt.hipEventRecord(e0, s)
+    for i in range(steps):
+        one(i)
+    hip.rt.hipEventRecord(e1, s)
+    ms = hip.elapsed_ms(e0, e1) / steps
+    alg = 16 * n + 4 * B  # two passes over the 8-byte pool records, B ids out
+    got = small.cpu().numpy()
+    return {"workload": "tactical_large_mixed_4m: Algorithm 1 on the 4,194,304-request pool and 256-queue policy "
+                        "(head-of-line score per queue, ArgMax queue drained oldest first, backfill from its "
+                        "neighbours), B=1024",
+            "ms_per_step": ms, "requests_per_s": n / (ms * 1e-3),
+            "hbm_frac_two_passes": alg / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, "bytes_per_step": alg,
+            "n_sel": int(got[0]), "q_prim": int(got[1]), "steps": steps}
 
 
 def streaming_bench(steps: int):
@@ -380,6 +436,7 @@ def main() -> int:
         "partition_ms": partition_ms,
     }
     if not args.no_extra:
+        out["tactical"] = tactical_bench(hip, pool, table, lens, arrs)
         out["batched_theta"] = batched_theta_bench(hip)
         out["streaming"] = streaming_bench(args.stream_steps)
     if not args.no_cpu:

@@ -20,6 +20,10 @@
  *   ewsjf_step       route + score + select fused into one pass over the pool.
  *   ewsjf_ring_insert  new requests into a ring pool and the partition window
  *                    (the streaming scheduler's per-step update).
+ *   ewsjf_tactical_step  Algorithm 1's own batch rule: the head-of-line score
+ *                    of every queue, the ArgMax queue drained oldest first,
+ *                    backfill from its neighbours, removal of queues that stay
+ *                    empty (Section 3.2).
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -88,7 +92,7 @@ enum {
 };
 
 /* Operations for ewsjf_workspace_bytes(). */
-enum { EWSJF_OP_PARTITION = 0, EWSJF_OP_SELECT = 1, EWSJF_OP_STEP = 2 };
+enum { EWSJF_OP_PARTITION = 0, EWSJF_OP_SELECT = 1, EWSJF_OP_STEP = 2, EWSJF_OP_TACTICAL = 3 };
 
 /* Refine-and-Prune parameters (host struct).  Section 4.2: Stage 1 picks the
  * initializer; Stage 2 splits at gaps larger than alpha * mean gap (alpha > 1,
@@ -149,7 +153,8 @@ typedef struct {
 size_t ewsjf_queue_table_bytes(void);
 
 /* Workspace bytes needed by an operation.  `n` is the pool (or window) size;
- * p is read only for EWSJF_OP_PARTITION (may be NULL otherwise). */
+ * p is read only for EWSJF_OP_PARTITION (may be NULL otherwise); n_theta is
+ * ignored for EWSJF_OP_TACTICAL (one parameter vector). */
 size_t ewsjf_workspace_bytes(int op, int64_t n, int32_t n_theta, int32_t B, const ewsjf_partition_params* p);
 
 /* Install a queue structure computed elsewhere (for example a policy loaded
@@ -225,6 +230,42 @@ ewsjf_status ewsjf_step_timed(int32_t* len, const float* arrival, int64_t n, flo
 ewsjf_status ewsjf_ring_insert(int32_t* ring_len, float* ring_arrival, int64_t capacity, int64_t pos,
                                int32_t* window, int64_t window_cap, int64_t wpos, const int32_t* new_len,
                                const float* new_arrival, int64_t n, hipStream_t stream);
+
+/* One step of the tactical loop as Algorithm 1 states it (Section 3.2),
+ * over per-queue FIFOs of the pending pool:
+ *  1. Score Updater: every non-empty queue's head-of-line request (its oldest:
+ *     arrival ascending, equal arrivals by id, a NaN arrival last) is scored
+ *     with Phi (Eq. 1 / Eq. 4, binary64 rounded once to binary32) and the
+ *     queue's profile; an empty queue's counter empty_cnt[q] goes up by one
+ *     (a non-empty step resets it to 0).
+ *  2. Batch Builder: the queue with the highest head score (ties: the lower
+ *     queue) gives its requests oldest first until B are taken (GreedyFill);
+ *     if the batch is not full, its non-empty neighbours q-1 and q+1 backfill
+ *     it oldest first, the one with the higher head score first (ties: the
+ *     lower queue).
+ *  3. RemoveQueue: after the batch is built, queues with empty_cnt >
+ *     empty_threshold are removed, lowest index first; each is re-absorbed
+ *     by the neighbour whose pair has the lower Eq. 3 utility (eps as in
+ *     ewsjf_partition_params; ties: the lower neighbour): the boundary
+ *     between them goes, count/sum add, lo/hi span both, mean = sum/count.
+ *     The last queue is never removed.  The table (k, bounds, lo, hi, count,
+ *     sum, mean, lut) and empty_cnt are rewritten in place on the device.
+ * len, arrival: device [n] pool (16-byte aligned); table: device queue table,
+ * read and updated; theta: device, one vector; cost: host; empty_cnt: device
+ * int32 [EWSJF_MAX_QUEUES], entries [0, k) in use (zero them when a new table
+ * is installed); ids: device int32 [B] in batch order (-1 after n_sel);
+ * n_sel, q_prim: device int32 [1] (q_prim = -1 when every queue is empty);
+ * head_score: device float32 [EWSJF_MAX_QUEUES] or NULL (NaN for empty
+ * queues); removed: device int32 [EWSJF_MAX_QUEUES] or NULL (1 for each queue,
+ * indexed as at the start of the step, removed by this step).
+ * flags: 0 or EWSJF_STEP_TOMBSTONE (empty the admitted slots).  Workspace:
+ * ewsjf_workspace_bytes(EWSJF_OP_TACTICAL, n, 1, B, NULL).  1 <= B <=
+ * EWSJF_MAX_B, empty_threshold >= 0, eps > 0, otherwise EWSJF_ERR_ARG. */
+ewsjf_status ewsjf_tactical_step(int32_t* len, const float* arrival, int64_t n, float now, void* table,
+                                 const ewsjf_theta* theta, const ewsjf_cost* cost, int32_t B, int32_t empty_threshold,
+                                 int32_t* empty_cnt, double eps, int32_t flags, int32_t* ids, int32_t* n_sel,
+                                 int32_t* q_prim, float* head_score, int32_t* removed, void* ws, size_t ws_bytes,
+                                 hipStream_t stream);
 
 /* Human-readable name of a status code (static storage). */
 const char* ewsjf_status_string(ewsjf_status s);

@@ -292,9 +292,10 @@ int32_t route_one(int32_t b, const int32_t* bounds, int32_t k) {
 //      (scores of this step use the queue indices at its start).  The
 //      lowest-index queue past the threshold goes first; it is re-absorbed
 //      by the neighbour whose pair has the lower utility U of Eq. 3 (the
-//      Stage-3 merge rule; equal U: the lower neighbour), aggregates adding
-//      up and the interval spanning both; the merged queue keeps the
-//      absorber's empty_cnt.  The last remaining queue is never removed.
+//      Stage-3 merge rule; equal U: the lower neighbour): the boundary
+//      between the two disappears, aggregates add up, lo/hi span both, and
+//      the merged queue keeps the absorber's empty_cnt.  The last remaining
+//      queue is never removed.
 // ---------------------------------------------------------------------------
 struct FifoKey {
   float arrival;  // canonical: NaN -> +inf, -0 -> +0
@@ -551,7 +552,7 @@ int oracle_tactical_step(const int32_t* len, const float* arrival, int64_t n, fl
   for (int32_t r = nb; r < B; ++r) ids[r] = -1;
   // RemoveQueue, after the batch: re-absorb each marked queue into a neighbour.
   std::vector<Leaf> qs(k);
-  std::vector<int32_t> cnt(empty_cnt, empty_cnt + k), orig(k);
+  std::vector<int32_t> cnt(empty_cnt, empty_cnt + k), orig(k), bnd(bounds, bounds + (k - 1));
   for (int32_t q = 0; q < k; ++q) {
     qs[q] = {count[q], sum[q], lo[q], hi[q]};
     orig[q] = q;
@@ -571,6 +572,7 @@ int oracle_tactical_step(const int32_t* len, const float* arrival, int64_t n, fl
     Leaf& A = qs[a];
     A = {A.n + qs[r].n, A.S + qs[r].S, std::min(A.lo, qs[r].lo), std::max(A.hi, qs[r].hi)};
     removed[orig[r]] = 1;
+    bnd.erase(bnd.begin() + std::min(r, a));
     qs.erase(qs.begin() + r);
     cnt.erase(cnt.begin() + r);
     orig.erase(orig.begin() + r);
@@ -579,7 +581,7 @@ int oracle_tactical_step(const int32_t* len, const float* arrival, int64_t n, fl
   const int32_t k2 = (int32_t)qs.size();
   *k_io = k2;
   for (int32_t q = 0; q < k2; ++q) {
-    if (q > 0) bounds[q - 1] = qs[q].lo;
+    if (q > 0) bounds[q - 1] = bnd[q - 1];
     count[q] = qs[q].n;
     sum[q] = qs[q].S;
     lo[q] = qs[q].lo;

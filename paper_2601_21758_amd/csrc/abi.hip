@@ -89,6 +89,10 @@ size_t ewsjf_workspace_bytes(int op, int64_t n, int32_t n_theta, int32_t B, cons
     if (n_theta < 1 || n_theta > EWSJF_MAX_THETA || B < 1 || B > EWSJF_MAX_B) return 0;
     return ewsjf::plan_select(n, n_theta, B).ws_bytes;
   }
+  if (op == EWSJF_OP_TACTICAL) {
+    if (B < 1 || B > EWSJF_MAX_B) return 0;
+    return ewsjf::tactical_ws_bytes(n, B);
+  }
   return 0;
 }
 
@@ -209,6 +213,28 @@ ewsjf_status ewsjf_step(int32_t* len, const float* arrival, int64_t n, float now
                         int32_t* ids, float* top, int32_t* n_sel, void* ws, size_t ws_bytes, hipStream_t stream) {
   return ewsjf_step_timed(len, arrival, n, now, table, theta, n_theta, cost, B, flags, ids, top, n_sel, ws, ws_bytes,
                           stream, nullptr);
+}
+
+ewsjf_status ewsjf_tactical_step(int32_t* len, const float* arrival, int64_t n, float now, void* table,
+                                 const ewsjf_theta* theta, const ewsjf_cost* cost, int32_t B, int32_t empty_threshold,
+                                 int32_t* empty_cnt, double eps, int32_t flags, int32_t* ids, int32_t* n_sel,
+                                 int32_t* q_prim, float* head_score, int32_t* removed, void* ws, size_t ws_bytes,
+                                 hipStream_t stream) {
+  if ((n > 0 && (len == nullptr || arrival == nullptr)) || table == nullptr || theta == nullptr || cost == nullptr ||
+      empty_cnt == nullptr || ids == nullptr || n_sel == nullptr || q_prim == nullptr || ws == nullptr)
+    return EWSJF_ERR_NULL;
+  if (n < 0 || n > kMaxN || B < 1 || B > EWSJF_MAX_B || empty_threshold < 0 || !cost_ok(cost) ||
+      !std::isfinite(now) || !(eps > 0.0) || !std::isfinite(eps))
+    return EWSJF_ERR_ARG;
+  if ((flags & ~EWSJF_STEP_TOMBSTONE) != 0) return EWSJF_ERR_ARG;
+  if (ws_bytes < ewsjf::tactical_ws_bytes(n, B)) return EWSJF_ERR_WORKSPACE;
+  if ((n > 0 && (!aligned16(len) || !aligned16(arrival))) || !aligned16(ws)) return EWSJF_ERR_ALIGN;
+  const ewsjf_status ds = check_device();
+  if (ds != EWSJF_OK) return ds;
+  return launched(ewsjf::launch_tactical_step(len, arrival, n, now, static_cast<ewsjf_queue_table*>(table), theta,
+                                              *cost, B, empty_threshold, empty_cnt, eps,
+                                              (flags & EWSJF_STEP_TOMBSTONE) ? len : nullptr, ids, n_sel, q_prim,
+                                              head_score, removed, ws, stream));
 }
 
 }  // extern "C"

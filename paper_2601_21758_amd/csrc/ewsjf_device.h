@@ -90,6 +90,18 @@ __device__ __forceinline__ uint64_t make_comp(uint32_t ukey, uint32_t id) {
 
 __device__ __forceinline__ uint32_t comp_id(uint64_t c) { return 0xFFFFFFFFu - (uint32_t)c; }
 
+// Queue (FIFO) order of the tactical step: arrival ascending, a NaN arrival
+// counted as +inf and -0 as +0.  arrival_key is ascending in that order;
+// fifo_key is its complement, so the oldest request has the largest key
+// (always >= 0x007FFFFF, never the reserved 0).
+__device__ __forceinline__ uint32_t arrival_key(float a) {
+  uint32_t u = __float_as_uint(a);
+  if (a != a) u = 0x7F800000u;     // NaN -> +inf
+  if (u == 0x80000000u) u = 0u;    // -0 -> +0
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ uint32_t fifo_key(float a) { return ~arrival_key(a); }
+
 // ---------------------------------------------------------------------------
 // Wave and block reductions.
 // ---------------------------------------------------------------------------

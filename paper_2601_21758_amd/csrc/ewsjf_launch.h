@@ -34,6 +34,29 @@ struct CandBufs {
 
 SelectPlan plan_select(int64_t n, int32_t n_theta, int32_t B);
 
+// Tactical step (Algorithm 1): the batch plan computed on the device after
+// the head-of-line pass.  Row 0 of the queue-order selection drains q_sel[0]
+// (the ArgMax queue); rows 1 and 2 the backfill neighbours in order.
+constexpr int kTacticalRows = 3;
+struct TacticalPlan {
+  int32_t q_sel[kTacticalRows];  // queue of each row, -1 if none
+  int32_t take[kTacticalRows];   // requests the batch takes from each row
+  int32_t q_prim;                // -1 when every queue is empty
+  int32_t k;                     // queues at the start of the step
+  int32_t n_removed;             // queues past the empty threshold
+  int32_t pad;
+};
+
+hipError_t launch_fifo_select(const int32_t* len, const float* arrival, int64_t n, const ewsjf_queue_table* table,
+                              const TacticalPlan* plan, int32_t B, int32_t* ids, float* top, int32_t* n_sel, void* ws,
+                              hipStream_t stream);
+
+size_t tactical_ws_bytes(int64_t n, int32_t B);
+hipError_t launch_tactical_step(int32_t* len, const float* arrival, int64_t n, float now, ewsjf_queue_table* table,
+                                const ewsjf_theta* theta, const ewsjf_cost& cost, int32_t B, int32_t empty_threshold,
+                                int32_t* empty_cnt, double eps, int32_t* tomb_len, int32_t* ids, int32_t* n_sel,
+                                int32_t* q_prim, float* head_score, int32_t* removed, void* ws, hipStream_t stream);
+
 // marks (optional, may be NULL): four events taking the start and end
 // timestamps of the streaming kernel and of the merge kernel.
 hipError_t launch_step(const int32_t* len, const float* arrival, int64_t n, float now,

@@ -127,6 +127,99 @@ struct PoolSource {
     out[2] = key1(r.l.z, r.a.z, sh);
     out[3] = key1(r.l.w, r.a.w, sh);
   }
+
+  __device__ __forceinline__ bool skip(int) const { return false; }
+};
+
+// Queue-order keys for the tactical step (Algorithm 1): row t of the grid
+// selects the oldest requests of queue plan->q_sel[t] (FIFO order: arrival
+// ascending, then id), so the composite (fifo key << 32 | ~id) is largest
+// for the oldest request.  Rows t > 0 (the backfill queues) that the plan
+// does not need are skipped before they read the pool.
+struct FifoSource {
+  const int32_t* len;
+  const float* arrival;
+  const ewsjf_queue_table* table;
+  const TacticalPlan* plan;
+
+  static constexpr int kLutVecs = kLutBytes / 16;
+  static constexpr int kLutPerThread = (kLutVecs + kStageThreads - 1) / kStageThreads;
+
+  struct Raw {
+    i32x4 l;
+    f32x4 a;
+  };
+  struct Shared {
+    uint8_t lut[kLutBytes];
+    int L;
+    int qsel;
+  };
+  struct Stage {
+    i32x4 v[kLutPerThread];
+    int L, qsel;
+  };
+
+  __device__ __forceinline__ void stage_load(Stage& st, int t) const {
+    const i32x4* src = reinterpret_cast<const i32x4*>(table->lut);
+#pragma unroll
+    for (int r = 0; r < kLutPerThread; ++r) {
+      const int i = threadIdx.x + r * kStageThreads;
+      st.v[r] = src[i < kLutVecs ? i : kLutVecs - 1];
+    }
+    st.L = table->max_len;
+    st.qsel = plan->q_sel[t];
+  }
+
+  __device__ __forceinline__ void stage_store(Shared& sh, const Stage& st) const {
+    i32x4* dst = reinterpret_cast<i32x4*>(sh.lut);
+#pragma unroll
+    for (int r = 0; r < kLutPerThread; ++r) {
+      const int i = threadIdx.x + r * kStageThreads;
+      if (r + 1 < kLutPerThread || i < kLutVecs) dst[i] = st.v[r];
+    }
+    if (threadIdx.x == 0) {
+      sh.L = st.L;
+      sh.qsel = st.qsel;
+    }
+  }
+
+  __device__ __forceinline__ Raw load4(int64_t base, int64_t n) const {
+    Raw r;
+    if (base + 3 < n) {
+      r.l = load_i32x4(len + base);
+      r.a = load_f32x4(arrival + base);
+    } else {
+      r.l = i32x4{0, 0, 0, 0};
+      r.a = f32x4{0.f, 0.f, 0.f, 0.f};
+      if (base + 0 < n) { r.l.x = len[base + 0]; r.a.x = arrival[base + 0]; }
+      if (base + 1 < n) { r.l.y = len[base + 1]; r.a.y = arrival[base + 1]; }
+      if (base + 2 < n) { r.l.z = len[base + 2]; r.a.z = arrival[base + 2]; }
+    }
+    return r;
+  }
+
+  __device__ __forceinline__ Raw load_chunk(int64_t c, int64_t n, int lane) const {
+    const int64_t first = c * kChunk;
+    Raw r;
+    r.l = chunk_load_i32x4(chunk_rsrc(len + first, n - first), lane);
+    const i32x4 a = chunk_load_i32x4(chunk_rsrc(arrival + first, n - first), lane);
+    r.a = __builtin_bit_cast(f32x4, a);
+    return r;
+  }
+
+  __device__ __forceinline__ uint32_t key1(int b, float a, const Shared& sh) const {
+    const int bc = min(max(b, 0), sh.L);
+    return (b > 0 && (int)sh.lut[bc] == sh.qsel) ? fifo_key(a) : 0u;
+  }
+
+  __device__ __forceinline__ void keys4(const Raw& r, const Shared& sh, uint32_t out[4]) const {
+    out[0] = key1(r.l.x, r.a.x, sh);
+    out[1] = key1(r.l.y, r.a.y, sh);
+    out[2] = key1(r.l.z, r.a.z, sh);
+    out[3] = key1(r.l.w, r.a.w, sh);
+  }
+
+  __device__ __forceinline__ bool skip(int t) const { return t > 0 && plan->take[t] == 0; }
 };
 
 struct ScoreSource {
@@ -184,6 +277,8 @@ struct ScoreSource {
     out[2] = key1(r.s.z);
     out[3] = key1(r.s.w);
   }
+
+  __device__ __forceinline__ bool skip(int) const { return false; }
 
   const float* row_ = nullptr;
   bool vec_ = false;  // the row is 16-byte aligned
@@ -246,6 +341,17 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
   __shared__ ListShared ls;
   const int t = blockIdx.y;
   const Src src = bind_theta(src0, t);
+  if (src.skip(t)) {  // a row with nothing to select: an empty, complete list
+    const size_t slot = (size_t)t * G + blockIdx.x;
+    for (int i = threadIdx.x; i < M; i += kBlock) cb.lists[slot * (size_t)M + i] = 0ull;
+    if (threadIdx.x == 0) {
+      cb.counts[slot] = 0u;
+      cb.bounds[slot] = 0ull;
+      cb.bounds2[slot] = 0ull;
+      cb.over_cnt[slot] = 0u;
+    }
+    return;
+  }
   const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
   const int64_t nchunks = (n + kChunk - 1) / kChunk;
   const int64_t my_chunks = nchunks > blockIdx.x ? (nchunks - blockIdx.x + G - 1) / G : 0;
@@ -506,6 +612,7 @@ struct MergeShared {
   int wtot[kWavesPerBlock];
   int cntX;
   int cntS;
+  int ntake;
   int cut_bin;
   int cut_cnt;
 };
@@ -610,6 +717,14 @@ __global__ __launch_bounds__(kBlock) void merge_candidates(Src src0, int64_t n, 
   const int tid = threadIdx.x;
   const Src src = bind_theta(src0, t);
   const size_t slot0 = (size_t)t * G;
+  if (src.skip(t)) {
+    for (int r = tid; r < B; r += kBlock) {
+      ids[(size_t)t * B + r] = -1;
+      top[(size_t)t * B + r] = __builtin_nanf("");
+    }
+    if (tid == 0) n_sel[t] = 0;
+    return;
+  }
 
   // One round trip: every list slot (G x M, empty slots hold 0) and the
   // completeness bounds, as bounded buffer loads (no branches, so the waits
@@ -747,14 +862,40 @@ __global__ __launch_bounds__(kBlock) void merge_candidates(Src src0, int64_t n, 
     if (tid == 0) ms.cntS = 0;
     __syncthreads();
     if (sT2[wbest] <= thr) {
-      const uint64_t* ov = cb.over + (slot0 + wbest) * (size_t)kOverCap;
-      const int oc = (int)cb.over_cnt[slot0 + wbest];
-      if (tid < oc) {
-        const uint64_t x = ov[tid];
-        if (x >= thr && x < best) ms.S[atomicAdd(&ms.cntS, 1)] = x;
+      // Every share at risk whose overflow list reaches the cut contributes
+      // in this one round (in share order, as many as fit kSortMax entries):
+      // entries j of the round belong to the share w with off[w] <= j <
+      // off[w + 1], off the prefix sum of the included list lengths.
+      bool elig = false;
+      int c = 0;
+      if (tid < G) {
+        elig = sT[tid] > thr && sT2[tid] <= thr;
+        c = elig ? (int)cb.over_cnt[slot0 + tid] : 0;
+      }
+      if (tid == 0) ms.ntake = kSortMax + 1;
+      int total;
+      const int off = block_exclusive_scan_n(c, ms.iscan, &total, kMaxGrid);
+      const bool incl = elig && off + c <= kSortMax;  // a prefix of the eligible shares
+      if (tid < G) ms.cnt[tid] = (uint32_t)off;
+      if (elig && !incl) atomicMin(&ms.ntake, off);
+      __syncthreads();
+      const int ntake = ms.ntake < total ? ms.ntake : total;
+      for (int j = tid; j < ntake; j += kBlock) {
+        int lo = 0, hi = G - 1;  // the largest w with off[w] <= j
+        while (lo < hi) {
+          const int mid = (lo + hi + 1) >> 1;
+          if ((int)ms.cnt[mid] <= j) lo = mid;
+          else hi = mid - 1;
+        }
+        const uint64_t x = cb.over[(slot0 + lo) * (size_t)kOverCap + (j - (int)ms.cnt[lo])];
+        if (x >= thr && x < sT[lo]) ms.S[atomicAdd(&ms.cntS, 1)] = x;
       }
       __syncthreads();
       U = merge_new(ms, U, ms.cntS, B);
+      tau = (U >= B) ? ms.X[B - 1] : 0ull;
+      if (incl) sT[tid] = 0ull;  // done
+      __syncthreads();
+      continue;
     } else {
       if (!staged) {
         if (tid < kStageThreads) {
@@ -906,6 +1047,25 @@ hipError_t launch_step(const int32_t* len, const float* arrival, int64_t n, floa
   if (e != hipSuccess) return e;
   hipExtLaunchKernelGGL(merge_candidates<PoolSource>, dim3(n_theta), dim3(kBlock), 0, stream, marks[2], marks[3],
                         0, src, n, p.G, p.M, B, cb, ids, top, n_sel, tomb_len);
+  return hipGetLastError();
+}
+
+hipError_t launch_fifo_select(const int32_t* len, const float* arrival, int64_t n, const ewsjf_queue_table* table,
+                              const TacticalPlan* plan, int32_t B, int32_t* ids, float* top, int32_t* n_sel, void* ws,
+                              hipStream_t stream) {
+  const SelectPlan p = plan_select(n, kTacticalRows, B);
+  const CandBufs cb = carve(p, ws);
+  FifoSource src;
+  src.len = len;
+  src.arrival = arrival;
+  src.table = table;
+  src.plan = plan;
+  hipLaunchKernelGGL(local_candidates<FifoSource>, dim3(p.G, kTacticalRows), dim3(kBlock), 0, stream, src, n, p.G,
+                     p.lg, p.M, cb);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(merge_candidates<FifoSource>, dim3(kTacticalRows), dim3(kBlock), 0, stream, src, n, p.G, p.M,
+                     B, cb, ids, top, n_sel, nullptr);
   return hipGetLastError();
 }
 

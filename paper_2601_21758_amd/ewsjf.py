@@ -195,6 +195,41 @@ def step(length: torch.Tensor, arrival: torch.Tensor, now: float, table: torch.T
     return ids, top, nsel
 
 
+def new_empty_counters(device=None) -> torch.Tensor:
+    """Per-queue empty-step counters for tactical_step (zero for a new table)."""
+    return torch.zeros(L.MAX_QUEUES, dtype=torch.int32, device=device)
+
+
+def tactical_step(length: torch.Tensor, arrival: torch.Tensor, now: float, table: torch.Tensor, theta: torch.Tensor,
+                  B: int, empty_threshold: int, empty_cnt: torch.Tensor, eps: float = 1e-6, cost_=DEFAULT_COST,
+                  tombstone: bool = False, ws: Workspace | None = None, stream=None):
+    """One step of Algorithm 1 (ewsjf_tactical_step): returns ids[B] (batch
+    order), n_sel[1], q_prim[1], head_score[MAX_QUEUES], removed[MAX_QUEUES].
+    The table and empty_cnt are updated in place."""
+    _need(length, torch.int32, "length")
+    _need(arrival, torch.float32, "arrival")
+    _need(empty_cnt, torch.int32, "empty_cnt")
+    theta = _theta(theta)
+    if theta.shape[0] != 1:
+        raise ValueError("tactical_step takes one parameter vector")
+    n, dev = length.numel(), length.device
+    ids = torch.empty(B, dtype=torch.int32, device=dev)
+    nsel = torch.empty(1, dtype=torch.int32, device=dev)
+    qp = torch.empty(1, dtype=torch.int32, device=dev)
+    hs = torch.empty(L.MAX_QUEUES, dtype=torch.float32, device=dev)
+    rm = torch.empty(L.MAX_QUEUES, dtype=torch.int32, device=dev)
+    ws = ws or Workspace(dev)
+    buf = ws.get(workspace_bytes(L.OP_TACTICAL, n, 1, B))
+    c = _cost(cost_)
+    flags = L.STEP_TOMBSTONE if tombstone else 0
+    L.check(L.lib().ewsjf_tactical_step(_vp(length), _vp(arrival), n, float(now), _vp(table), _vp(theta), C.byref(c),
+                                        int(B), int(empty_threshold), _vp(empty_cnt), float(eps), flags, _vp(ids),
+                                        _vp(nsel), _vp(qp), _vp(hs), _vp(rm), _vp(buf), buf.numel(),
+                                        _stream(stream)),
+            "ewsjf_tactical_step")
+    return ids, nsel, qp, hs, rm
+
+
 def ring_insert(ring_len: torch.Tensor, ring_arrival: torch.Tensor, pos: int, new_len: torch.Tensor,
                 new_arrival: torch.Tensor, window: torch.Tensor | None = None, wpos: int = 0, stream=None) -> None:
     """Write new requests into ring slots (pos + i) mod capacity and their

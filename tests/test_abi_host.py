@@ -133,6 +133,34 @@ def test_ring_insert_argument_errors():
     assert ins(rl=None, ra=None, nl=None, na=None, n=0) == L.OK
 
 
+def test_tactical_step_argument_errors():
+    lib = L.lib()
+    c = L.Cost(0.01, 1e-4, 0.0)
+    need = lib.ewsjf_workspace_bytes(L.OP_TACTICAL, 1000, 1, 64, None)
+    assert need > 0 and lib.ewsjf_workspace_bytes(L.OP_TACTICAL, 1000, 1, 0, None) == 0
+
+    def tac(length=FAKE, arr=FAKE, n=1000, now=60.0, table=FAKE, theta=FAKE, cost=c, B=64, thr=2, ec=FAKE, eps=1e-6,
+            flags=0, ids=FAKE, nsel=FAKE, qp=FAKE, hs=FAKE, rm=FAKE, ws=FAKE, wsb=need):
+        return lib.ewsjf_tactical_step(length, arr, n, now, table, theta, C.byref(cost) if cost is not None else None,
+                                       B, thr, ec, eps, flags, ids, nsel, qp, hs, rm, ws, wsb, None)
+
+    assert tac(length=None) == L.ERR_NULL
+    assert tac(table=None) == L.ERR_NULL
+    assert tac(ec=None) == L.ERR_NULL
+    assert tac(qp=None) == L.ERR_NULL
+    assert tac(cost=None) == L.ERR_NULL
+    assert tac(B=0) == L.ERR_ARG
+    assert tac(B=4097) == L.ERR_ARG
+    assert tac(thr=-1) == L.ERR_ARG
+    assert tac(eps=0.0) == L.ERR_ARG
+    assert tac(eps=float("nan")) == L.ERR_ARG
+    assert tac(now=float("inf")) == L.ERR_ARG
+    assert tac(n=-1) == L.ERR_ARG
+    assert tac(flags=4) == L.ERR_ARG
+    assert tac(wsb=need - 1) == L.ERR_WORKSPACE
+    assert tac(arr=FAKE_MIS) == L.ERR_ALIGN
+
+
 def test_partition_argument_errors():
     lib = L.lib()
     need = lib.ewsjf_workspace_bytes(L.OP_PARTITION, 100, 0, 0, C.byref(_p()))
