@@ -19,6 +19,7 @@ constexpr int kListCap = 1024;               // per-workgroup candidate list in 
 constexpr int kShortList = 256;              // lists ranked by all waves at once (up to 4 entries per lane)
 constexpr int kWaveCap = kListCap / (kBlock / kWave);  // one region of the list per wave
 constexpr int kOverCap = 128;                // overflow entries kept per workgroup
+constexpr int kDenseWave = 32;              // region entries that mark a wave holding a cluster of high keys
 constexpr int kStageWaves = 4;                // waves that stage the per-workgroup tables
 constexpr int kStageThreads = kStageWaves * kWave;
 constexpr int kMergeCap = 9088;              // merge kernel candidate capacity (LDS, >= 2 * kSortMax)

@@ -129,6 +129,7 @@ struct PoolSource {
   }
 
   __device__ __forceinline__ bool skip(int) const { return false; }
+  static constexpr bool kClustered = false;
 };
 
 // Queue-order keys for the tactical step (Algorithm 1): row t of the grid
@@ -220,6 +221,11 @@ struct FifoSource {
   }
 
   __device__ __forceinline__ bool skip(int t) const { return t > 0 && plan->take[t] == 0; }
+  // The oldest requests of a queue sit together in an arrival-ordered pool:
+  // the streaming kernel keeps a spill list for full wave regions and lowers
+  // the workgroup bound past a clustered wave (both cost the score sources
+  // time and registers, so they are compiled in for this source only).
+  static constexpr bool kClustered = true;
 };
 
 struct ScoreSource {
@@ -279,6 +285,7 @@ struct ScoreSource {
   }
 
   __device__ __forceinline__ bool skip(int) const { return false; }
+  static constexpr bool kClustered = false;
 
   const float* row_ = nullptr;
   bool vec_ = false;  // the row is 16-byte aligned
@@ -305,6 +312,7 @@ __device__ __forceinline__ ScoreSource bind_theta<ScoreSource>(const ScoreSource
 struct ListShared {
   uint64_t list[kListCap];  // kWavesPerBlock regions of kWaveCap entries
   uint64_t list2[kListCap];
+  uint64_t spill[kListCap];  // entries of waves whose region is full (0 = unused)
   uint32_t hist[256];
   uint64_t red[kWavesPerBlock];
   int iscan[kWavesPerBlock];
@@ -313,6 +321,8 @@ struct ListShared {
   int wcnt[kWavesPerBlock];
   int ovf;
   int nout;
+  int nspill;
+  uint32_t lowbar;  // the lowered workgroup bound (0: not lowered)
 };
 static_assert(kWaveCap == kWave, "the final filter maps one region slot to one lane");
 
@@ -378,8 +388,12 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
   if (threadIdx.x == 0) {
     ls.ovf = 0;
     ls.nout = 0;
+    ls.nspill = 0;
+    ls.lowbar = 0u;
   }
   if (threadIdx.x < kShortList) ls.rank[threadIdx.x] = 0;
+  static_assert(kListCap == kBlock, "one spill entry per thread");
+  if constexpr (Src::kClustered) ls.spill[threadIdx.x] = 0ull;
   __syncthreads();
 
   // Each wave writes every element whose key is >= its bar into its own
@@ -392,8 +406,8 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
   uint32_t my_bar = 0;  // this wave's largest bar over the passes
   int wcnt = 0;         // entries of this wave's region (wave-uniform)
   bool wovf = false;    // the region overflowed: elements were lost
+  uint32_t key[kElemsPerLane];  // the last pass's keys stay live for the bound lowering below
   for (int pass = 0; pass < passes; ++pass) {
-    uint32_t key[kElemsPerLane];
     // A wave stalls at a load while the memory pipeline is full, so it
     // scores a chunk that has arrived before it issues the next load; the
     // other waves keep the pipeline full meanwhile.
@@ -438,12 +452,36 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
         }
       }
     };
-    emit(my_bar > 1u ? my_bar : 1u);
+    const uint32_t thr = my_bar > 1u ? my_bar : 1u;
+    emit(thr);
+    if (Src::kClustered && wcnt > kWaveCap) {
+      // Too many keys at or above the bar for the wave's region (data whose
+      // high keys cluster in this wave): the rest goes to the workgroup's
+      // spill list if it has room (one reservation per wave; a reservation
+      // that does not fit is left as zeros, which mean "no entry").
+      const int need = wcnt - kWaveCap;
+      int base = 0;
+      if (lane == 0) base = atomicAdd(&ls.nspill, need);
+      base = __shfl(base, 0);
+      if (base + need <= kListCap) {
+        int c = wcnt0;
+#pragma unroll
+        for (int e = 0; e < kElemsPerLane; ++e) {
+          const bool p = key[e] >= thr;
+          const uint64_t sm = __ballot(p);
+          const int pos = c + lanes_below(sm);
+          if (p && pos >= kWaveCap)
+            ls.spill[base + pos - kWaveCap] =
+                make_comp(key[e], (uint32_t)(chunk_of(G, pass, e / 4) * kChunk + lane * 4 + (e & 3)));
+          c += __popcll(sm);
+        }
+        wcnt = kWaveCap;
+      }
+    }
     if (wcnt > kWaveCap) {
-      // Too many keys at or above the bar (data whose high keys cluster in
-      // this wave): raise the bar just above the (room)-th largest key, so
-      // fewer than `room` keys qualify, and emit again.  Only equal keys
-      // beyond the room can still overflow (then the list is marked
+      // No spill room either: raise the bar just above the (room)-th largest
+      // key, so fewer than `room` keys qualify, and emit again.  Only equal
+      // keys beyond the room can still overflow (then the list is marked
       // incomplete and the merge re-reads the share).
       const int room = kWaveCap - wcnt0;
       if (room > 0) {
@@ -497,24 +535,80 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
     }
     return;
   }
-  uint32_t T_bar = 0;
+  // The workgroup's bound: the largest wave bar t1.  When the wave holding
+  // t1 is dense (a cluster of high keys, such as old requests in
+  // neighbouring slots), it also lists its keys in [t2, t1), t2 the second
+  // largest bar, so the bound drops to t2 and no longer sits far above the
+  // rest of the share.  (Single pass only: the keys are still in registers.)
+  uint32_t t1 = 0, t2 = 0;
+  int v1 = 0;
 #pragma unroll
-  for (int i = 0; i < kWavesPerBlock; ++i) T_bar = ls.bar[i] > T_bar ? ls.bar[i] : T_bar;
+  for (int i = 0; i < kWavesPerBlock; ++i) {
+    const uint32_t b = ls.bar[i];
+    if (b > t1) {
+      t2 = t1;
+      t1 = b;
+      v1 = i;
+    } else if (b > t2) {
+      t2 = b;
+    }
+  }
+  const uint32_t lo2 = t2 > 1u ? t2 : 1u;
+  uint32_t T_bar = t1;
+  if (Src::kClustered && passes == 1 && lo2 < t1 && ls.wcnt[v1] >= kDenseWave) {  // uniform
+    if (wv == v1) {
+      int need = 0;
+#pragma unroll
+      for (int e = 0; e < kElemsPerLane; ++e) need += __popcll(__ballot(key[e] >= lo2 && key[e] < t1));
+      int base = 0;
+      if (lane == 0) base = atomicAdd(&ls.nspill, need);
+      base = __shfl(base, 0);
+      if (base + need <= kListCap) {
+        int c = base;
+#pragma unroll
+        for (int e = 0; e < kElemsPerLane; ++e) {
+          const bool p = key[e] >= lo2 && key[e] < t1;
+          const uint64_t sm = __ballot(p);
+          if (p)
+            ls.spill[c + lanes_below(sm)] =
+                make_comp(key[e], (uint32_t)(chunk_of(G, 0, e / 4) * kChunk + lane * 4 + (e & 3)));
+          c += __popcll(sm);
+        }
+        if (lane == 0) ls.lowbar = lo2;
+      }
+    }
+    __syncthreads();
+    if (ls.lowbar != 0u) T_bar = ls.lowbar;
+  }
   const uint64_t lowc = (uint64_t)T_bar << 32;
-  // Entries >= lowc are exactly the share's elements >= lowc.
-  {
-    const uint64_t x = lane < ls.wcnt[wv] ? ls.list[threadIdx.x] : 0ull;
+  // Entries >= lowc (regions and spill) are exactly the share's elements >=
+  // lowc.  More than kListCap of them: the list cannot hold the share's
+  // candidates, so nothing is guaranteed (the merge re-reads the share).
+  auto keep_into_list2 = [&](uint64_t x) {
     const bool keep = x >= lowc && x != 0ull;
     const uint64_t bal = __ballot(keep);
     if (bal) {
       int b0 = 0;
       if (lane == 0) b0 = atomicAdd(&ls.nout, __popcll(bal));
       b0 = __shfl(b0, 0);
-      if (keep) ls.list2[b0 + __popcll(bal & lanemask_lt())] = x;
+      const int at = b0 + __popcll(bal & lanemask_lt());
+      if (keep && at < kListCap) ls.list2[at] = x;
     }
-  }
+  };
+  keep_into_list2(lane < ls.wcnt[wv] ? ls.list[threadIdx.x] : 0ull);
+  if (Src::kClustered && ls.nspill != 0) keep_into_list2(ls.spill[threadIdx.x]);  // uniform
   __syncthreads();
   const int cnt = ls.nout;
+  if (cnt > kListCap) {
+    for (int i = threadIdx.x; i < M; i += kBlock) out_list[i] = 0ull;
+    if (threadIdx.x == 0) {
+      cb.counts[slot] = 0u;
+      cb.bounds[slot] = ~0ull;
+      cb.bounds2[slot] = ~0ull;
+      cb.over_cnt[slot] = 0u;
+    }
+    return;
+  }
   if (cnt <= M) {
     for (int i = threadIdx.x; i < M; i += kBlock) out_list[i] = i < cnt ? ls.list2[i] : 0ull;
     if (threadIdx.x == 0) {
@@ -612,7 +706,6 @@ struct MergeShared {
   int wtot[kWavesPerBlock];
   int cntX;
   int cntS;
-  int ntake;
   int cut_bin;
   int cut_cnt;
 };
@@ -862,38 +955,45 @@ __global__ __launch_bounds__(kBlock) void merge_candidates(Src src0, int64_t n, 
     if (tid == 0) ms.cntS = 0;
     __syncthreads();
     if (sT2[wbest] <= thr) {
-      // Every share at risk whose overflow list reaches the cut contributes
-      // in this one round (in share order, as many as fit kSortMax entries):
-      // entries j of the round belong to the share w with off[w] <= j <
-      // off[w + 1], off the prefix sum of the included list lengths.
-      bool elig = false;
-      int c = 0;
-      if (tid < G) {
-        elig = sT[tid] > thr && sT2[tid] <= thr;
-        c = elig ? (int)cb.over_cnt[slot0 + tid] : 0;
-      }
-      if (tid == 0) ms.ntake = kSortMax + 1;
-      int total;
-      const int off = block_exclusive_scan_n(c, ms.iscan, &total, kMaxGrid);
-      const bool incl = elig && off + c <= kSortMax;  // a prefix of the eligible shares
-      if (tid < G) ms.cnt[tid] = (uint32_t)off;
-      if (elig && !incl) atomicMin(&ms.ntake, off);
-      __syncthreads();
-      const int ntake = ms.ntake < total ? ms.ntake : total;
-      for (int j = tid; j < ntake; j += kBlock) {
-        int lo = 0, hi = G - 1;  // the largest w with off[w] <= j
-        while (lo < hi) {
-          const int mid = (lo + hi + 1) >> 1;
-          if ((int)ms.cnt[mid] <= j) lo = mid;
-          else hi = mid - 1;
+      // The shares at risk whose overflow lists reach the cut contribute in
+      // one round: the first kOverBatch of them (kOverBatch * kOverCap <=
+      // kSortMax, so every reservation fits), the r-th handled by wave r mod
+      // 16.  Every wave derives the same share order from LDS itself.
+      constexpr int kOverBatch = kSortMax / kOverCap;
+      static_assert(kMaxGrid % kWave == 0 && kOverBatch <= 2 * kWavesPerBlock, "two shares per wave at most");
+      int mine0 = -1, mine1 = -1, r = 0;
+      for (int q = 0; q < kMaxGrid / kWave && r < kOverBatch; ++q) {
+        const int wq = q * kWave + lane;
+        uint64_t m = __ballot(wq < G && sT[wq] > thr && sT2[wq] <= thr);
+        while (m != 0ull && r < kOverBatch) {
+          const int w = q * kWave + (int)__builtin_ctzll(m);
+          m &= m - 1;
+          if ((r & (kWavesPerBlock - 1)) == wv) {
+            if (mine0 < 0) mine0 = w;
+            else mine1 = w;
+            const uint64_t* ov = cb.over + (slot0 + w) * (size_t)kOverCap;
+            const int oc = (int)cb.over_cnt[slot0 + w];
+            const uint64_t bw = sT[w];
+            const uint64_t x0 = lane < oc ? ov[lane] : 0ull;
+            const uint64_t x1 = lane + kWave < oc ? ov[lane + kWave] : 0ull;
+            const bool p0 = x0 >= thr && x0 < bw, p1 = x1 >= thr && x1 < bw;
+            const uint64_t m0 = __ballot(p0), m1 = __ballot(p1);
+            int base = 0;
+            if (lane == 0) base = atomicAdd(&ms.cntS, (int)(__popcll(m0) + __popcll(m1)));
+            base = __shfl(base, 0);
+            if (p0) ms.S[base + lanes_below(m0)] = x0;
+            if (p1) ms.S[base + __popcll(m0) + lanes_below(m1)] = x1;
+          }
+          ++r;
         }
-        const uint64_t x = cb.over[(slot0 + lo) * (size_t)kOverCap + (j - (int)ms.cnt[lo])];
-        if (x >= thr && x < sT[lo]) ms.S[atomicAdd(&ms.cntS, 1)] = x;
       }
       __syncthreads();
       U = merge_new(ms, U, ms.cntS, B);
       tau = (U >= B) ? ms.X[B - 1] : 0ull;
-      if (incl) sT[tid] = 0ull;  // done
+      if (lane == 0) {  // done
+        if (mine0 >= 0) sT[mine0] = 0ull;
+        if (mine1 >= 0) sT[mine1] = 0ull;
+      }
       __syncthreads();
       continue;
     } else {
