@@ -87,7 +87,7 @@ size_t ewsjf_workspace_bytes(int op, int64_t n, int32_t n_theta, int32_t B, cons
   }
   if (op == EWSJF_OP_SELECT || op == EWSJF_OP_STEP) {
     if (n_theta < 1 || n_theta > EWSJF_MAX_THETA || B < 1 || B > EWSJF_MAX_B) return 0;
-    return ewsjf::plan_select(n, n_theta, B).ws_bytes;
+    return op == EWSJF_OP_STEP ? ewsjf::plan_step(n, n_theta, B).ws_bytes : ewsjf::plan_select(n, n_theta, B).ws_bytes;
   }
   if (op == EWSJF_OP_TACTICAL) {
     if (B < 1 || B > EWSJF_MAX_B) return 0;
@@ -199,7 +199,7 @@ ewsjf_status ewsjf_step_timed(int32_t* len, const float* arrival, int64_t n, flo
     return EWSJF_ERR_ARG;
   if ((flags & ~EWSJF_STEP_TOMBSTONE) != 0) return EWSJF_ERR_ARG;
   if ((flags & EWSJF_STEP_TOMBSTONE) && n_theta != 1) return EWSJF_ERR_ARG;
-  if (ws_bytes < ewsjf::plan_select(n, n_theta, B).ws_bytes) return EWSJF_ERR_WORKSPACE;
+  if (ws_bytes < ewsjf::plan_step(n, n_theta, B).ws_bytes) return EWSJF_ERR_WORKSPACE;
   if ((n > 0 && (!aligned16(len) || !aligned16(arrival))) || !aligned16(ws)) return EWSJF_ERR_ALIGN;
   const ewsjf_status ds = check_device();
   if (ds != EWSJF_OK) return ds;

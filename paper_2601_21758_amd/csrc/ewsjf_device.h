@@ -558,14 +558,30 @@ struct CostF {
   float c0, c1, c2;
 };
 
-__device__ __forceinline__ float phi_f32(int b, float arrival, float now, const QParams& p, const CostF& c) {
+// Phi (Eq. 1 / Eq. 4) regrouped as three per-request terms and the folded
+// per-queue weights of one parameter vector:
+//   Phi = (q+1) w_b alpha + (q+1) w_u beta + (q+1) w_f ln2 gamma,
+//   alpha = 1/(b+1), beta = W / ((b+1) C), gamma = log2(b+1) / (b+1).
+// Every kernel that forms a request's key uses these two functions, so a
+// request gets the same key wherever it is scored (the merge's re-reads
+// compare keys with the streaming kernel's).
+struct PhiTerms {
+  float al, be, ga;
+};
+__device__ __forceinline__ PhiTerms phi_terms(int b, float arrival, float now, const CostF& c) {
   const float fb = (float)b;
   const float bp1 = fb + 1.0f;
   const float W = fmaxf(now - arrival, 0.0f);  // NaN arrival or future arrival -> 0
   const float C = __builtin_fmaf(__builtin_fmaf(c.c2, fb, c.c1), fb, c.c0);
-  const float lg = __builtin_amdgcn_logf(bp1);  // log2(b + 1)
-  const float num = __builtin_fmaf(p.wf2 * lg, C, __builtin_fmaf(p.wb, C, p.wu * W));
-  return num * __builtin_amdgcn_rcpf(bp1 * C);
+  const float r = __builtin_amdgcn_rcpf(bp1 * C);
+  const float al = C * r;
+  return PhiTerms{al, W * r, __builtin_amdgcn_logf(bp1) * al};
+}
+__device__ __forceinline__ float phi_of(const QParams& p, const PhiTerms& t) {
+  return __builtin_fmaf(p.wb, t.al, __builtin_fmaf(p.wu, t.be, p.wf2 * t.ga));
+}
+__device__ __forceinline__ float phi_f32(int b, float arrival, float now, const QParams& p, const CostF& c) {
+  return phi_of(p, phi_terms(b, arrival, now, c));
 }
 
 // Order-preserving key of a score computed in registers: NaN -> -inf,

@@ -32,7 +32,11 @@ struct CandBufs {
   uint64_t* bounds2;   // [slot]: every composite >= bound2 is in the slots or the overflow
 };
 
-SelectPlan plan_select(int64_t n, int32_t n_theta, int32_t B);
+// packed: each workgroup takes a full pass of chunks (the many-vector step).
+SelectPlan plan_select(int64_t n, int32_t n_theta, int32_t B, bool packed = false);
+// The plan ewsjf_step uses: packed for several vectors over a pool that fits
+// one pass per workgroup.
+SelectPlan plan_step(int64_t n, int32_t n_theta, int32_t B);
 
 // Tactical step (Algorithm 1): the batch plan computed on the device after
 // the head-of-line pass.  Row 0 of the queue-order selection drains q_sel[0]

@@ -345,6 +345,111 @@ __device__ __forceinline__ void load_one(const Src& src, int64_t n, int G, int p
 // point, so the load/score interleaving below stays as written.
 __device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
 
+// Publishes a workgroup's filtered list list2[0..cnt) (every element of the
+// share >= lowc) into its M slots, overflow list and bounds.  Called by the
+// whole block (cnt is uniform).  kClearRank: leave the rank sums at zero for
+// another list in the same kernel.
+template <bool kClearRank>
+__device__ __forceinline__ void publish_list(ListShared& ls, int cnt, uint64_t lowc, int M, size_t slot,
+                                             const CandBufs& cb) {
+  const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
+  uint64_t* out_list = cb.lists + slot * (size_t)M;
+  uint64_t* over_list = cb.over + slot * (size_t)kOverCap;
+  if (cnt > kListCap) {
+    for (int i = threadIdx.x; i < M; i += kBlock) out_list[i] = 0ull;
+    if (threadIdx.x == 0) {
+      cb.counts[slot] = 0u;
+      cb.bounds[slot] = ~0ull;
+      cb.bounds2[slot] = ~0ull;
+      cb.over_cnt[slot] = 0u;
+    }
+    return;
+  }
+  if (cnt <= M) {
+    for (int i = threadIdx.x; i < M; i += kBlock) out_list[i] = i < cnt ? ls.list2[i] : 0ull;
+    if (threadIdx.x == 0) {
+      cb.counts[slot] = (uint32_t)cnt;
+      cb.bounds[slot] = lowc;
+      cb.bounds2[slot] = lowc;
+      cb.over_cnt[slot] = 0u;
+    }
+    return;
+  }
+  // Keep exactly the M largest: every element >= the M-th largest is listed.
+  // Each element's rank is the number of larger entries (composites are
+  // distinct, so ranks are 0..cnt-1).  The entries ranked below the M slots
+  // go to the overflow list (up to kOverCap of them), which the merge reads
+  // before it would re-read the share from the pool.
+  const int listed = min(cnt, M + kOverCap);
+  auto place = [&](uint64_t x, int rank) {
+    if (rank < M) out_list[rank] = x;
+    else if (rank < listed) over_list[rank - M] = x;
+    if (rank == M - 1) {
+      cb.counts[slot] = (uint32_t)M;
+      cb.bounds[slot] = x > lowc ? x : lowc;
+    }
+    if (rank == listed - 1) cb.bounds2[slot] = (cnt <= M + kOverCap || x < lowc) ? lowc : x;
+  };
+  if (cnt <= kShortList) {
+    // The common case: every wave holds all entries (up to 4 per lane),
+    // compares them with its own few (entries w, w + 16, ...) and adds its
+    // counts into LDS, so no wave runs a long serial chain.
+    constexpr int kG = kShortList / kWave;
+    const int ng = (cnt + kWave - 1) / kWave;  // entries per lane in use
+    uint64_t x[kG];
+    int part[kG];
+#pragma unroll
+    for (int g = 0; g < kG; ++g) {
+      x[g] = g < ng && g * kWave + lane < cnt ? ls.list2[g * kWave + lane] : 0ull;
+      part[g] = 0;
+    }
+    // This wave's entries j = wv + 16 i, four reads at a time (an entry past
+    // the list reads as 0, which is never larger).
+    for (int j0 = wv; j0 < cnt; j0 += 4 * kWavesPerBlock) {
+      uint64_t y[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int j = j0 + u * kWavesPerBlock;
+        y[u] = j < cnt ? ls.list2[j] : 0ull;
+      }
+#pragma unroll
+      for (int g = 0; g < kG; ++g)
+        if (g < ng) {
+#pragma unroll
+          for (int u = 0; u < 4; ++u) part[g] += y[u] > x[g];
+        }
+    }
+#pragma unroll
+    for (int g = 0; g < kG; ++g)
+      if (g < ng && g * kWave + lane < cnt && part[g] != 0) atomicAdd(&ls.rank[g * kWave + lane], part[g]);
+    __syncthreads();
+    if (wv < kG && threadIdx.x < cnt) {
+      place(ls.list2[threadIdx.x], ls.rank[threadIdx.x]);
+      if (kClearRank) ls.rank[threadIdx.x] = 0;  // ready for the next list
+    }
+    if (threadIdx.x == 0) cb.over_cnt[slot] = (uint32_t)(listed - M);
+    return;
+  }
+  // Longer lists: tpe consecutive lanes count each element's rank, each over
+  // a slice of the list, and sum with lane exchanges.
+  int tpe = 1;
+  if (cnt > 128)
+    while (tpe < kWave && 2 * tpe * cnt <= kBlock) tpe *= 2;
+  const int e = threadIdx.x / tpe, part = threadIdx.x & (tpe - 1);
+  const int per = (cnt + tpe - 1) / tpe;
+  uint64_t x = 0;
+  int rank = 0;
+  if (e < cnt) {
+    x = ls.list2[e];
+    const int j0 = part * per, j1 = min(cnt, j0 + per);
+#pragma unroll 8
+    for (int j = j0; j < j1; ++j) rank += ls.list2[j] > x;
+  }
+  for (int o = 1; o < tpe; o <<= 1) rank += (int)xor_lane_u32_dyn((uint32_t)rank, o);
+  if (e < cnt && part == 0) place(x, rank);
+  if (threadIdx.x == 0) cb.over_cnt[slot] = (uint32_t)(listed - M);
+}
+
 template <class Src>
 __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, int G, int lg, int M, CandBufs cb) {
   __shared__ typename Src::Shared sh;
@@ -524,7 +629,6 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
   // Publish into the workgroup's M fixed slots (unused slots hold 0).
   const size_t slot = (size_t)t * G + blockIdx.x;
   uint64_t* out_list = cb.lists + slot * (size_t)M;
-  uint64_t* over_list = cb.over + slot * (size_t)kOverCap;
   if (ls.ovf != 0) {
     for (int i = threadIdx.x; i < M; i += kBlock) out_list[i] = 0ull;
     if (threadIdx.x == 0) {
@@ -598,97 +702,145 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
   keep_into_list2(lane < ls.wcnt[wv] ? ls.list[threadIdx.x] : 0ull);
   if (Src::kClustered && ls.nspill != 0) keep_into_list2(ls.spill[threadIdx.x]);  // uniform
   __syncthreads();
-  const int cnt = ls.nout;
-  if (cnt > kListCap) {
-    for (int i = threadIdx.x; i < M; i += kBlock) out_list[i] = 0ull;
-    if (threadIdx.x == 0) {
-      cb.counts[slot] = 0u;
-      cb.bounds[slot] = ~0ull;
-      cb.bounds2[slot] = ~0ull;
-      cb.over_cnt[slot] = 0u;
+  publish_list<false>(ls, ls.nout, lowc, M, slot, cb);
+}
+
+
+// ---------------------------------------------------------------------------
+// Many parameter vectors over one pool (ewsjf_step with n_theta > 1).  Each
+// workgroup reads its share of the pool once (one pass: at most 64 chunks)
+// and lists candidates for kThetaPerBlock vectors in turn.  Routing, the
+// log, the reciprocal and the wait are the same for every vector, so they
+// are computed once per request as three terms,
+//   alpha = 1 / (b+1),  beta = W / ((b+1) C),  gamma = log2(b+1) / (b+1),
+// and a vector's score is Phi = (q+1) w_b alpha + (q+1) w_u beta +
+// (q+1) w_f ln2 gamma (Eq. 1 / Eq. 4 regrouped), three FMAs with the
+// folded per-queue weights.  The list work per vector is as in
+// local_candidates; the counters it uses alternate between two copies, so
+// one vector's list can be published while the next vector's keys are
+// formed, without a workgroup barrier in between.
+// ---------------------------------------------------------------------------
+constexpr int kThetaPerBlock = 16;
+
+__global__ __launch_bounds__(kBlock) void local_candidates_multi(PoolSource src, int64_t n, int n_theta, int G,
+                                                                 int lg, int M, CandBufs cb) {
+  __shared__ uint8_t lut[kLutBytes];
+  __shared__ QParams qp[kThetaPerBlock][EWSJF_MAX_QUEUES];
+  __shared__ ListShared ls;
+  __shared__ int s_ovf[2], s_nout[2];
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = tid / kWave;
+  const int t0 = blockIdx.y * kThetaPerBlock;
+  const int nt = n_theta - t0 < kThetaPerBlock ? n_theta - t0 : kThetaPerBlock;
+
+  // This wave's four chunks first (the longest wait), then the table and the
+  // block's parameter vectors into LDS.
+  PoolSource::Raw raw[kChunksPerPass];
+#pragma unroll
+  for (int j = 0; j < kChunksPerPass; ++j) raw[j] = src.load_chunk(chunk_of(G, 0, j), n, lane);
+  {
+    const i32x4* lsrc = reinterpret_cast<const i32x4*>(src.table->lut);
+    i32x4* ldst = reinterpret_cast<i32x4*>(lut);
+    for (int i = tid; i < kLutBytes / 16; i += kBlock) ldst[i] = lsrc[i];
+    const int k = src.table->k;
+    for (int i = tid; i < nt * EWSJF_MAX_QUEUES; i += kBlock) {
+      const int tt = i / EWSJF_MAX_QUEUES, q = i % EWSJF_MAX_QUEUES;
+      if (q < k) qp[tt][q] = make_qparams(src.theta[t0 + tt], src.table->mean[q], q);
     }
-    return;
   }
-  if (cnt <= M) {
-    for (int i = threadIdx.x; i < M; i += kBlock) out_list[i] = i < cnt ? ls.list2[i] : 0ull;
-    if (threadIdx.x == 0) {
-      cb.counts[slot] = (uint32_t)cnt;
-      cb.bounds[slot] = lowc;
-      cb.bounds2[slot] = lowc;
-      cb.over_cnt[slot] = 0u;
-    }
-    return;
+  const int L = src.table->max_len;
+  if (tid < 2) {
+    s_ovf[tid] = 0;
+    s_nout[tid] = 0;
   }
-  // Keep exactly the M largest: every element >= the M-th largest is listed.
-  // Each element's rank is the number of larger entries (composites are
-  // distinct, so ranks are 0..cnt-1).  The entries ranked below the M slots
-  // go to the overflow list (up to kOverCap of them), which the merge reads
-  // before it would re-read the share from the pool.
-  const int listed = min(cnt, M + kOverCap);
-  auto place = [&](uint64_t x, int rank) {
-    if (rank < M) out_list[rank] = x;
-    else if (rank < listed) over_list[rank - M] = x;
-    if (rank == M - 1) {
-      cb.counts[slot] = (uint32_t)M;
-      cb.bounds[slot] = x > lowc ? x : lowc;
+  if (tid < kShortList) ls.rank[tid] = 0;
+  __syncthreads();
+
+  // Per request: queue (-1 for an empty slot) and the three terms.
+  int qv[kElemsPerLane];
+  PhiTerms tm[kElemsPerLane];
+#pragma unroll
+  for (int e = 0; e < kElemsPerLane; ++e) {
+    const int b = raw[e / 4].l[e & 3];
+    qv[e] = b > 0 ? (int)lut[min(b, L)] : -1;
+    tm[e] = phi_terms(b, raw[e / 4].a[e & 3], src.now, src.cost);
+  }
+
+  uint64_t* const region = ls.list + wv * kWaveCap;
+  for (int tt = 0; tt < nt; ++tt) {
+    const int t = t0 + tt, pb = tt & 1;
+    uint32_t key[kElemsPerLane];
+#pragma unroll
+    for (int e = 0; e < kElemsPerLane; ++e) {
+      const float phi = phi_of(qp[tt][qv[e] < 0 ? 0 : qv[e]], tm[e]);
+      key[e] = qv[e] >= 0 ? ukey_fast(phi) : 0u;
     }
-    if (rank == listed - 1) cb.bounds2[slot] = (cnt <= M + kOverCap || x < lowc) ? lowc : x;
-  };
-  if (cnt <= kShortList) {
-    // The common case: every wave holds all entries (up to 4 per lane),
-    // compares them with its own few (entries w, w + 16, ...) and adds its
-    // counts into LDS, so no wave runs a long serial chain.
-    constexpr int kG = kShortList / kWave;
-    const int ng = (cnt + kWave - 1) / kWave;  // entries per lane in use
-    uint64_t x[kG];
-    int part[kG];
+    uint32_t lmax = 0;
 #pragma unroll
-    for (int g = 0; g < kG; ++g) {
-      x[g] = g < ng && g * kWave + lane < cnt ? ls.list2[g * kWave + lane] : 0ull;
-      part[g] = 0;
-    }
-    // This wave's entries j = wv + 16 i, four reads at a time (an entry past
-    // the list reads as 0, which is never larger).
-    for (int j0 = wv; j0 < cnt; j0 += 4 * kWavesPerBlock) {
-      uint64_t y[4];
+    for (int e = 0; e < 12; ++e) lmax = key[e] > lmax ? key[e] : lmax;
+    uint32_t my_bar = wave_group_bar(lmax, lg);
+    int wcnt = 0;
+    auto emit = [&](uint32_t thr) {
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int j = j0 + u * kWavesPerBlock;
-        y[u] = j < cnt ? ls.list2[j] : 0ull;
-      }
-#pragma unroll
-      for (int g = 0; g < kG; ++g)
-        if (g < ng) {
-#pragma unroll
-          for (int u = 0; u < 4; ++u) part[g] += y[u] > x[g];
+      for (int e = 0; e < kElemsPerLane; ++e) {
+        const bool p = key[e] >= thr;
+        const uint64_t sm = __ballot(p);
+        if (sm != 0ull) {
+          const int pos = wcnt + lanes_below(sm);
+          if (p && pos < kWaveCap)
+            region[pos] = make_comp(key[e], (uint32_t)(chunk_of(G, 0, e / 4) * kChunk + lane * 4 + (e & 3)));
+          wcnt += __popcll(sm);
         }
+      }
+    };
+    emit(my_bar > 1u ? my_bar : 1u);
+    if (wcnt > kWaveCap) {  // as in local_candidates: raise the bar to fit the region
+      const uint32_t kth = wave_kth_largest(key, kWaveCap);
+      if (kth != 0xFFFFFFFFu) {
+        my_bar = kth + 1u > my_bar ? kth + 1u : my_bar;
+        wcnt = 0;
+        emit(my_bar);
+      }
     }
-#pragma unroll
-    for (int g = 0; g < kG; ++g)
-      if (g < ng && g * kWave + lane < cnt && part[g] != 0) atomicAdd(&ls.rank[g * kWave + lane], part[g]);
+    if (lane == 0) {
+      ls.bar[wv] = my_bar;
+      ls.wcnt[wv] = wcnt < kWaveCap ? wcnt : kWaveCap;
+      if (wcnt > kWaveCap) s_ovf[pb] = 1;
+    }
     __syncthreads();
-    if (wv < kG && threadIdx.x < cnt) place(ls.list2[threadIdx.x], ls.rank[threadIdx.x]);
-    if (threadIdx.x == 0) cb.over_cnt[slot] = (uint32_t)(listed - M);
-    return;
+    // Every wave is past the previous vector now: clear its counters.
+    if (tid == 0) {
+      s_ovf[pb ^ 1] = 0;
+      s_nout[pb ^ 1] = 0;
+    }
+    const size_t slot = (size_t)t * G + blockIdx.x;
+    if (s_ovf[pb] != 0) {  // uniform
+      for (int i = tid; i < M; i += kBlock) cb.lists[slot * (size_t)M + i] = 0ull;
+      if (tid == 0) {
+        cb.counts[slot] = 0u;
+        cb.bounds[slot] = ~0ull;  // nothing guaranteed: the merge re-reads this share
+        cb.bounds2[slot] = ~0ull;
+        cb.over_cnt[slot] = 0u;
+      }
+      continue;
+    }
+    uint32_t T_bar = 0;
+#pragma unroll
+    for (int i = 0; i < kWavesPerBlock; ++i) T_bar = ls.bar[i] > T_bar ? ls.bar[i] : T_bar;
+    const uint64_t lowc = (uint64_t)T_bar << 32;
+    {
+      const uint64_t x = lane < ls.wcnt[wv] ? ls.list[tid] : 0ull;
+      const bool keep = x >= lowc && x != 0ull;
+      const uint64_t bal = __ballot(keep);
+      if (bal) {
+        int b0 = 0;
+        if (lane == 0) b0 = atomicAdd(&s_nout[pb], __popcll(bal));
+        b0 = __shfl(b0, 0);
+        if (keep) ls.list2[b0 + __popcll(bal & lanemask_lt())] = x;
+      }
+    }
+    __syncthreads();
+    publish_list<true>(ls, s_nout[pb], lowc, M, slot, cb);
   }
-  // Longer lists: tpe consecutive lanes count each element's rank, each over
-  // a slice of the list, and sum with lane exchanges.
-  int tpe = 1;
-  if (cnt > 128)
-    while (tpe < kWave && 2 * tpe * cnt <= kBlock) tpe *= 2;
-  const int e = threadIdx.x / tpe, part = threadIdx.x & (tpe - 1);
-  const int per = (cnt + tpe - 1) / tpe;
-  uint64_t x = 0;
-  int rank = 0;
-  if (e < cnt) {
-    x = ls.list2[e];
-    const int j0 = part * per, j1 = min(cnt, j0 + per);
-#pragma unroll 8
-    for (int j = j0; j < j1; ++j) rank += ls.list2[j] > x;
-  }
-  for (int o = 1; o < tpe; o <<= 1) rank += (int)xor_lane_u32_dyn((uint32_t)rank, o);
-  if (e < cnt && part == 0) place(x, rank);
-  if (threadIdx.x == 0) cb.over_cnt[slot] = (uint32_t)(listed - M);
 }
 
 // ---------------------------------------------------------------------------
@@ -1063,10 +1215,12 @@ __global__ __launch_bounds__(kBlock) void merge_candidates(Src src0, int64_t n, 
 // ---------------------------------------------------------------------------
 // Host-side launch helpers.
 // ---------------------------------------------------------------------------
-SelectPlan plan_select(int64_t n, int32_t n_theta, int32_t B) {
+SelectPlan plan_select(int64_t n, int32_t n_theta, int32_t B, bool packed) {
   SelectPlan p;
   const int64_t nchunks = (n + kChunk - 1) / kChunk;
-  int64_t G = (nchunks + kWavesPerBlock - 1) / kWavesPerBlock;
+  // Packed: every wave holds all four chunks of its one pass.
+  const int64_t per_wg = packed ? (int64_t)kWavesPerBlock * kChunksPerPass : (int64_t)kWavesPerBlock;
+  int64_t G = (nchunks + per_wg - 1) / per_wg;
   if (G < 1) G = 1;
   if (G > kMaxGrid) G = kMaxGrid;
   p.G = (int)G;
@@ -1117,11 +1271,21 @@ static CandBufs carve(const SelectPlan& p, void* ws) {
   return c;
 }
 
+static bool step_packed(int64_t n, int32_t n_theta) {
+  const int64_t nchunks = (n + kChunk - 1) / kChunk;
+  return n_theta > 1 && nchunks <= (int64_t)kMaxGrid * kWavesPerBlock * kChunksPerPass;
+}
+
+SelectPlan plan_step(int64_t n, int32_t n_theta, int32_t B) {
+  return plan_select(n, n_theta, B, step_packed(n, n_theta));
+}
+
 hipError_t launch_step(const int32_t* len, const float* arrival, int64_t n, float now,
                        const ewsjf_queue_table* table, const ewsjf_theta* theta, int32_t n_theta,
                        const ewsjf_cost& cost, int32_t B, int32_t* tomb_len, int32_t* ids, float* top,
                        int32_t* n_sel, void* ws, hipStream_t stream, hipEvent_t* marks) {
-  const SelectPlan p = plan_select(n, n_theta, B);
+  const bool packed = step_packed(n, n_theta);
+  const SelectPlan p = plan_select(n, n_theta, B, packed);
   const CandBufs cb = carve(p, ws);
   PoolSource src;
   src.len = len;
@@ -1130,9 +1294,14 @@ hipError_t launch_step(const int32_t* len, const float* arrival, int64_t n, floa
   src.theta = theta;
   src.now = now;
   src.cost = CostF{(float)cost.c0, (float)cost.c1, (float)cost.c2};
+  const dim3 multi_grid(p.G, (n_theta + kThetaPerBlock - 1) / kThetaPerBlock);
   if (marks == nullptr) {
-    hipLaunchKernelGGL(local_candidates<PoolSource>, dim3(p.G, n_theta), dim3(kBlock), 0, stream, src, n, p.G,
-                       p.lg, p.M, cb);
+    if (packed)
+      hipLaunchKernelGGL(local_candidates_multi, multi_grid, dim3(kBlock), 0, stream, src, n, n_theta, p.G, p.lg,
+                         p.M, cb);
+    else
+      hipLaunchKernelGGL(local_candidates<PoolSource>, dim3(p.G, n_theta), dim3(kBlock), 0, stream, src, n, p.G,
+                         p.lg, p.M, cb);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(merge_candidates<PoolSource>, dim3(n_theta), dim3(kBlock), 0, stream, src, n, p.G, p.M,
@@ -1141,8 +1310,12 @@ hipError_t launch_step(const int32_t* len, const float* arrival, int64_t n, floa
   }
   // The events take the start and end timestamps of each kernel's own
   // dispatch.
-  hipExtLaunchKernelGGL(local_candidates<PoolSource>, dim3(p.G, n_theta), dim3(kBlock), 0, stream, marks[0],
-                        marks[1], 0, src, n, p.G, p.lg, p.M, cb);
+  if (packed)
+    hipExtLaunchKernelGGL(local_candidates_multi, multi_grid, dim3(kBlock), 0, stream, marks[0], marks[1], 0, src, n,
+                          n_theta, p.G, p.lg, p.M, cb);
+  else
+    hipExtLaunchKernelGGL(local_candidates<PoolSource>, dim3(p.G, n_theta), dim3(kBlock), 0, stream, marks[0],
+                          marks[1], 0, src, n, p.G, p.lg, p.M, cb);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipExtLaunchKernelGGL(merge_candidates<PoolSource>, dim3(n_theta), dim3(kBlock), 0, stream, marks[2], marks[3],

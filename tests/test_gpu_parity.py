@@ -212,6 +212,44 @@ def test_step_batched_theta(E):
         check_admission(ids[ti], top[ti], nsel[ti], rids[0], rtop[0], rnsel[0], rs[0])
 
 
+@pytest.mark.parametrize("n,nt,B", [(20011, 37, 64), (300001, 17, 4096), (4095, 2, 100), (1 << 20, 33, 256),
+                                    (1, 5, 8), (0, 3, 16)])
+def test_step_many_vectors_every_vector(E, n, nt, B):
+    # several parameter vectors over one pool (the packed many-vector kernel);
+    # every vector is checked, vector counts not a multiple of the block's 16
+    p = W.make_pool("three", max(n, 1), 31, arrivals="uniform", horizon=300.0, window=None, K=32, B=B, n_theta=nt)
+    L, A = p.length[:n], p.arrival[:n]
+    say(f"step many vectors n={n} n_theta={nt} B={B}")
+    t = oracle.partition(np.clip(p.length, 1, None), init_queues=32, max_queues=32)
+    ids, top, nsel = (host(x) for x in E.step(dev(L), dev(A), p.now, upload(E, t), dev(p.theta), B, p.cost))
+    rids, rtop, rnsel, rs = oracle.step(L, A, p.now, t, p.theta, B, p.cost)
+    for ti in range(nt):
+        check_admission(ids[ti], top[ti], nsel[ti], rids[ti], rtop[ti], rnsel[ti], rs[ti])
+
+
+def test_step_two_vectors_on_the_4m_pool(E):
+    p = W.config(2)
+    theta = np.stack([W.THETA_MID, W.config(3).theta[5]]).astype(np.float32)
+    say("step cfg2 with two vectors")
+    t = oracle_table(p)
+    ids, top, nsel, _ = run_step(E, p, t, theta=theta)
+    rids, rtop, rnsel, rs = oracle.step(p.length, p.arrival, p.now, t, theta, p.B, p.cost)
+    for ti in range(2):
+        check_admission(ids[ti], top[ti], nsel[ti], rids[ti], rtop[ti], rnsel[ti], rs[ti])
+
+
+@pytest.mark.parametrize("kind", W.ADVERSARIAL_KINDS)
+def test_step_many_vectors_adversarial(E, kind):
+    L, A, now = W.adversarial(kind, 100003, 5)
+    theta = W.config(3).theta[:19]
+    say(f"step many vectors adversarial {kind}")
+    t = oracle.partition(np.clip(L, 1, None), init_queues=16, max_queues=16)
+    ids, top, nsel = (host(x) for x in E.step(dev(L), dev(A), now, upload(E, t), dev(theta), 300))
+    rids, rtop, rnsel, rs = oracle.step(L, A, now, t, theta, 300)
+    for ti in range(theta.shape[0]):
+        check_admission(ids[ti], top[ti], nsel[ti], rids[ti], rtop[ti], rnsel[ti], rs[ti])
+
+
 @pytest.mark.parametrize("kind", W.ADVERSARIAL_KINDS)
 @pytest.mark.parametrize("B", [1, 512, 4096])
 def test_step_adversarial(E, kind, B):
