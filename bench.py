@@ -247,24 +247,23 @@ def streaming_bench(steps: int):
         for j in range(nb):
             i = b0 + j
             ev[j][0].record()
-            sched.insert(dl[i], da[i])
-            if i % sw.rp_every == 0:
-                sched.launch_repartition()
-            sched.step(float(nows[i]), tombstone=True)
+            sched.step(float(nows[i]), tombstone=True, length=dl[i], arrival=da[i])
             ev[j][1].record()
+            if i % sw.rp_every == 0:  # over the window after step i's arrivals; in effect from step i + 1
+                sched.launch_repartition()
         torch.cuda.synchronize()
         for j in range(nb):
             lat[b0 + j] = ev[j][0].elapsed_time(ev[j][1]) * 1e3
     steady = lat[100:] if steps > 100 else lat
-    rp = lat[101::sw.rp_every] if steps > 101 else np.zeros(0)
+    rp = lat[101::sw.rp_every] if steps > 101 else np.zeros(0)  # the steps that take a new table
     return {"workload": "streaming_drift_1m: 1,048,576-slot ring, 4,096 arrivals and B=512 admissions per step, "
                         "64-queue Refine-and-Prune over the last 65,536 arrivals every 100 steps (side stream, "
                         "effective the next step), short-request weight drifting 0.9 -> 0.3",
             "steps": steps, "p50_us": float(np.percentile(steady, 50)), "p99_us": float(np.percentile(steady, 99)),
             "mean_us": float(steady.mean()), "max_us": float(steady.max()),
             "after_repartition_p50_us": float(np.median(rp)) if rp.size else None,
-            "latency": "device time from the step's first insert copy to the end of its admission, "
-                       "steps 100.. (steps before 100 are warm-up)",
+            "latency": "device time of one step (arrivals inserted and admission, ewsjf_ring_step), steps 100.. "
+                       "(steps before 100 are warm-up)",
             "percentiles_us": {str(q): float(np.percentile(steady, q)) for q in (10, 25, 50, 75, 90, 95, 99)},
             "slowest_steps": [[int(i), float(lat[i])] for i in np.argsort(lat)[::-1][:8]]}
 

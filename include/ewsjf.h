@@ -20,6 +20,9 @@
  *   ewsjf_step       route + score + select fused into one pass over the pool.
  *   ewsjf_ring_insert  new requests into a ring pool and the partition window
  *                    (the streaming scheduler's per-step update).
+ *   ewsjf_ring_step  ewsjf_ring_insert + ewsjf_step (one vector) in the same two
+ *                    kernels: the streaming scheduler's per-step update and
+ *                    admission.
  *   ewsjf_tactical_step  Algorithm 1's own batch rule: the head-of-line score
  *                    of every queue, the ArgMax queue drained oldest first,
  *                    backfill from its neighbours, removal of queues that stay
@@ -230,6 +233,22 @@ ewsjf_status ewsjf_step_timed(int32_t* len, const float* arrival, int64_t n, flo
 ewsjf_status ewsjf_ring_insert(int32_t* ring_len, float* ring_arrival, int64_t capacity, int64_t pos,
                                int32_t* window, int64_t window_cap, int64_t wpos, const int32_t* new_len,
                                const float* new_arrival, int64_t n, hipStream_t stream);
+
+/* The streaming scheduler's step (Section 3.2: requests keep joining the pool
+ * between admissions): the effect of ewsjf_ring_insert(ring_len, ring_arrival,
+ * capacity, pos, window, window_cap, wpos, new_len, new_arrival, n_new) followed
+ * by ewsjf_step over the ring (n = capacity) with one parameter vector, in the
+ * step's two kernels: the streaming kernel substitutes the new requests for the
+ * slots it loads and stores them (and their lengths into the window), so there
+ * is no separate insert launch.  Arguments and rules as for those two calls
+ * (ring arrays 16-byte aligned; workspace ewsjf_workspace_bytes(EWSJF_OP_STEP,
+ * capacity, 1, B, NULL)); the new arrays must not overlap the ring or the
+ * window.  EWSJF_STEP_TOMBSTONE empties the admitted slots after selection. */
+ewsjf_status ewsjf_ring_step(int32_t* ring_len, float* ring_arrival, int64_t capacity, int64_t pos, int32_t* window,
+                             int64_t window_cap, int64_t wpos, const int32_t* new_len, const float* new_arrival,
+                             int64_t n_new, float now, const void* table, const ewsjf_theta* theta,
+                             const ewsjf_cost* cost, int32_t B, int32_t flags, int32_t* ids, float* top,
+                             int32_t* n_sel, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* One step of the tactical loop as Algorithm 1 states it (Section 3.2),
  * over per-queue FIFOs of the pending pool:

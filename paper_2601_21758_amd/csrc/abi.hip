@@ -237,4 +237,31 @@ ewsjf_status ewsjf_tactical_step(int32_t* len, const float* arrival, int64_t n, 
                                               head_score, removed, ws, stream));
 }
 
+ewsjf_status ewsjf_ring_step(int32_t* ring_len, float* ring_arrival, int64_t capacity, int64_t pos, int32_t* window,
+                             int64_t window_cap, int64_t wpos, const int32_t* new_len, const float* new_arrival,
+                             int64_t n_new, float now, const void* table, const ewsjf_theta* theta,
+                             const ewsjf_cost* cost, int32_t B, int32_t flags, int32_t* ids, float* top,
+                             int32_t* n_sel, void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (ring_len == nullptr || ring_arrival == nullptr || table == nullptr || theta == nullptr || cost == nullptr ||
+      ids == nullptr || top == nullptr || n_sel == nullptr || ws == nullptr)
+    return EWSJF_ERR_NULL;
+  if (n_new > 0 && (new_len == nullptr || new_arrival == nullptr)) return EWSJF_ERR_NULL;
+  if (window_cap > 0 && window == nullptr) return EWSJF_ERR_NULL;
+  if (capacity < 1 || capacity > kMaxN || pos < 0 || pos >= capacity || n_new < 0 || n_new > capacity)
+    return EWSJF_ERR_ARG;
+  if (window_cap < 0 || window_cap > kMaxN || wpos < 0 || (window_cap > 0 && (wpos >= window_cap || n_new > window_cap)) ||
+      (window_cap == 0 && wpos != 0))
+    return EWSJF_ERR_ARG;
+  if (B < 1 || B > EWSJF_MAX_B || !cost_ok(cost) || !std::isfinite(now)) return EWSJF_ERR_ARG;
+  if ((flags & ~EWSJF_STEP_TOMBSTONE) != 0) return EWSJF_ERR_ARG;
+  if (ws_bytes < ewsjf::plan_select(capacity, 1, B).ws_bytes) return EWSJF_ERR_WORKSPACE;
+  if (!aligned16(ring_len) || !aligned16(ring_arrival) || !aligned16(ws)) return EWSJF_ERR_ALIGN;
+  const ewsjf_status ds = check_device();
+  if (ds != EWSJF_OK) return ds;
+  return launched(ewsjf::launch_ring_step(ring_len, ring_arrival, capacity, pos, window, window_cap, wpos, new_len,
+                                          new_arrival, n_new, now, static_cast<const ewsjf_queue_table*>(table),
+                                          theta, *cost, B, (flags & EWSJF_STEP_TOMBSTONE) ? ring_len : nullptr, ids,
+                                          top, n_sel, ws, stream));
+}
+
 }  // extern "C"

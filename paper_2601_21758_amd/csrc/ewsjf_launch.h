@@ -55,6 +55,13 @@ hipError_t launch_fifo_select(const int32_t* len, const float* arrival, int64_t 
                               const TacticalPlan* plan, int32_t B, int32_t* ids, float* top, int32_t* n_sel, void* ws,
                               hipStream_t stream);
 
+// ring insert + one-vector step in the same two kernels (ewsjf_ring_step)
+hipError_t launch_ring_step(int32_t* ring_len, float* ring_arrival, int64_t capacity, int64_t pos, int32_t* window,
+                            int64_t window_cap, int64_t wpos, const int32_t* new_len, const float* new_arrival,
+                            int64_t n_new, float now, const ewsjf_queue_table* table, const ewsjf_theta* theta,
+                            const ewsjf_cost& cost, int32_t B, int32_t* tomb_len, int32_t* ids, float* top,
+                            int32_t* n_sel, void* ws, hipStream_t stream);
+
 size_t tactical_ws_bytes(int64_t n, int32_t B);
 hipError_t launch_tactical_step(int32_t* len, const float* arrival, int64_t n, float now, ewsjf_queue_table* table,
                                 const ewsjf_theta* theta, const ewsjf_cost& cost, int32_t B, int32_t empty_threshold,

@@ -228,6 +228,57 @@ struct FifoSource {
   static constexpr bool kClustered = true;
 };
 
+// The streaming pool with this step's arrivals (the streaming scheduler's
+// per-step update fused into the step): a ring of request slots, of which
+// the slots (pos + i) mod capacity, i < n_new, take new request i.  The
+// streaming kernel substitutes the new requests for the loaded slots of the
+// chunks that hold them and writes them to the ring (and their lengths to
+// the partition window), so the step sees the pool after the insert and
+// later steps find it stored.
+struct RingSource : PoolSource {
+  int32_t* ring_len;
+  float* ring_arrival;
+  int64_t capacity, pos;
+  int32_t* window;
+  int64_t window_cap, wpos;
+  const int32_t* new_len;
+  const float* new_arrival;
+  int64_t n_new;
+
+  __device__ __forceinline__ Raw load_chunk(int64_t c, int64_t n, int lane) const {
+    Raw r = PoolSource::load_chunk(c, n, lane);
+    const int64_t first = c * kChunk;
+    if (first < n) {  // wave-uniform from here on
+      int64_t d0 = first - pos;
+      if (d0 < 0) d0 += capacity;
+      int64_t d1 = pos - first;
+      if (d1 < 0) d1 += capacity;
+      if (d0 < n_new || d1 < kChunk) {  // the chunk holds new requests
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int64_t slot = first + 4 * lane + e;
+          int64_t d = slot - pos;
+          if (d < 0) d += capacity;
+          if (slot < n && d < n_new) {
+            const int32_t b = new_len[d];
+            const float a = new_arrival[d];
+            r.l[e] = b;
+            r.a[e] = a;
+            ring_len[slot] = b;
+            ring_arrival[slot] = a;
+            if (window_cap > 0) {
+              int64_t w = wpos + d;
+              if (w >= window_cap) w -= window_cap;
+              window[w] = b;
+            }
+          }
+        }
+      }
+    }
+    return r;
+  }
+};
+
 struct ScoreSource {
   const float* score;  // [n_theta][n]
   int64_t n;
@@ -1320,6 +1371,39 @@ hipError_t launch_step(const int32_t* len, const float* arrival, int64_t n, floa
   if (e != hipSuccess) return e;
   hipExtLaunchKernelGGL(merge_candidates<PoolSource>, dim3(n_theta), dim3(kBlock), 0, stream, marks[2], marks[3],
                         0, src, n, p.G, p.M, B, cb, ids, top, n_sel, tomb_len);
+  return hipGetLastError();
+}
+
+hipError_t launch_ring_step(int32_t* ring_len, float* ring_arrival, int64_t capacity, int64_t pos, int32_t* window,
+                            int64_t window_cap, int64_t wpos, const int32_t* new_len, const float* new_arrival,
+                            int64_t n_new, float now, const ewsjf_queue_table* table, const ewsjf_theta* theta,
+                            const ewsjf_cost& cost, int32_t B, int32_t* tomb_len, int32_t* ids, float* top,
+                            int32_t* n_sel, void* ws, hipStream_t stream) {
+  const SelectPlan p = plan_select(capacity, 1, B);
+  const CandBufs cb = carve(p, ws);
+  RingSource src;
+  src.len = ring_len;
+  src.arrival = ring_arrival;
+  src.table = table;
+  src.theta = theta;
+  src.now = now;
+  src.cost = CostF{(float)cost.c0, (float)cost.c1, (float)cost.c2};
+  src.ring_len = ring_len;
+  src.ring_arrival = ring_arrival;
+  src.capacity = capacity;
+  src.pos = pos;
+  src.window = window;
+  src.window_cap = window_cap;
+  src.wpos = wpos;
+  src.new_len = new_len;
+  src.new_arrival = new_arrival;
+  src.n_new = n_new;
+  hipLaunchKernelGGL(local_candidates<RingSource>, dim3(p.G, 1), dim3(kBlock), 0, stream, src, capacity, p.G, p.lg,
+                     p.M, cb);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(merge_candidates<RingSource>, dim3(1), dim3(kBlock), 0, stream, src, capacity, p.G, p.M, B, cb,
+                     ids, top, n_sel, tomb_len);
   return hipGetLastError();
 }
 

@@ -195,6 +195,35 @@ def step(length: torch.Tensor, arrival: torch.Tensor, now: float, table: torch.T
     return ids, top, nsel
 
 
+def ring_step(ring_len: torch.Tensor, ring_arrival: torch.Tensor, pos: int, new_len: torch.Tensor,
+              new_arrival: torch.Tensor, now: float, table: torch.Tensor, theta: torch.Tensor, B: int,
+              cost_=DEFAULT_COST, window: torch.Tensor | None = None, wpos: int = 0, tombstone: bool = False, out=None,
+              ws: Workspace | None = None, stream=None):
+    """ring_insert + step (one vector) fused (ewsjf_ring_step)."""
+    _need(ring_len, torch.int32, "ring_len")
+    _need(ring_arrival, torch.float32, "ring_arrival")
+    _need(new_len, torch.int32, "new_len")
+    _need(new_arrival, torch.float32, "new_arrival")
+    if window is not None:
+        _need(window, torch.int32, "window")
+    theta = _theta(theta)
+    if theta.shape[0] != 1:
+        raise ValueError("ring_step takes one parameter vector")
+    cap = ring_len.numel()
+    ids, top, nsel = _outs(1, B, ring_len.device, out)
+    ws = ws or Workspace(ring_len.device)
+    buf = ws.get(workspace_bytes(L.OP_STEP, cap, 1, B))
+    c = _cost(cost_)
+    wp, wc = (_vp(window), window.numel()) if window is not None else (None, 0)
+    flags = L.STEP_TOMBSTONE if tombstone else 0
+    L.check(L.lib().ewsjf_ring_step(_vp(ring_len), _vp(ring_arrival), cap, int(pos), wp, wc, int(wpos),
+                                    _vp(new_len), _vp(new_arrival), new_len.numel(), float(now), _vp(table),
+                                    _vp(theta), C.byref(c), int(B), flags, _vp(ids), _vp(top), _vp(nsel), _vp(buf),
+                                    buf.numel(), _stream(stream)),
+            "ewsjf_ring_step")
+    return ids, top, nsel
+
+
 def new_empty_counters(device=None) -> torch.Tensor:
     """Per-queue empty-step counters for tactical_step (zero for a new table)."""
     return torch.zeros(L.MAX_QUEUES, dtype=torch.int32, device=device)

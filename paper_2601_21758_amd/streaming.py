@@ -2,16 +2,17 @@
 window of recent arrival lengths, and double-buffered queue tables.
 
 Each step inserts the step's arrivals into the ring (request id = ring slot;
-an overwritten, still-pending request is evicted), optionally launches
-Refine-and-Prune over the window on a side stream, and runs the fused step
-(route + score + top-B admission), tombstoning the admitted slots.  The
-partition launched at step s sees the window after step s's arrivals and
-takes effect at step s + 1: the paper runs the partitioner off the
-critical path, in the strategic loop (Section 3.1; Section 5), over a window
-of recent requests (Section 4.2).
+an overwritten, still-pending request is evicted) and runs the fused step
+(route + score + top-B admission), tombstoning the admitted slots; with
+step(now, length=..., arrival=...) the insert happens inside the step's own
+kernels (ewsjf_ring_step).  After step s, launch_repartition() starts
+Refine-and-Prune over the window (which holds step s's arrivals) on a side
+stream; the new table takes effect at step s + 1.  The paper runs the
+partitioner off the critical path, in the strategic loop (Section 3.1;
+Section 5), over a window of recent requests (Section 4.2).
 
-Every step runs in libewsjf.so's kernels: ewsjf_ring_insert, ewsjf_partition
-and ewsjf_step.
+Every step runs in libewsjf.so's kernels: ewsjf_ring_step (or
+ewsjf_ring_insert and ewsjf_step), and ewsjf_partition.
 """
 from __future__ import annotations
 
@@ -109,15 +110,28 @@ class StreamingScheduler:
             done.record(self.side)
         self.pending = done
 
-    def step(self, now: float, tombstone: bool = True):
-        """One scheduling step over the ring: (ids[1,B], top[1,B], n_sel[1])."""
+    def step(self, now: float, tombstone: bool = True, length: torch.Tensor | None = None,
+             arrival: torch.Tensor | None = None):
+        """One scheduling step over the ring: (ids[1,B], top[1,B], n_sel[1]).
+        With length/arrival, the step's arrivals are inserted first, inside
+        the step's kernels (same effect as insert() then step())."""
         main = torch.cuda.current_stream(self.device)
         if self.pending is not None:
             main.wait_event(self.pending)
             self.cur = 1 - self.cur
             self.pending = None
-        return ewsjf.step(self.len, self.arr, now, self.tables[self.cur], self.theta, self.B, self.cost,
-                          tombstone=tombstone, out=self.out, ws=self.ws_step)
+        if length is None:
+            return ewsjf.step(self.len, self.arr, now, self.tables[self.cur], self.theta, self.B, self.cost,
+                              tombstone=tombstone, out=self.out, ws=self.ws_step)
+        n = length.numel()
+        if arrival is None or arrival.numel() != n or n > self.capacity or n > self.window:
+            raise ValueError("one step inserts at most min(capacity, window) arrivals")
+        out = ewsjf.ring_step(self.len, self.arr, self.ring_pos, length, arrival, now, self.tables[self.cur],
+                              self.theta, self.B, self.cost, window=self.win, wpos=self.win_pos, tombstone=tombstone,
+                              out=self.out, ws=self.ws_step)
+        self.ring_pos = (self.ring_pos + n) % self.capacity
+        self.win_pos = (self.win_pos + n) % self.window
+        return out
 
     def apply_tombstones(self, ids) -> None:
         """Mark the given slots empty (len = 0)."""

@@ -46,7 +46,8 @@ class OracleStream:
 
     def step(self, now):
         """Route, score and select over the ring with the current table; the
-        partition of the previous repartition() takes effect here first."""
+        partition of the previous repartition() (called after the previous
+        step) takes effect here first."""
         if self.next_table is not None:
             self.table, self.next_table = self.next_table, None
         ids, top, nsel, sc = oracle.step(self.len, self.arr, now, self.table, self.theta, self.B, self.cost)

@@ -161,6 +161,32 @@ def test_tactical_step_argument_errors():
     assert tac(arr=FAKE_MIS) == L.ERR_ALIGN
 
 
+def test_ring_step_argument_errors():
+    lib = L.lib()
+    c = L.Cost(0.01, 1e-4, 0.0)
+    need = lib.ewsjf_workspace_bytes(L.OP_STEP, 100, 1, 8, None)
+
+    def rs(rl=FAKE, ra=FAKE, cap=100, pos=0, w=FAKE, wc=50, wpos=0, nl=FAKE, na=FAKE, n=10, now=1.0, table=FAKE,
+           theta=FAKE, cost=c, B=8, flags=0, ids=FAKE, top=FAKE, nsel=FAKE, ws=FAKE, wsb=need):
+        return lib.ewsjf_ring_step(rl, ra, cap, pos, w, wc, wpos, nl, na, n, now, table, theta,
+                                   C.byref(cost) if cost is not None else None, B, flags, ids, top, nsel, ws, wsb, None)
+
+    assert rs(rl=None) == L.ERR_NULL
+    assert rs(nl=None) == L.ERR_NULL
+    assert rs(w=None) == L.ERR_NULL
+    assert rs(table=None) == L.ERR_NULL
+    assert rs(cap=0) == L.ERR_ARG
+    assert rs(pos=100) == L.ERR_ARG
+    assert rs(n=101) == L.ERR_ARG
+    assert rs(n=51) == L.ERR_ARG
+    assert rs(wpos=50) == L.ERR_ARG
+    assert rs(B=0) == L.ERR_ARG
+    assert rs(flags=2) == L.ERR_ARG
+    assert rs(now=float("nan")) == L.ERR_ARG
+    assert rs(wsb=need - 1) == L.ERR_WORKSPACE
+    assert rs(ra=FAKE_MIS) == L.ERR_ALIGN
+
+
 def test_partition_argument_errors():
     lib = L.lib()
     need = lib.ewsjf_workspace_bytes(L.OP_PARTITION, 100, 0, 0, C.byref(_p()))

@@ -69,7 +69,7 @@ def test_constructor_rejects_window_larger_than_ring():
 
 
 # ---- lockstep parity on the GPU ---------------------------------------------------
-def _lockstep(capacity, per_step, steps, window, rp_every, B, K, label, tombstone_check_every=0):
+def _lockstep(capacity, per_step, steps, window, rp_every, B, K, label, tombstone_check_every=0, fused=False):
     from paper_2601_21758_amd import ewsjf
     s = W.Streaming(seed=4, capacity=capacity, per_step=per_step, steps=steps, window=window, rp_every=rp_every,
                     B=B, K=K)
@@ -83,15 +83,20 @@ def _lockstep(capacity, per_step, steps, window, rp_every, B, K, label, tombston
     near = 0
     for step in range(steps):
         L, A = s.arrivals(step)
-        gpu.insert(torch.from_numpy(L).cuda(), torch.from_numpy(A).cuda())
+        Lg, Ag = torch.from_numpy(L).cuda(), torch.from_numpy(A).cuda()
         ref.insert(L, A)
         now = float(A[-1])
+        tomb = tombstone_check_every and step % tombstone_check_every == 0
+        if fused:  # the insert inside the step's kernels
+            ids, top, nsel = gpu.step(now, tombstone=bool(tomb), length=Lg, arrival=Ag)
+        else:
+            gpu.insert(Lg, Ag)
+            ids, top, nsel = gpu.step(now, tombstone=bool(tomb))
+        rids, rtop, rnsel, rsc = ref.step(now)
+        # the partition over the window after this step's arrivals takes effect at the next step
         if step % rp_every == 0:
             gpu.launch_repartition()
             rt = ref.repartition()
-        tomb = tombstone_check_every and step % tombstone_check_every == 0
-        ids, top, nsel = gpu.step(now, tombstone=bool(tomb))
-        rids, rtop, rnsel, rsc = ref.step(now)
         torch.cuda.synchronize()
         gi = ids.cpu().numpy()[0]
         near += check_admission(gi, top.cpu().numpy()[0], nsel.cpu().numpy()[0], rids, rtop, rnsel, rsc)
@@ -129,9 +134,19 @@ def test_streaming_lockstep_ring_wraps_many_times():
 
 
 @pytest.mark.gpu
+def test_streaming_lockstep_fused_insert():
+    # arrivals inserted inside the step's kernels (ewsjf_ring_step): a ring
+    # that wraps, with tombstone and partition hand-overs
+    _lockstep(capacity=6144, per_step=1000, steps=30, window=3000, rp_every=4, B=100, K=8, label="fused-wrap",
+              tombstone_check_every=2, fused=True)
+    _lockstep(capacity=1 << 16, per_step=700, steps=60, window=8192, rp_every=10, B=64, K=16, label="fused",
+              tombstone_check_every=5, fused=True)
+
+
+@pytest.mark.gpu
 def test_streaming_lockstep_full_size_prefix():
     # the streaming workload at full size (1,048,576-slot ring, 4,096 arrivals
     # and 512 admissions per step, 65,536-length window, 64 queues): the first
     # 101 steps, so two hand-overs (steps 0 and 100) are covered
     _lockstep(capacity=1 << 20, per_step=4096, steps=101, window=65536, rp_every=100, B=512, K=64, label="full",
-              tombstone_check_every=25)
+              tombstone_check_every=25, fused=True)
