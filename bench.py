@@ -332,6 +332,17 @@ def main() -> int:
     rt.hipEventRecord(e1, C.c_void_p(stream.cuda_stream))
     partition_ms = hip.elapsed_ms(e0, e1) / 10
     k_queues = E.read_table(table)["k"]
+    # the same partition started from the window's kept histogram
+    whist = E.window_histogram(window, prm.max_len)
+    t_hist = E.partition_hist(whist, prm, ws=pws)
+    torch.cuda.synchronize()
+    if not torch.equal(t_hist, table):
+        raise RuntimeError("partition from the histogram differs from the partition of the window")
+    rt.hipEventRecord(e0, C.c_void_p(stream.cuda_stream))
+    for _ in range(10):
+        E.partition_hist(whist, prm, table=t_hist, ws=pws)
+    rt.hipEventRecord(e1, C.c_void_p(stream.cuda_stream))
+    partition_hist_ms = hip.elapsed_ms(e0, e1) / 10
 
     ids = torch.empty((1, B), dtype=torch.int32, device=dev)
     top = torch.empty((1, B), dtype=torch.float32, device=dev)
@@ -433,6 +444,7 @@ def main() -> int:
         "kernels_ms": {"local_candidates": k1_ms, "merge_candidates": k2_ms},
         "eager_ms_per_step": eager_ms, "graph_matches_eager": graph_ok,
         "partition_ms": partition_ms,
+        "partition_from_histogram_ms": partition_hist_ms,
     }
     if not args.no_extra:
         out["tactical"] = tactical_bench(hip, pool, table, lens, arrs)

@@ -8,6 +8,11 @@
 //   window_hist      LDS-privatized histogram of clamped window lengths, one
 //                    partial histogram per workgroup (no global atomics).
 //   hist_reduce      column sums of the partial histograms.
+//   hist_clear /     the same histogram into a caller-owned array, flushed
+//   window_hist_add  with one global atomic per non-empty bin per workgroup
+//                    (the starting point of a histogram that the streaming
+//                    inserts then keep current; the partition can start from
+//                    it instead of from the window).
 //   rp_distinct      one workgroup: distinct values v[], counts c[] and exact
 //                    int64 prefix sums of counts and of count * value.
 //   rp_kmeans3 /     the exact 1-D 3-means initializer: every split (i, j) of
@@ -50,7 +55,8 @@ struct alignas(16) Leaf {
 
 struct PartWs {
   uint32_t* partial;  // [Gh][L+1]
-  uint32_t* hist;     // [L+1]
+  uint32_t* hist_buf; // [L+1] the window's histogram when the partition builds it
+  const uint32_t* hist;  // the histogram the partition reads: hist_buf or the caller's
   int32_t* v;         // [L] distinct values
   uint32_t* c;        // [L] multiplicities
   int64_t* PN;        // [L+1] prefix sums of c
@@ -87,7 +93,8 @@ PartWs carve_part(void* ws, int64_t n, int L) {
     return p;
   };
   w.partial = reinterpret_cast<uint32_t*>(take((size_t)w.Gh * (L + 1) * 4));
-  w.hist = reinterpret_cast<uint32_t*>(take((size_t)(L + 1) * 4));
+  w.hist_buf = reinterpret_cast<uint32_t*>(take((size_t)(L + 1) * 4));
+  w.hist = w.hist_buf;
   w.v = reinterpret_cast<int32_t*>(take((size_t)L * 4));
   w.c = reinterpret_cast<uint32_t*>(take((size_t)L * 4));
   w.PN = reinterpret_cast<int64_t*>(take((size_t)(L + 1) * 8));
@@ -110,22 +117,36 @@ size_t carve_size(int64_t n, int L) {
 }
 
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kBlock) void window_hist(const int32_t* __restrict__ win, int64_t n, int L,
-                                                      uint32_t* __restrict__ partial) {
-  __shared__ uint32_t h[EWSJF_MAX_LEN + 1];
+// This workgroup's share of the window counted into h[0..L] (LDS).
+__device__ void lds_window_hist(const int32_t* __restrict__ win, int64_t n, int L, uint32_t* h) {
   for (int b = threadIdx.x; b <= L; b += kBlock) h[b] = 0u;
   __syncthreads();
   const int64_t per = (n + gridDim.x - 1) / gridDim.x;
   const int64_t beg = per * blockIdx.x;
   const int64_t end = beg + per < n ? beg + per : n;
-  for (int64_t i = beg + threadIdx.x; i < end; i += kBlock) {
-    int x = win[i];
-    x = x < 1 ? 1 : (x > L ? L : x);
-    atomicAdd(&h[x], 1u);
-  }
+  for (int64_t i = beg + threadIdx.x; i < end; i += kBlock) atomicAdd(&h[clamp_len(win[i], L)], 1u);
   __syncthreads();
+}
+
+__global__ __launch_bounds__(kBlock) void window_hist(const int32_t* __restrict__ win, int64_t n, int L,
+                                                      uint32_t* __restrict__ partial) {
+  __shared__ uint32_t h[EWSJF_MAX_LEN + 1];
+  lds_window_hist(win, n, L, h);
   uint32_t* out = partial + (size_t)blockIdx.x * (L + 1);
   for (int b = threadIdx.x; b <= L; b += kBlock) out[b] = h[b];
+}
+
+__global__ void hist_clear(uint32_t* __restrict__ hist, int L) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b <= L) hist[b] = 0u;
+}
+
+__global__ __launch_bounds__(kBlock) void window_hist_add(const int32_t* __restrict__ win, int64_t n, int L,
+                                                          uint32_t* __restrict__ hist) {
+  __shared__ uint32_t h[EWSJF_MAX_LEN + 1];
+  lds_window_hist(win, n, L, h);
+  for (int b = threadIdx.x; b <= L; b += kBlock)
+    if (h[b]) atomicAdd(&hist[b], h[b]);
 }
 
 __global__ void hist_reduce(const uint32_t* __restrict__ partial, int Gh, int L, uint32_t* __restrict__ hist) {
@@ -412,6 +433,21 @@ __global__ __launch_bounds__(kBlock) void rp_refine_prune(PartWs w, ewsjf_partit
   const int V = w.meta[0];
   const int L = p.max_len;
   const double inf = __builtin_inf();
+  if (V == 0) {
+    // An empty histogram (only a caller-kept one can be empty): one queue
+    // that holds nothing and covers every length.
+    if (tid == 0) {
+      w.meta[3] = 0;
+      tab->k = 1;
+      tab->max_len = L;
+      tab->n_distinct = tab->n_coarse = tab->n_leaves = tab->reserved0 = 0;
+      tab->n_window = 0;
+      tab->lo[0] = tab->hi[0] = 0;
+      tab->count[0] = tab->sum[0] = 0;
+      tab->mean[0] = 0.0;
+    }
+    return;
+  }
 
   // ---- Stage 1: coarse cluster starts -------------------------------------
   for (int j = tid; j < V; j += kBlock) sm.u.a.v[j] = (uint16_t)w.v[j];
@@ -526,7 +562,7 @@ __global__ __launch_bounds__(kBlock) void rp_refine_prune(PartWs w, ewsjf_partit
     tab->n_coarse = n_coarse;
     tab->n_leaves = n_leaves;
     tab->reserved0 = 0;
-    tab->n_window = n_window;
+    tab->n_window = n_window >= 0 ? n_window : w.PN[V];
   }
   // Within the queue budget: the leaves are the queues.  Otherwise Stage 3
   // (rp_merge) writes them.
@@ -717,12 +753,13 @@ size_t partition_ws_bytes(int64_t n_window, const ewsjf_partition_params& p) {
   return carve_size(n_window, p.max_len);
 }
 
-hipError_t launch_partition(const int32_t* window, int64_t n_window, const ewsjf_partition_params& p,
-                            ewsjf_queue_table* table, void* ws, hipStream_t stream) {
+namespace {
+
+// Stages 1-3 and the routing lut from the histogram w.hist (n_window < 0:
+// the table records the histogram's total as the window size).
+hipError_t launch_stages(const PartWs& w, const ewsjf_partition_params& p, int64_t n_window, ewsjf_queue_table* table,
+                         hipStream_t stream) {
   const int L = p.max_len;
-  PartWs w = carve_part(ws, n_window, L);
-  hipLaunchKernelGGL(window_hist, dim3(w.Gh), dim3(kBlock), 0, stream, window, n_window, L, w.partial);
-  hipLaunchKernelGGL(hist_reduce, dim3((L + 1 + 255) / 256), dim3(256), 0, stream, w.partial, w.Gh, L, w.hist);
   hipLaunchKernelGGL(rp_distinct, dim3(1), dim3(kBlock), 0, stream, w, L);
   if (p.init_mode == EWSJF_INIT_KMEANS3) {
     hipLaunchKernelGGL(rp_kmeans3, dim3(kKmeansBlocks), dim3(kBlock), 0, stream, w);
@@ -733,6 +770,33 @@ hipError_t launch_partition(const int32_t* window, int64_t n_window, const ewsjf
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   return launch_build_lut(table, stream);
+}
+
+}  // namespace
+
+hipError_t launch_partition(const int32_t* window, int64_t n_window, const ewsjf_partition_params& p,
+                            ewsjf_queue_table* table, void* ws, hipStream_t stream) {
+  const int L = p.max_len;
+  PartWs w = carve_part(ws, n_window, L);
+  hipLaunchKernelGGL(window_hist, dim3(w.Gh), dim3(kBlock), 0, stream, window, n_window, L, w.partial);
+  hipLaunchKernelGGL(hist_reduce, dim3((L + 1 + 255) / 256), dim3(256), 0, stream, w.partial, w.Gh, L, w.hist_buf);
+  return launch_stages(w, p, n_window, table, stream);
+}
+
+hipError_t launch_partition_hist(const uint32_t* hist, const ewsjf_partition_params& p, ewsjf_queue_table* table,
+                                 void* ws, hipStream_t stream) {
+  PartWs w = carve_part(ws, 0, p.max_len);
+  w.hist = hist;
+  return launch_stages(w, p, -1, table, stream);
+}
+
+hipError_t launch_window_histogram(const int32_t* window, int64_t n_window, int L, uint32_t* hist,
+                                   hipStream_t stream) {
+  hipLaunchKernelGGL(hist_clear, dim3((L + 1 + 255) / 256), dim3(256), 0, stream, hist, L);
+  if (n_window > 0)
+    hipLaunchKernelGGL(window_hist_add, dim3(hist_blocks(n_window)), dim3(kBlock), 0, stream, window, n_window, L,
+                       hist);
+  return hipGetLastError();
 }
 
 }  // namespace ewsjf

@@ -11,8 +11,16 @@ stream; the new table takes effect at step s + 1.  The paper runs the
 partitioner off the critical path, in the strategic loop (Section 3.1;
 Section 5), over a window of recent requests (Section 4.2).
 
+With incremental=True (the default) the inserts also keep the window's
+length histogram current (each overwritten length's count moves to the new
+length), and the repartition starts from a copy of that histogram
+(ewsjf_partition_hist) instead of re-reading the window: the same table, bit
+for bit, since Refine-and-Prune sees the window only through its distinct
+lengths and their multiplicities.
+
 Every step runs in libewsjf.so's kernels: ewsjf_ring_step (or
-ewsjf_ring_insert and ewsjf_step), and ewsjf_partition.
+ewsjf_ring_insert and ewsjf_step), and ewsjf_partition_hist (or
+ewsjf_partition).
 """
 from __future__ import annotations
 
@@ -34,11 +42,12 @@ class StreamingScheduler:
 
     capacity: ring slots (request ids); window: partitioner window length;
     B: admissions per step; params: ewsjf.params(...); theta: one parameter
-    vector (6 floats); cost: (c0, c1, c2).
+    vector (6 floats); cost: (c0, c1, c2); incremental: keep the window's
+    histogram and partition from it.
     """
 
     def __init__(self, capacity: int, window: int, B: int, params: L.PartitionParams, theta, cost=ewsjf.DEFAULT_COST,
-                 device="cuda"):
+                 device="cuda", incremental: bool = True):
         if capacity <= 0 or window <= 0 or window > capacity:
             raise ValueError("need 0 < window <= capacity")
         self.device = torch.device(device)
@@ -48,7 +57,13 @@ class StreamingScheduler:
         self.len = torch.zeros(self.capacity, dtype=torch.int32, device=self.device)
         self.arr = torch.zeros(self.capacity, dtype=torch.float32, device=self.device)
         self.win = torch.zeros(self.window, dtype=torch.int32, device=self.device)
-        self.snap = torch.zeros(self.window, dtype=torch.int32, device=self.device)
+        self.incremental = bool(incremental)
+        if self.incremental:  # the window's histogram and the copy a partition reads
+            self.hist = torch.zeros(params.max_len + 1, dtype=torch.int32, device=self.device)
+            self.snap = torch.zeros(params.max_len + 1, dtype=torch.int32, device=self.device)
+        else:  # the copy of the window a partition reads
+            self.hist = None
+            self.snap = torch.zeros(self.window, dtype=torch.int32, device=self.device)
         self.tables = [ewsjf.new_table(self.device), ewsjf.new_table(self.device)]
         self.cur = 0
         self.ws_step = ewsjf.Workspace(self.device)
@@ -80,7 +95,11 @@ class StreamingScheduler:
         self.win.copy_(length[self.capacity - self.window:])
         self.win_pos = 0
         self.ring_pos = 0
-        ewsjf.partition(self.win, self.params, table=self.tables[self.cur], ws=self.ws_part)
+        if self.incremental:
+            ewsjf.window_histogram(self.win, self.params.max_len, hist=self.hist)
+            ewsjf.partition_hist(self.hist, self.params, table=self.tables[self.cur], ws=self.ws_part)
+        else:
+            ewsjf.partition(self.win, self.params, table=self.tables[self.cur], ws=self.ws_part)
         self.pending = None
 
     def insert(self, length: torch.Tensor, arrival: torch.Tensor) -> None:
@@ -89,7 +108,8 @@ class StreamingScheduler:
         n = length.numel()
         if arrival.numel() != n or n > self.capacity or n > self.window:
             raise ValueError("one step inserts at most min(capacity, window) arrivals")
-        ewsjf.ring_insert(self.len, self.arr, self.ring_pos, length, arrival, window=self.win, wpos=self.win_pos)
+        ewsjf.ring_insert(self.len, self.arr, self.ring_pos, length, arrival, window=self.win, wpos=self.win_pos,
+                          hist=self.hist)
         self.ring_pos = (self.ring_pos + n) % self.capacity
         self.win_pos = (self.win_pos + n) % self.window
 
@@ -99,13 +119,18 @@ class StreamingScheduler:
         if self.pending is not None:
             raise RuntimeError("a partition is already pending")
         main = torch.cuda.current_stream(self.device)
-        self.snap.copy_(self.win)  # the next insert may overwrite the window
+        # the next insert may change the window and its histogram
+        self.snap.copy_(self.hist if self.incremental else self.win)
         ready = torch.cuda.Event()
         ready.record(main)
         nxt = 1 - self.cur
         with torch.cuda.stream(self.side):
             self.side.wait_event(ready)
-            ewsjf.partition(self.snap, self.params, table=self.tables[nxt], ws=self.ws_part, stream=self.side)
+            if self.incremental:
+                ewsjf.partition_hist(self.snap, self.params, table=self.tables[nxt], ws=self.ws_part,
+                                     stream=self.side)
+            else:
+                ewsjf.partition(self.snap, self.params, table=self.tables[nxt], ws=self.ws_part, stream=self.side)
             done = torch.cuda.Event()
             done.record(self.side)
         self.pending = done
@@ -128,7 +153,7 @@ class StreamingScheduler:
             raise ValueError("one step inserts at most min(capacity, window) arrivals")
         out = ewsjf.ring_step(self.len, self.arr, self.ring_pos, length, arrival, now, self.tables[self.cur],
                               self.theta, self.B, self.cost, window=self.win, wpos=self.win_pos, tombstone=tombstone,
-                              out=self.out, ws=self.ws_step)
+                              out=self.out, ws=self.ws_step, hist=self.hist)
         self.ring_pos = (self.ring_pos + n) % self.capacity
         self.win_pos = (self.win_pos + n) % self.window
         return out
