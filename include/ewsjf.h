@@ -19,12 +19,10 @@
  *                    score, ties to the lowest request id.
  *   ewsjf_step       route + score + select fused into one pass over the pool.
  *   ewsjf_ring_insert  new requests into a ring pool and the partition window
- *                    (the streaming scheduler's per-step update), optionally
- *                    keeping the window's length histogram current.
- *   ewsjf_window_histogram / ewsjf_partition_hist  the window's length
- *                    histogram, and Refine-and-Prune started from it (the
- *                    sliding-window partitioner that skips re-reading the
- *                    window).
+ *                    (the streaming scheduler's per-step update).
+ *   ewsjf_window_histogram / ewsjf_window_advance / ewsjf_partition_hist
+ *                    the window's length histogram, moved forward as the
+ *                    window slides, and Refine-and-Prune started from it.
  *   ewsjf_ring_step  ewsjf_ring_insert + ewsjf_step (one vector) in the same two
  *                    kernels: the streaming scheduler's per-step update and
  *                    admission.
@@ -232,60 +230,66 @@ ewsjf_status ewsjf_step_timed(int32_t* len, const float* arrival, int64_t n, flo
  * lengths into window slots (wpos + i) mod window_cap.
  * ring_len, ring_arrival: device [capacity]; window: device int32 [window_cap]
  * (may be NULL with window_cap == 0); new_len, new_arrival: device [n].
- * window_hist (optional, device uint32 [hist_max_len + 1]): the histogram of
- * the window's lengths clamped to [1, hist_max_len], as ewsjf_window_histogram
- * writes it; each overwritten window length's count moves to the new length,
- * so the histogram stays that of the window (the online, sliding-window
- * reading of the partitioner's input, Section 3.1).  NULL with
- * hist_max_len == 0 keeps none; otherwise a window is required and
- * 1 <= hist_max_len <= EWSJF_MAX_LEN.
  * 0 <= pos < capacity, 0 <= wpos < max(window_cap, 1), n <= capacity and
  * n <= window_cap when a window is given; otherwise EWSJF_ERR_ARG.  The new
- * arrays must not overlap the ring, the window or the histogram.  No
- * alignment requirement. */
+ * arrays must not overlap the ring or the window.  No alignment requirement. */
 ewsjf_status ewsjf_ring_insert(int32_t* ring_len, float* ring_arrival, int64_t capacity, int64_t pos,
-                               int32_t* window, int64_t window_cap, int64_t wpos, uint32_t* window_hist,
-                               int32_t hist_max_len, const int32_t* new_len, const float* new_arrival, int64_t n,
-                               hipStream_t stream);
+                               int32_t* window, int64_t window_cap, int64_t wpos, const int32_t* new_len,
+                               const float* new_arrival, int64_t n, hipStream_t stream);
 
 /* Histogram of a window of prompt lengths: hist[b] = number of window
  * entries whose length clamped to [1, max_len] is b (hist[0] = 0).  The
  * partitioner reads the sorted window only through its distinct values and
- * their multiplicities (Section 4.2), which this histogram holds.  window:
- * device int32 [n_window] (n_window >= 0; may be NULL when 0); hist: device
- * uint32 [max_len + 1], written in full; 1 <= max_len <= EWSJF_MAX_LEN. */
-ewsjf_status ewsjf_window_histogram(const int32_t* window, int64_t n_window, int32_t max_len, uint32_t* hist,
-                                    hipStream_t stream);
+ * their multiplicities (Section 4.2), which this histogram holds.  The window
+ * is ring[(begin + i) mod ring_cap] for i < n: a plain array is (window,
+ * n_window, 0, n_window); a window kept as the last n lengths of a ring of
+ * recent lengths (the ring calls' window argument) is a range of it.
+ * ring: device int32 [ring_cap] (may be NULL when n == 0); hist: device uint32
+ * [max_len + 1], written in full.  0 <= n <= ring_cap, 0 <= begin <
+ * max(ring_cap, 1), 1 <= max_len <= EWSJF_MAX_LEN; otherwise EWSJF_ERR_ARG. */
+ewsjf_status ewsjf_window_histogram(const int32_t* ring, int64_t ring_cap, int64_t begin, int64_t n, int32_t max_len,
+                                    uint32_t* hist, hipStream_t stream);
+
+/* The sliding window of the online strategic loop (Section 3.1: the
+ * partitioner's input is a window of recent requests) moved forward by n
+ * entries, in the histogram: the counts of the n lengths that leave the window,
+ * ring[(sub_pos + i) mod ring_cap], move to the n lengths that join it,
+ * ring[(add_pos + i) mod ring_cap], i < n (lengths clamped to [1, max_len]).
+ * Exact: the result is the histogram of the moved window whatever the order
+ * of the updates.  The caller names the entries; both ranges must still hold
+ * those lengths (a ring of at least window + n entries keeps them).  ring:
+ * device int32 [ring_cap]; hist: device uint32 [max_len + 1].  1 <= ring_cap,
+ * 0 <= add_pos, sub_pos < ring_cap, 0 <= n <= ring_cap, 1 <= max_len <=
+ * EWSJF_MAX_LEN; otherwise EWSJF_ERR_ARG.  n == 0 does nothing. */
+ewsjf_status ewsjf_window_advance(const int32_t* ring, int64_t ring_cap, int64_t add_pos, int64_t sub_pos, int64_t n,
+                                  int32_t max_len, uint32_t* hist, hipStream_t stream);
 
 /* Refine-and-Prune (Section 4.2) from a window histogram (device uint32
- * [p->max_len + 1], bin 0 ignored, as ewsjf_window_histogram writes it or the
- * ring calls keep it): the same queue table, bit for bit, as ewsjf_partition
- * over any window with that histogram; the table's n_window is the
- * histogram's total.  A histogram with no entries gives one queue covering
- * every length with count 0, sum 0, lo = hi = 0 and mean 0.  Workspace:
- * ewsjf_workspace_bytes(EWSJF_OP_PARTITION, 0, 0, 0, p) bytes.  The histogram
- * is only read; a ring call that updates it must not overlap this call. */
+ * [p->max_len + 1], bin 0 ignored, as ewsjf_window_histogram and
+ * ewsjf_window_advance write it): the same queue table, bit for bit, as
+ * ewsjf_partition over any window with that histogram; the table's n_window
+ * is the histogram's total.  A histogram with no entries gives one queue
+ * covering every length with count 0, sum 0, lo = hi = 0 and mean 0.
+ * Workspace: ewsjf_workspace_bytes(EWSJF_OP_PARTITION, 0, 0, 0, p) bytes.  The
+ * histogram is only read. */
 ewsjf_status ewsjf_partition_hist(const uint32_t* hist, const ewsjf_partition_params* p, void* table, void* ws,
                                   size_t ws_bytes, hipStream_t stream);
 
 /* The streaming scheduler's step (Section 3.2: requests keep joining the pool
  * between admissions): the effect of ewsjf_ring_insert(ring_len, ring_arrival,
- * capacity, pos, window, window_cap, wpos, window_hist, hist_max_len, new_len,
- * new_arrival, n_new) followed by ewsjf_step over the ring (n = capacity) with
- * one parameter vector, in the step's two kernels: the streaming kernel
- * substitutes the new requests for the slots it loads and stores them (and
- * their lengths into the window, moving the histogram's counts when one is
- * kept), so there is no separate insert launch.  Arguments and rules as for
- * those two calls (ring arrays 16-byte aligned; workspace
- * ewsjf_workspace_bytes(EWSJF_OP_STEP, capacity, 1, B, NULL)); the new arrays
- * must not overlap the ring, the window or the histogram.
- * EWSJF_STEP_TOMBSTONE empties the admitted slots after selection. */
+ * capacity, pos, window, window_cap, wpos, new_len, new_arrival, n_new) followed
+ * by ewsjf_step over the ring (n = capacity) with one parameter vector, in the
+ * step's two kernels: the streaming kernel substitutes the new requests for the
+ * slots it loads and stores them (and their lengths into the window), so there
+ * is no separate insert launch.  Arguments and rules as for those two calls
+ * (ring arrays 16-byte aligned; workspace ewsjf_workspace_bytes(EWSJF_OP_STEP,
+ * capacity, 1, B, NULL)); the new arrays must not overlap the ring or the
+ * window.  EWSJF_STEP_TOMBSTONE empties the admitted slots after selection. */
 ewsjf_status ewsjf_ring_step(int32_t* ring_len, float* ring_arrival, int64_t capacity, int64_t pos, int32_t* window,
-                             int64_t window_cap, int64_t wpos, uint32_t* window_hist, int32_t hist_max_len,
-                             const int32_t* new_len, const float* new_arrival, int64_t n_new, float now,
-                             const void* table, const ewsjf_theta* theta, const ewsjf_cost* cost, int32_t B,
-                             int32_t flags, int32_t* ids, float* top, int32_t* n_sel, void* ws, size_t ws_bytes,
-                             hipStream_t stream);
+                             int64_t window_cap, int64_t wpos, const int32_t* new_len, const float* new_arrival,
+                             int64_t n_new, float now, const void* table, const ewsjf_theta* theta,
+                             const ewsjf_cost* cost, int32_t B, int32_t flags, int32_t* ids, float* top,
+                             int32_t* n_sel, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* One step of the tactical loop as Algorithm 1 states it (Section 3.2),
  * over per-queue FIFOs of the pending pool:

@@ -20,8 +20,8 @@ OP_PARTITION, OP_SELECT, OP_STEP, OP_TACTICAL = 0, 1, 2, 3
 
 EXPORTED = ("ewsjf_queue_table_bytes", "ewsjf_workspace_bytes", "ewsjf_table_upload", "ewsjf_partition",
             "ewsjf_route", "ewsjf_score", "ewsjf_select", "ewsjf_step", "ewsjf_step_timed", "ewsjf_ring_insert",
-            "ewsjf_tactical_step", "ewsjf_ring_step", "ewsjf_window_histogram", "ewsjf_partition_hist",
-            "ewsjf_status_string", "ewsjf_version")
+            "ewsjf_tactical_step", "ewsjf_ring_step", "ewsjf_window_histogram", "ewsjf_window_advance",
+            "ewsjf_partition_hist", "ewsjf_status_string", "ewsjf_version")
 
 
 class PartitionParams(C.Structure):
@@ -79,16 +79,18 @@ def lib():
         L.ewsjf_step_timed.argtypes = [vp, vp, i64, f32, vp, vp, i32, C.POINTER(Cost), i32, i32, vp, vp, vp, vp, sz,
                                        vp, vp]
         L.ewsjf_step_timed.restype = C.c_int
-        L.ewsjf_ring_insert.argtypes = [vp, vp, i64, i64, vp, i64, i64, vp, i32, vp, vp, i64, vp]
+        L.ewsjf_ring_insert.argtypes = [vp, vp, i64, i64, vp, i64, i64, vp, vp, i64, vp]
         L.ewsjf_ring_insert.restype = C.c_int
         L.ewsjf_tactical_step.argtypes = [vp, vp, i64, f32, vp, vp, C.POINTER(Cost), i32, i32, vp, C.c_double, i32,
                                           vp, vp, vp, vp, vp, vp, sz, vp]
         L.ewsjf_tactical_step.restype = C.c_int
-        L.ewsjf_ring_step.argtypes = [vp, vp, i64, i64, vp, i64, i64, vp, i32, vp, vp, i64, f32, vp, vp,
-                                      C.POINTER(Cost), i32, i32, vp, vp, vp, vp, sz, vp]
+        L.ewsjf_ring_step.argtypes = [vp, vp, i64, i64, vp, i64, i64, vp, vp, i64, f32, vp, vp, C.POINTER(Cost), i32,
+                                      i32, vp, vp, vp, vp, sz, vp]
         L.ewsjf_ring_step.restype = C.c_int
-        L.ewsjf_window_histogram.argtypes = [vp, i64, i32, vp, vp]
+        L.ewsjf_window_histogram.argtypes = [vp, i64, i64, i64, i32, vp, vp]
         L.ewsjf_window_histogram.restype = C.c_int
+        L.ewsjf_window_advance.argtypes = [vp, i64, i64, i64, i64, i32, vp, vp]
+        L.ewsjf_window_advance.restype = C.c_int
         L.ewsjf_partition_hist.argtypes = [vp, C.POINTER(PartitionParams), vp, vp, sz, vp]
         L.ewsjf_partition_hist.restype = C.c_int
         L.ewsjf_status_string.argtypes = [C.c_int]

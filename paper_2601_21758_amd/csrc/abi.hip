@@ -58,21 +58,6 @@ constexpr int64_t kMaxN = 0x7fffffffLL;  // request ids are int32
 
 ewsjf_status launched(hipError_t e) { return e == hipSuccess ? EWSJF_OK : EWSJF_ERR_LAUNCH; }
 
-// The window arguments of the ring calls: NULL/range checks for n inserted
-// lengths, or the status to return.
-ewsjf_status window_args(int32_t* window, int64_t window_cap, int64_t wpos, uint32_t* window_hist,
-                         int32_t hist_max_len, int64_t n, ewsjf::WindowRing* out) {
-  if (window_cap > 0 && window == nullptr) return EWSJF_ERR_NULL;
-  if (window_cap < 0 || window_cap > kMaxN || wpos < 0 || (window_cap > 0 && (wpos >= window_cap || n > window_cap)) ||
-      (window_cap == 0 && wpos != 0))
-    return EWSJF_ERR_ARG;
-  if (window_hist != nullptr ? (window_cap == 0 || hist_max_len < 1 || hist_max_len > EWSJF_MAX_LEN)
-                             : hist_max_len != 0)
-    return EWSJF_ERR_ARG;
-  *out = ewsjf::WindowRing{window, window_cap, wpos, window_hist, hist_max_len};
-  return EWSJF_OK;
-}
-
 }  // namespace
 
 extern "C" {
@@ -147,29 +132,43 @@ ewsjf_status ewsjf_partition(const int32_t* window, int64_t n_window, const ewsj
 }
 
 ewsjf_status ewsjf_ring_insert(int32_t* ring_len, float* ring_arrival, int64_t capacity, int64_t pos,
-                               int32_t* window, int64_t window_cap, int64_t wpos, uint32_t* window_hist,
-                               int32_t hist_max_len, const int32_t* new_len, const float* new_arrival, int64_t n,
-                               hipStream_t stream) {
+                               int32_t* window, int64_t window_cap, int64_t wpos, const int32_t* new_len,
+                               const float* new_arrival, int64_t n, hipStream_t stream) {
   if (n > 0 && (ring_len == nullptr || ring_arrival == nullptr || new_len == nullptr || new_arrival == nullptr))
     return EWSJF_ERR_NULL;
-  ewsjf::WindowRing win;
-  const ewsjf_status ws = window_args(window, window_cap, wpos, window_hist, hist_max_len, n, &win);
-  if (ws != EWSJF_OK) return ws;
+  if (window_cap > 0 && window == nullptr) return EWSJF_ERR_NULL;
   if (capacity < 1 || capacity > kMaxN || pos < 0 || pos >= capacity || n < 0 || n > capacity) return EWSJF_ERR_ARG;
+  if (window_cap < 0 || window_cap > kMaxN || wpos < 0 || (window_cap > 0 && (wpos >= window_cap || n > window_cap)) ||
+      (window_cap == 0 && wpos != 0))
+    return EWSJF_ERR_ARG;
   if (n == 0) return EWSJF_OK;
   const ewsjf_status ds = check_device();
   if (ds != EWSJF_OK) return ds;
-  return launched(ewsjf::launch_ring_insert(ring_len, ring_arrival, capacity, pos, win, new_len, new_arrival, n,
-                                            stream));
+  return launched(ewsjf::launch_ring_insert(ring_len, ring_arrival, capacity, pos, window, window_cap, wpos, new_len,
+                                            new_arrival, n, stream));
 }
 
-ewsjf_status ewsjf_window_histogram(const int32_t* window, int64_t n_window, int32_t max_len, uint32_t* hist,
-                                    hipStream_t stream) {
-  if (hist == nullptr || (n_window > 0 && window == nullptr)) return EWSJF_ERR_NULL;
-  if (n_window < 0 || n_window > kMaxN || max_len < 1 || max_len > EWSJF_MAX_LEN) return EWSJF_ERR_ARG;
+ewsjf_status ewsjf_window_histogram(const int32_t* ring, int64_t ring_cap, int64_t begin, int64_t n, int32_t max_len,
+                                    uint32_t* hist, hipStream_t stream) {
+  if (hist == nullptr || (n > 0 && ring == nullptr)) return EWSJF_ERR_NULL;
+  if (ring_cap < 0 || ring_cap > kMaxN || n < 0 || n > ring_cap || begin < 0 ||
+      begin >= (ring_cap > 0 ? ring_cap : 1) || max_len < 1 || max_len > EWSJF_MAX_LEN)
+    return EWSJF_ERR_ARG;
   const ewsjf_status ds = check_device();
   if (ds != EWSJF_OK) return ds;
-  return launched(ewsjf::launch_window_histogram(window, n_window, max_len, hist, stream));
+  return launched(ewsjf::launch_window_histogram(ring, ring_cap, begin, n, max_len, hist, stream));
+}
+
+ewsjf_status ewsjf_window_advance(const int32_t* ring, int64_t ring_cap, int64_t add_pos, int64_t sub_pos, int64_t n,
+                                  int32_t max_len, uint32_t* hist, hipStream_t stream) {
+  if (n > 0 && (ring == nullptr || hist == nullptr)) return EWSJF_ERR_NULL;
+  if (ring_cap < 1 || ring_cap > kMaxN || n < 0 || n > ring_cap || add_pos < 0 || add_pos >= ring_cap ||
+      sub_pos < 0 || sub_pos >= ring_cap || max_len < 1 || max_len > EWSJF_MAX_LEN)
+    return EWSJF_ERR_ARG;
+  if (n == 0) return EWSJF_OK;
+  const ewsjf_status ds = check_device();
+  if (ds != EWSJF_OK) return ds;
+  return launched(ewsjf::launch_window_advance(ring, ring_cap, add_pos, sub_pos, n, max_len, hist, stream));
 }
 
 ewsjf_status ewsjf_partition_hist(const uint32_t* hist, const ewsjf_partition_params* p, void* table, void* ws,
@@ -273,18 +272,19 @@ ewsjf_status ewsjf_tactical_step(int32_t* len, const float* arrival, int64_t n, 
 }
 
 ewsjf_status ewsjf_ring_step(int32_t* ring_len, float* ring_arrival, int64_t capacity, int64_t pos, int32_t* window,
-                             int64_t window_cap, int64_t wpos, uint32_t* window_hist, int32_t hist_max_len,
-                             const int32_t* new_len, const float* new_arrival, int64_t n_new, float now, const void* table, const ewsjf_theta* theta,
+                             int64_t window_cap, int64_t wpos, const int32_t* new_len, const float* new_arrival,
+                             int64_t n_new, float now, const void* table, const ewsjf_theta* theta,
                              const ewsjf_cost* cost, int32_t B, int32_t flags, int32_t* ids, float* top,
                              int32_t* n_sel, void* ws, size_t ws_bytes, hipStream_t stream) {
   if (ring_len == nullptr || ring_arrival == nullptr || table == nullptr || theta == nullptr || cost == nullptr ||
       ids == nullptr || top == nullptr || n_sel == nullptr || ws == nullptr)
     return EWSJF_ERR_NULL;
   if (n_new > 0 && (new_len == nullptr || new_arrival == nullptr)) return EWSJF_ERR_NULL;
-  ewsjf::WindowRing win;
-  const ewsjf_status wst = window_args(window, window_cap, wpos, window_hist, hist_max_len, n_new, &win);
-  if (wst != EWSJF_OK) return wst;
+  if (window_cap > 0 && window == nullptr) return EWSJF_ERR_NULL;
   if (capacity < 1 || capacity > kMaxN || pos < 0 || pos >= capacity || n_new < 0 || n_new > capacity)
+    return EWSJF_ERR_ARG;
+  if (window_cap < 0 || window_cap > kMaxN || wpos < 0 || (window_cap > 0 && (wpos >= window_cap || n_new > window_cap)) ||
+      (window_cap == 0 && wpos != 0))
     return EWSJF_ERR_ARG;
   if (B < 1 || B > EWSJF_MAX_B || !cost_ok(cost) || !std::isfinite(now)) return EWSJF_ERR_ARG;
   if ((flags & ~EWSJF_STEP_TOMBSTONE) != 0) return EWSJF_ERR_ARG;
@@ -292,10 +292,10 @@ ewsjf_status ewsjf_ring_step(int32_t* ring_len, float* ring_arrival, int64_t cap
   if (!aligned16(ring_len) || !aligned16(ring_arrival) || !aligned16(ws)) return EWSJF_ERR_ALIGN;
   const ewsjf_status ds = check_device();
   if (ds != EWSJF_OK) return ds;
-  return launched(ewsjf::launch_ring_step(ring_len, ring_arrival, capacity, pos, win, new_len, new_arrival, n_new, now,
-                                          static_cast<const ewsjf_queue_table*>(table), theta, *cost, B,
-                                          (flags & EWSJF_STEP_TOMBSTONE) ? ring_len : nullptr, ids, top, n_sel, ws,
-                                          stream));
+  return launched(ewsjf::launch_ring_step(ring_len, ring_arrival, capacity, pos, window, window_cap, wpos, new_len,
+                                          new_arrival, n_new, now, static_cast<const ewsjf_queue_table*>(table),
+                                          theta, *cost, B, (flags & EWSJF_STEP_TOMBSTONE) ? ring_len : nullptr, ids,
+                                          top, n_sel, ws, stream));
 }
 
 }  // extern "C"

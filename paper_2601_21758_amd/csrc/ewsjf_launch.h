@@ -55,36 +55,9 @@ hipError_t launch_fifo_select(const int32_t* len, const float* arrival, int64_t 
                               const TacticalPlan* plan, int32_t B, int32_t* ids, float* top, int32_t* n_sel, void* ws,
                               hipStream_t stream);
 
-// The partition window as a ring of lengths (cap == 0: none) and, when hist
-// is set, the histogram of its lengths clamped to [1, max_len] that the
-// inserts keep current.
-struct WindowRing {
-  int32_t* len;
-  int64_t cap, pos;
-  uint32_t* hist;
-  int32_t max_len;
-};
-
-// A window length as the partition counts it: clamped to [1, L].
-__host__ __device__ __forceinline__ int clamp_len(int32_t b, int L) { return b < 1 ? 1 : (b > L ? L : b); }
-
-// Window slot w (< cap) takes length b; the histogram, when kept, moves one
-// count from the overwritten length to b.  Each slot is written by one lane
-// of one launch, so the read of the old length cannot race.
-__device__ __forceinline__ void window_put(const WindowRing& win, int64_t w, int32_t b) {
-  if (win.hist != nullptr) {
-    const int o = clamp_len(win.len[w], win.max_len), c = clamp_len(b, win.max_len);
-    if (o != c) {
-      atomicSub(&win.hist[o], 1u);
-      atomicAdd(&win.hist[c], 1u);
-    }
-  }
-  win.len[w] = b;
-}
-
 // ring insert + one-vector step in the same two kernels (ewsjf_ring_step)
-hipError_t launch_ring_step(int32_t* ring_len, float* ring_arrival, int64_t capacity, int64_t pos,
-                            const WindowRing& win, const int32_t* new_len, const float* new_arrival,
+hipError_t launch_ring_step(int32_t* ring_len, float* ring_arrival, int64_t capacity, int64_t pos, int32_t* window,
+                            int64_t window_cap, int64_t wpos, const int32_t* new_len, const float* new_arrival,
                             int64_t n_new, float now, const ewsjf_queue_table* table, const ewsjf_theta* theta,
                             const ewsjf_cost& cost, int32_t B, int32_t* tomb_len, int32_t* ids, float* top,
                             int32_t* n_sel, void* ws, hipStream_t stream);
@@ -114,9 +87,9 @@ hipError_t launch_score(const int32_t* len, const float* arrival, int64_t n, flo
 
 // Builds the routing lut of a device table whose header and bounds are set.
 hipError_t launch_build_lut(ewsjf_queue_table* table, hipStream_t stream);
-hipError_t launch_ring_insert(int32_t* ring_len, float* ring_arrival, int64_t capacity, int64_t pos,
-                              const WindowRing& win, const int32_t* new_len, const float* new_arrival, int64_t n,
-                              hipStream_t stream);
+hipError_t launch_ring_insert(int32_t* ring_len, float* ring_arrival, int64_t capacity, int64_t pos, int32_t* window,
+                              int64_t window_cap, int64_t wpos, const int32_t* new_len, const float* new_arrival,
+                              int64_t n, hipStream_t stream);
 
 // Refine-and-Prune.
 size_t partition_ws_bytes(int64_t n_window, const ewsjf_partition_params& p);
@@ -126,8 +99,13 @@ hipError_t launch_partition(const int32_t* window, int64_t n_window, const ewsjf
 // partition_ws_bytes(0, p)
 hipError_t launch_partition_hist(const uint32_t* hist, const ewsjf_partition_params& p, ewsjf_queue_table* table,
                                  void* ws, hipStream_t stream);
-// hist[0..L] := histogram of window[0..n) clamped to [1, L]
-hipError_t launch_window_histogram(const int32_t* window, int64_t n_window, int L, uint32_t* hist,
+// hist[0..L] := histogram of ring[(begin + i) mod cap], i < n, clamped to [1, L]
+// (n <= cap, begin < cap)
+hipError_t launch_window_histogram(const int32_t* ring, int64_t cap, int64_t begin, int64_t n, int L, uint32_t* hist,
                                    hipStream_t stream);
+// hist += counts of ring[(add + i) mod cap], hist -= counts of ring[(sub + i) mod cap],
+// i < n (add, sub < cap; n <= cap)
+hipError_t launch_window_advance(const int32_t* ring, int64_t cap, int64_t add, int64_t sub, int64_t n, int L,
+                                 uint32_t* hist, hipStream_t stream);
 
 }  // namespace ewsjf

@@ -8,11 +8,12 @@
 //   window_hist      LDS-privatized histogram of clamped window lengths, one
 //                    partial histogram per workgroup (no global atomics).
 //   hist_reduce      column sums of the partial histograms.
-//   hist_clear /     the same histogram into a caller-owned array, flushed
-//   window_hist_add  with one global atomic per non-empty bin per workgroup
-//                    (the starting point of a histogram that the streaming
-//                    inserts then keep current; the partition can start from
-//                    it instead of from the window).
+//   hist_clear /     the same histogram into a caller-owned array (of a
+//   window_hist_add  window kept as a range of a ring of recent lengths),
+//                    flushed with one global atomic per non-empty bin per
+//                    workgroup; the partition can start from it.
+//   window_hist_move the window moved forward by n entries: the counts of
+//                    the lengths that leave it go to the ones that join it.
 //   rp_distinct      one workgroup: distinct values v[], counts c[] and exact
 //                    int64 prefix sums of counts and of count * value.
 //   rp_kmeans3 /     the exact 1-D 3-means initializer: every split (i, j) of
@@ -117,21 +118,34 @@ size_t carve_size(int64_t n, int L) {
 }
 
 // ---------------------------------------------------------------------------
-// This workgroup's share of the window counted into h[0..L] (LDS).
-__device__ void lds_window_hist(const int32_t* __restrict__ win, int64_t n, int L, uint32_t* h) {
+// A window length as the partition counts it: clamped to [1, L].
+__device__ __forceinline__ int clamp_len(int32_t b, int L) { return b < 1 ? 1 : (b > L ? L : b); }
+
+// The entry i < n of a window kept as ring[(begin + i) mod cap] (begin < cap,
+// n <= cap, so one subtraction wraps it).
+__device__ __forceinline__ int32_t ring_at(const int32_t* __restrict__ ring, int64_t cap, int64_t begin, int64_t i) {
+  int64_t j = begin + i;
+  if (j >= cap) j -= cap;
+  return ring[j];
+}
+
+// This workgroup's share of the n window entries counted into h[0..L] (LDS).
+__device__ void lds_window_hist(const int32_t* __restrict__ ring, int64_t cap, int64_t begin, int64_t n, int L,
+                                uint32_t* h) {
   for (int b = threadIdx.x; b <= L; b += kBlock) h[b] = 0u;
   __syncthreads();
   const int64_t per = (n + gridDim.x - 1) / gridDim.x;
   const int64_t beg = per * blockIdx.x;
   const int64_t end = beg + per < n ? beg + per : n;
-  for (int64_t i = beg + threadIdx.x; i < end; i += kBlock) atomicAdd(&h[clamp_len(win[i], L)], 1u);
+  for (int64_t i = beg + threadIdx.x; i < end; i += kBlock)
+    atomicAdd(&h[clamp_len(ring_at(ring, cap, begin, i), L)], 1u);
   __syncthreads();
 }
 
 __global__ __launch_bounds__(kBlock) void window_hist(const int32_t* __restrict__ win, int64_t n, int L,
                                                       uint32_t* __restrict__ partial) {
   __shared__ uint32_t h[EWSJF_MAX_LEN + 1];
-  lds_window_hist(win, n, L, h);
+  lds_window_hist(win, n, 0, n, L, h);
   uint32_t* out = partial + (size_t)blockIdx.x * (L + 1);
   for (int b = threadIdx.x; b <= L; b += kBlock) out[b] = h[b];
 }
@@ -141,10 +155,11 @@ __global__ void hist_clear(uint32_t* __restrict__ hist, int L) {
   if (b <= L) hist[b] = 0u;
 }
 
-__global__ __launch_bounds__(kBlock) void window_hist_add(const int32_t* __restrict__ win, int64_t n, int L,
+__global__ __launch_bounds__(kBlock) void window_hist_add(const int32_t* __restrict__ ring, int64_t cap,
+                                                          int64_t begin, int64_t n, int L,
                                                           uint32_t* __restrict__ hist) {
   __shared__ uint32_t h[EWSJF_MAX_LEN + 1];
-  lds_window_hist(win, n, L, h);
+  lds_window_hist(ring, cap, begin, n, L, h);
   for (int b = threadIdx.x; b <= L; b += kBlock)
     if (h[b]) atomicAdd(&hist[b], h[b]);
 }
@@ -155,6 +170,32 @@ __global__ void hist_reduce(const uint32_t* __restrict__ partial, int Gh, int L,
   uint32_t s = 0;
   for (int g = 0; g < Gh; ++g) s += partial[(size_t)g * (L + 1) + b];
   hist[b] = s;
+}
+
+// The window moves forward by n entries: the counts of the n lengths that
+// leave it (ring[(sub + i) mod cap]) move to the n that join it
+// (ring[(add + i) mod cap]).  Per-workgroup signed deltas in LDS, flushed as
+// modular uint32 adds: the final counts are exact in any flush order.
+__global__ __launch_bounds__(kBlock) void window_hist_move(const int32_t* __restrict__ ring, int64_t cap, int64_t add,
+                                                           int64_t sub, int64_t n, int L,
+                                                           uint32_t* __restrict__ hist) {
+  __shared__ int32_t d[EWSJF_MAX_LEN + 1];
+  for (int b = threadIdx.x; b <= L; b += kBlock) d[b] = 0;
+  __syncthreads();
+  const int64_t per = (n + gridDim.x - 1) / gridDim.x;
+  const int64_t beg = per * blockIdx.x;
+  const int64_t end = beg + per < n ? beg + per : n;
+  for (int64_t i = beg + threadIdx.x; i < end; i += kBlock) {
+    const int ca = clamp_len(ring_at(ring, cap, add, i), L);
+    const int cs = clamp_len(ring_at(ring, cap, sub, i), L);
+    if (ca != cs) {
+      atomicAdd(&d[ca], 1);
+      atomicSub(&d[cs], 1);
+    }
+  }
+  __syncthreads();
+  for (int b = threadIdx.x; b <= L; b += kBlock)
+    if (d[b]) atomicAdd(&hist[b], (uint32_t)d[b]);
 }
 
 // Exclusive int64 block scan (kBlock threads).
@@ -432,7 +473,6 @@ __global__ __launch_bounds__(kBlock) void rp_refine_prune(PartWs w, ewsjf_partit
   const int tid = threadIdx.x;
   const int V = w.meta[0];
   const int L = p.max_len;
-  const double inf = __builtin_inf();
   if (V == 0) {
     // An empty histogram (only a caller-kept one can be empty): one queue
     // that holds nothing and covers every length.
@@ -790,12 +830,18 @@ hipError_t launch_partition_hist(const uint32_t* hist, const ewsjf_partition_par
   return launch_stages(w, p, -1, table, stream);
 }
 
-hipError_t launch_window_histogram(const int32_t* window, int64_t n_window, int L, uint32_t* hist,
+hipError_t launch_window_histogram(const int32_t* ring, int64_t cap, int64_t begin, int64_t n, int L, uint32_t* hist,
                                    hipStream_t stream) {
   hipLaunchKernelGGL(hist_clear, dim3((L + 1 + 255) / 256), dim3(256), 0, stream, hist, L);
-  if (n_window > 0)
-    hipLaunchKernelGGL(window_hist_add, dim3(hist_blocks(n_window)), dim3(kBlock), 0, stream, window, n_window, L,
-                       hist);
+  if (n > 0)
+    hipLaunchKernelGGL(window_hist_add, dim3(hist_blocks(n)), dim3(kBlock), 0, stream, ring, cap, begin, n, L, hist);
+  return hipGetLastError();
+}
+
+hipError_t launch_window_advance(const int32_t* ring, int64_t cap, int64_t add, int64_t sub, int64_t n, int L,
+                                 uint32_t* hist, hipStream_t stream) {
+  hipLaunchKernelGGL(window_hist_move, dim3(hist_blocks(n)), dim3(kBlock), 0, stream, ring, cap, add, sub, n, L,
+                     hist);
   return hipGetLastError();
 }
 

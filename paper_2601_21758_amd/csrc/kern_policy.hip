@@ -60,12 +60,12 @@ __global__ __launch_bounds__(kBlock) void route_kernel(const int32_t* __restrict
 
 // ---------------------------------------------------------------------------
 // Streaming pool update: new requests into consecutive ring slots and their
-// lengths into the window ring (with the window's histogram moved from each
-// overwritten length to the new one).
+// lengths into the window ring.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void ring_insert_kernel(int32_t* __restrict__ ring_len,
                                                           float* __restrict__ ring_arrival, int64_t capacity,
-                                                          int64_t pos, WindowRing win,
+                                                          int64_t pos, int32_t* __restrict__ window,
+                                                          int64_t window_cap, int64_t wpos,
                                                           const int32_t* __restrict__ new_len,
                                                           const float* __restrict__ new_arrival, int64_t n) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -75,19 +75,19 @@ __global__ __launch_bounds__(256) void ring_insert_kernel(int32_t* __restrict__ 
   if (slot >= capacity) slot -= capacity;  // n <= capacity and pos < capacity
   ring_len[slot] = b;
   ring_arrival[slot] = new_arrival[i];
-  if (win.cap > 0) {
-    int64_t w = win.pos + i;
-    if (w >= win.cap) w -= win.cap;  // n <= win.cap and win.pos < win.cap
-    window_put(win, w, b);
+  if (window_cap > 0) {
+    int64_t w = wpos + i;
+    if (w >= window_cap) w -= window_cap;  // n <= window_cap and wpos < window_cap
+    window[w] = b;
   }
 }
 
-hipError_t launch_ring_insert(int32_t* ring_len, float* ring_arrival, int64_t capacity, int64_t pos,
-                              const WindowRing& win, const int32_t* new_len, const float* new_arrival, int64_t n,
-                              hipStream_t stream) {
+hipError_t launch_ring_insert(int32_t* ring_len, float* ring_arrival, int64_t capacity, int64_t pos, int32_t* window,
+                              int64_t window_cap, int64_t wpos, const int32_t* new_len, const float* new_arrival,
+                              int64_t n, hipStream_t stream) {
   const int64_t blocks = (n + 255) / 256;
   hipLaunchKernelGGL(ring_insert_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, ring_len, ring_arrival,
-                     capacity, pos, win, new_len, new_arrival, n);
+                     capacity, pos, window, window_cap, wpos, new_len, new_arrival, n);
   return hipGetLastError();
 }
 

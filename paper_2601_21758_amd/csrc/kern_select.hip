@@ -233,13 +233,14 @@ struct FifoSource {
 // the slots (pos + i) mod capacity, i < n_new, take new request i.  The
 // streaming kernel substitutes the new requests for the loaded slots of the
 // chunks that hold them and writes them to the ring (and their lengths to
-// the partition window, keeping its histogram current when one is kept), so
-// the step sees the pool after the insert and later steps find it stored.
+// the partition window), so the step sees the pool after the insert and
+// later steps find it stored.
 struct RingSource : PoolSource {
   int32_t* ring_len;
   float* ring_arrival;
   int64_t capacity, pos;
-  WindowRing win;
+  int32_t* window;
+  int64_t window_cap, wpos;
   const int32_t* new_len;
   const float* new_arrival;
   int64_t n_new;
@@ -265,10 +266,10 @@ struct RingSource : PoolSource {
             r.a[e] = a;
             ring_len[slot] = b;
             ring_arrival[slot] = a;
-            if (win.cap > 0) {
-              int64_t w = win.pos + d;
-              if (w >= win.cap) w -= win.cap;
-              window_put(win, w, b);
+            if (window_cap > 0) {
+              int64_t w = wpos + d;
+              if (w >= window_cap) w -= window_cap;
+              window[w] = b;
             }
           }
         }
@@ -1373,8 +1374,8 @@ hipError_t launch_step(const int32_t* len, const float* arrival, int64_t n, floa
   return hipGetLastError();
 }
 
-hipError_t launch_ring_step(int32_t* ring_len, float* ring_arrival, int64_t capacity, int64_t pos,
-                            const WindowRing& win, const int32_t* new_len, const float* new_arrival,
+hipError_t launch_ring_step(int32_t* ring_len, float* ring_arrival, int64_t capacity, int64_t pos, int32_t* window,
+                            int64_t window_cap, int64_t wpos, const int32_t* new_len, const float* new_arrival,
                             int64_t n_new, float now, const ewsjf_queue_table* table, const ewsjf_theta* theta,
                             const ewsjf_cost& cost, int32_t B, int32_t* tomb_len, int32_t* ids, float* top,
                             int32_t* n_sel, void* ws, hipStream_t stream) {
@@ -1391,7 +1392,9 @@ hipError_t launch_ring_step(int32_t* ring_len, float* ring_arrival, int64_t capa
   src.ring_arrival = ring_arrival;
   src.capacity = capacity;
   src.pos = pos;
-  src.win = win;
+  src.window = window;
+  src.window_cap = window_cap;
+  src.wpos = wpos;
   src.new_len = new_len;
   src.new_arrival = new_arrival;
   src.n_new = n_new;

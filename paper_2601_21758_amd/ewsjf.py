@@ -87,19 +87,31 @@ def partition(window: torch.Tensor, p: L.PartitionParams, table: torch.Tensor | 
     return table
 
 
-def window_histogram(window: torch.Tensor, max_len: int, hist: torch.Tensor | None = None,
-                     stream=None) -> torch.Tensor:
-    """Histogram of the window's lengths clamped to [1, max_len]: int32
+def window_histogram(ring: torch.Tensor, max_len: int, hist: torch.Tensor | None = None, begin: int = 0,
+                     n: int | None = None, stream=None) -> torch.Tensor:
+    """Histogram of the window ring[(begin + i) mod len(ring)], i < n (the
+    whole array by default), lengths clamped to [1, max_len]: int32
     [max_len + 1] (the library's uint32 counts, bit for bit), hist[0] = 0."""
-    _need(window, torch.int32, "window")
+    _need(ring, torch.int32, "ring")
+    n = ring.numel() if n is None else int(n)
     if hist is None:
-        hist = torch.empty(int(max_len) + 1, dtype=torch.int32, device=window.device)
+        hist = torch.empty(int(max_len) + 1, dtype=torch.int32, device=ring.device)
     _need(hist, torch.int32, "hist")
     if hist.numel() != int(max_len) + 1:
         raise ValueError("hist needs max_len + 1 entries")
-    L.check(L.lib().ewsjf_window_histogram(_vp(window), window.numel(), int(max_len), _vp(hist), _stream(stream)),
-            "ewsjf_window_histogram")
+    L.check(L.lib().ewsjf_window_histogram(_vp(ring), ring.numel(), int(begin), n, int(max_len), _vp(hist),
+                                           _stream(stream)), "ewsjf_window_histogram")
     return hist
+
+
+def window_advance(ring: torch.Tensor, add_pos: int, sub_pos: int, n: int, hist: torch.Tensor, stream=None) -> None:
+    """Move the window's histogram (int32 [max_len + 1]) forward by n entries:
+    the counts of ring[(sub_pos + i) mod len(ring)] go to ring[(add_pos + i)
+    mod len(ring)], i < n."""
+    _need(ring, torch.int32, "ring")
+    _need(hist, torch.int32, "hist")
+    L.check(L.lib().ewsjf_window_advance(_vp(ring), ring.numel(), int(add_pos), int(sub_pos), int(n),
+                                         hist.numel() - 1, _vp(hist), _stream(stream)), "ewsjf_window_advance")
 
 
 def partition_hist(hist: torch.Tensor, p: L.PartitionParams, table: torch.Tensor | None = None,
@@ -115,21 +127,6 @@ def partition_hist(hist: torch.Tensor, p: L.PartitionParams, table: torch.Tensor
     L.check(L.lib().ewsjf_partition_hist(_vp(hist), C.byref(p), _vp(table), _vp(buf), buf.numel(), _stream(stream)),
             "ewsjf_partition_hist")
     return table
-
-
-def _window_args(window, hist):
-    """(window ptr, window_cap, hist ptr, hist_max_len) for the ring calls."""
-    if window is not None:
-        _need(window, torch.int32, "window")
-    if hist is not None:
-        if window is None:
-            raise ValueError("a window histogram needs the window")
-        _need(hist, torch.int32, "hist")
-        if hist.numel() < 2:
-            raise ValueError("hist needs max_len + 1 >= 2 entries")
-    wp, wc = (_vp(window), window.numel()) if window is not None else (None, 0)
-    hp, hm = (_vp(hist), hist.numel() - 1) if hist is not None else (None, 0)
-    return wp, wc, hp, hm
 
 
 def upload_table(bounds, mean, max_len: int = L.MAX_LEN, lo=None, hi=None, count=None, sum=None,
@@ -243,14 +240,14 @@ def step(length: torch.Tensor, arrival: torch.Tensor, now: float, table: torch.T
 def ring_step(ring_len: torch.Tensor, ring_arrival: torch.Tensor, pos: int, new_len: torch.Tensor,
               new_arrival: torch.Tensor, now: float, table: torch.Tensor, theta: torch.Tensor, B: int,
               cost_=DEFAULT_COST, window: torch.Tensor | None = None, wpos: int = 0, tombstone: bool = False, out=None,
-              ws: Workspace | None = None, stream=None, hist: torch.Tensor | None = None):
-    """ring_insert + step (one vector) fused (ewsjf_ring_step); `hist`, the
-    window's histogram, is kept current as the window is overwritten."""
+              ws: Workspace | None = None, stream=None):
+    """ring_insert + step (one vector) fused (ewsjf_ring_step)."""
     _need(ring_len, torch.int32, "ring_len")
     _need(ring_arrival, torch.float32, "ring_arrival")
     _need(new_len, torch.int32, "new_len")
     _need(new_arrival, torch.float32, "new_arrival")
-    wp, wc, hp, hm = _window_args(window, hist)
+    if window is not None:
+        _need(window, torch.int32, "window")
     theta = _theta(theta)
     if theta.shape[0] != 1:
         raise ValueError("ring_step takes one parameter vector")
@@ -259,8 +256,9 @@ def ring_step(ring_len: torch.Tensor, ring_arrival: torch.Tensor, pos: int, new_
     ws = ws or Workspace(ring_len.device)
     buf = ws.get(workspace_bytes(L.OP_STEP, cap, 1, B))
     c = _cost(cost_)
+    wp, wc = (_vp(window), window.numel()) if window is not None else (None, 0)
     flags = L.STEP_TOMBSTONE if tombstone else 0
-    L.check(L.lib().ewsjf_ring_step(_vp(ring_len), _vp(ring_arrival), cap, int(pos), wp, wc, int(wpos), hp, hm,
+    L.check(L.lib().ewsjf_ring_step(_vp(ring_len), _vp(ring_arrival), cap, int(pos), wp, wc, int(wpos),
                                     _vp(new_len), _vp(new_arrival), new_len.numel(), float(now), _vp(table),
                                     _vp(theta), C.byref(c), int(B), flags, _vp(ids), _vp(top), _vp(nsel), _vp(buf),
                                     buf.numel(), _stream(stream)),
@@ -304,16 +302,17 @@ def tactical_step(length: torch.Tensor, arrival: torch.Tensor, now: float, table
 
 
 def ring_insert(ring_len: torch.Tensor, ring_arrival: torch.Tensor, pos: int, new_len: torch.Tensor,
-                new_arrival: torch.Tensor, window: torch.Tensor | None = None, wpos: int = 0, stream=None,
-                hist: torch.Tensor | None = None) -> None:
+                new_arrival: torch.Tensor, window: torch.Tensor | None = None, wpos: int = 0, stream=None) -> None:
     """Write new requests into ring slots (pos + i) mod capacity and their
-    lengths into window slots (wpos + i) mod len(window), in one launch;
-    `hist`, the window's histogram, is kept current."""
+    lengths into window slots (wpos + i) mod len(window), in one launch."""
     _need(ring_len, torch.int32, "ring_len")
     _need(ring_arrival, torch.float32, "ring_arrival")
     _need(new_len, torch.int32, "new_len")
     _need(new_arrival, torch.float32, "new_arrival")
-    wv, wc, hp, hm = _window_args(window, hist)
+    if window is not None:
+        _need(window, torch.int32, "window")
+    wv = _vp(window) if window is not None else C.c_void_p(None)
+    wc = window.numel() if window is not None else 0
     L.check(L.lib().ewsjf_ring_insert(_vp(ring_len), _vp(ring_arrival), ring_len.numel(), int(pos), wv, wc,
-                                      int(wpos), hp, hm, _vp(new_len), _vp(new_arrival), new_len.numel(), _stream(stream)),
+                                      int(wpos), _vp(new_len), _vp(new_arrival), new_len.numel(), _stream(stream)),
             "ewsjf_ring_insert")

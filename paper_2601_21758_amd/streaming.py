@@ -1,26 +1,31 @@
-"""Streaming scheduler state on one GPU: a ring of request slots, a sliding
-window of recent arrival lengths, and double-buffered queue tables.
+"""Streaming scheduler state on one GPU: a ring of request slots, a log of
+recent arrival lengths holding the partitioner's sliding window, and
+double-buffered queue tables.
 
 Each step inserts the step's arrivals into the ring (request id = ring slot;
 an overwritten, still-pending request is evicted) and runs the fused step
 (route + score + top-B admission), tombstoning the admitted slots; with
 step(now, length=..., arrival=...) the insert happens inside the step's own
-kernels (ewsjf_ring_step).  After step s, launch_repartition() starts
-Refine-and-Prune over the window (which holds step s's arrivals) on a side
-stream; the new table takes effect at step s + 1.  The paper runs the
-partitioner off the critical path, in the strategic loop (Section 3.1;
-Section 5), over a window of recent requests (Section 4.2).
+kernels (ewsjf_ring_step).  The step also stores the arrivals' lengths into
+the log (a ring of `log_capacity` >= `window` entries); the window is always
+its last `window` entries.
 
-With incremental=True (the default) the inserts also keep the window's
-length histogram current (each overwritten length's count moves to the new
-length), and the repartition starts from a copy of that histogram
-(ewsjf_partition_hist) instead of re-reading the window: the same table, bit
-for bit, since Refine-and-Prune sees the window only through its distinct
-lengths and their multiplicities.
+The paper runs the partitioner off the critical path, in the strategic loop
+(Section 3.1; Section 5), over a window of recent requests (Section 4.2).
+launch_repartition() after step s does its work on a side stream: it brings
+the window's length histogram up to date (ewsjf_window_advance moves the
+counts of the lengths that left the window to the ones that joined it, when
+the log still holds both; otherwise ewsjf_window_histogram recounts the
+window from the log) and runs Refine-and-Prune from the histogram
+(ewsjf_partition_hist: the same table, bit for bit, as partitioning the
+window, since Refine-and-Prune sees it only through its distinct lengths and
+their multiplicities).  The new table takes effect at step s + 1.  A step
+whose log writes would overwrite entries a queued side-stream read still
+needs waits for that read first.
 
 Every step runs in libewsjf.so's kernels: ewsjf_ring_step (or
-ewsjf_ring_insert and ewsjf_step), and ewsjf_partition_hist (or
-ewsjf_partition).
+ewsjf_ring_insert and ewsjf_step) on the caller's stream; ewsjf_window_advance
+or ewsjf_window_histogram, then ewsjf_partition_hist, on the side stream.
 """
 from __future__ import annotations
 
@@ -42,28 +47,29 @@ class StreamingScheduler:
 
     capacity: ring slots (request ids); window: partitioner window length;
     B: admissions per step; params: ewsjf.params(...); theta: one parameter
-    vector (6 floats); cost: (c0, c1, c2); incremental: keep the window's
-    histogram and partition from it.
+    vector (6 floats); cost: (c0, c1, c2); incremental: move the window's
+    histogram forward when the log allows it (False: recount the window at
+    every repartition); log_capacity: length-log entries (default 2 *
+    window).
     """
 
     def __init__(self, capacity: int, window: int, B: int, params: L.PartitionParams, theta, cost=ewsjf.DEFAULT_COST,
-                 device="cuda", incremental: bool = True):
+                 device="cuda", incremental: bool = True, log_capacity: int | None = None):
         if capacity <= 0 or window <= 0 or window > capacity:
             raise ValueError("need 0 < window <= capacity")
+        log_capacity = 2 * int(window) if log_capacity is None else int(log_capacity)
+        if log_capacity < window:
+            raise ValueError("the length log must hold the window")
         self.device = torch.device(device)
         self.capacity, self.window, self.B = int(capacity), int(window), int(B)
+        self.log_cap = log_capacity
         self.params, self.cost = params, cost
+        self.incremental = bool(incremental)
         self.theta = _dev(np.asarray(theta, np.float32).reshape(1, 6), torch.float32, self.device)
         self.len = torch.zeros(self.capacity, dtype=torch.int32, device=self.device)
         self.arr = torch.zeros(self.capacity, dtype=torch.float32, device=self.device)
-        self.win = torch.zeros(self.window, dtype=torch.int32, device=self.device)
-        self.incremental = bool(incremental)
-        if self.incremental:  # the window's histogram and the copy a partition reads
-            self.hist = torch.zeros(params.max_len + 1, dtype=torch.int32, device=self.device)
-            self.snap = torch.zeros(params.max_len + 1, dtype=torch.int32, device=self.device)
-        else:  # the copy of the window a partition reads
-            self.hist = None
-            self.snap = torch.zeros(self.window, dtype=torch.int32, device=self.device)
+        self.log = torch.zeros(self.log_cap, dtype=torch.int32, device=self.device)
+        self.hist = torch.zeros(params.max_len + 1, dtype=torch.int32, device=self.device)
         self.tables = [ewsjf.new_table(self.device), ewsjf.new_table(self.device)]
         self.cur = 0
         self.ws_step = ewsjf.Workspace(self.device)
@@ -72,14 +78,26 @@ class StreamingScheduler:
                     torch.empty((1, self.B), dtype=torch.float32, device=self.device),
                     torch.empty((1,), dtype=torch.int32, device=self.device))
         self.side = torch.cuda.Stream(device=self.device)  # default priority
-        self.pending = None  # event of a partition that takes effect at the next step
-        self.ring_pos = 0    # next ring slot to write
-        self.win_pos = 0     # next window slot to write (the oldest entry)
+        self.pending = None    # event of a partition that takes effect at the next step
+        self.ring_pos = 0      # next ring slot to write
+        self.head = 0          # lengths written to the log so far; the window is [head - window, head)
+        self.hist_head = 0     # self.hist counts the window [hist_head - window, hist_head)
+        self.read_lo = None    # oldest log entry a queued side-stream read still needs
+        self.read_done = None  # event after that read
+        self.advanced = 0      # repartitions that moved the histogram (the rest recounted the window)
 
     # -- state ----------------------------------------------------------------
     def table(self) -> torch.Tensor:
         """The queue table the next step uses (once any pending partition lands)."""
         return self.tables[self.cur if self.pending is None else 1 - self.cur]
+
+    def window_lengths(self) -> torch.Tensor:
+        """The current window (a copy, oldest first), after the side stream's
+        queued reads; for checks."""
+        main = torch.cuda.current_stream(self.device)
+        main.wait_stream(self.side)
+        idx = (torch.arange(self.head - self.window, self.head, device=self.device) % self.log_cap)
+        return self.log[idx]
 
     def fill(self, length, arrival) -> None:
         """Fill every ring slot (ids 0..capacity-1), take the window from the
@@ -89,50 +107,67 @@ class StreamingScheduler:
         arrival = _dev(arrival, torch.float32, self.device)
         if length.numel() != self.capacity or arrival.numel() != self.capacity:
             raise ValueError("the initial fill covers every ring slot")
+        main = torch.cuda.current_stream(self.device)
+        main.wait_stream(self.side)  # earlier side-stream work is done
         self.len.copy_(length)
         self.arr.copy_(arrival)
-        # window slot i holds the i-th oldest of the last `window` arrivals
-        self.win.copy_(length[self.capacity - self.window:])
-        self.win_pos = 0
+        self.log[:self.window].copy_(length[self.capacity - self.window:])
         self.ring_pos = 0
-        if self.incremental:
-            ewsjf.window_histogram(self.win, self.params.max_len, hist=self.hist)
-            ewsjf.partition_hist(self.hist, self.params, table=self.tables[self.cur], ws=self.ws_part)
-        else:
-            ewsjf.partition(self.win, self.params, table=self.tables[self.cur], ws=self.ws_part)
+        self.head = self.hist_head = self.window
+        self.read_lo = self.read_done = None
+        ewsjf.window_histogram(self.log, self.params.max_len, hist=self.hist, begin=0, n=self.window)
+        ewsjf.partition_hist(self.hist, self.params, table=self.tables[self.cur], ws=self.ws_part)
         self.pending = None
+        self.side.wait_stream(main)  # the side stream's next reads follow the fill
+
+    def _log_slot(self, n: int) -> int:
+        """The log slot of the next n lengths; first makes the current stream
+        wait for a queued side-stream read those writes would overwrite."""
+        if n > self.log_cap:
+            raise ValueError("one step inserts at most log_capacity arrivals")
+        if self.read_lo is not None and self.head + n - self.log_cap > self.read_lo:
+            torch.cuda.current_stream(self.device).wait_event(self.read_done)
+            self.read_lo = self.read_done = None
+        return self.head % self.log_cap
 
     def insert(self, length: torch.Tensor, arrival: torch.Tensor) -> None:
         """Write one step's arrivals into the next ring slots (evicting what
-        was there) and into the window (replacing its oldest entries)."""
+        was there) and their lengths into the log."""
         n = length.numel()
-        if arrival.numel() != n or n > self.capacity or n > self.window:
-            raise ValueError("one step inserts at most min(capacity, window) arrivals")
-        ewsjf.ring_insert(self.len, self.arr, self.ring_pos, length, arrival, window=self.win, wpos=self.win_pos,
-                          hist=self.hist)
+        if arrival.numel() != n or n > self.capacity:
+            raise ValueError("one step inserts at most capacity arrivals")
+        wpos = self._log_slot(n)
+        ewsjf.ring_insert(self.len, self.arr, self.ring_pos, length, arrival, window=self.log, wpos=wpos)
         self.ring_pos = (self.ring_pos + n) % self.capacity
-        self.win_pos = (self.win_pos + n) % self.window
+        self.head += n
 
     def launch_repartition(self) -> None:
-        """Partition the current window on the side stream; the new table
-        takes effect at the next step()."""
+        """Partition the window as of the last step on the side stream; the
+        new table takes effect at the next step()."""
         if self.pending is not None:
             raise RuntimeError("a partition is already pending")
         main = torch.cuda.current_stream(self.device)
-        # the next insert may change the window and its histogram
-        self.snap.copy_(self.hist if self.incremental else self.win)
-        ready = torch.cuda.Event()
-        ready.record(main)
-        nxt = 1 - self.cur
-        with torch.cuda.stream(self.side):
-            self.side.wait_event(ready)
-            if self.incremental:
-                ewsjf.partition_hist(self.snap, self.params, table=self.tables[nxt], ws=self.ws_part,
-                                     stream=self.side)
-            else:
-                ewsjf.partition(self.snap, self.params, table=self.tables[nxt], ws=self.ws_part, stream=self.side)
-            done = torch.cuda.Event()
-            done.record(self.side)
+        self.side.wait_stream(main)  # the log holds every step so far
+        H, W, R, new = self.head, self.window, self.log_cap, self.head - self.hist_head
+        if self.incremental and new < W and new <= R - W:
+            # the entries that left ([hist_head - W, H - W)) and joined ([hist_head, H)) are both in the log
+            ewsjf.window_advance(self.log, self.hist_head % R, (self.hist_head - W) % R, new, self.hist,
+                                 stream=self.side)
+            lo = self.hist_head - W
+            self.advanced += 1
+        else:
+            ewsjf.window_histogram(self.log, self.params.max_len, hist=self.hist, begin=(H - W) % R, n=W,
+                                   stream=self.side)
+            lo = H - W
+        self.hist_head = H
+        read = torch.cuda.Event()
+        read.record(self.side)
+        self.read_lo = lo if self.read_lo is None else min(self.read_lo, lo)
+        self.read_done = read
+        ewsjf.partition_hist(self.hist, self.params, table=self.tables[1 - self.cur], ws=self.ws_part,
+                             stream=self.side)
+        done = torch.cuda.Event()
+        done.record(self.side)
         self.pending = done
 
     def step(self, now: float, tombstone: bool = True, length: torch.Tensor | None = None,
@@ -149,13 +184,14 @@ class StreamingScheduler:
             return ewsjf.step(self.len, self.arr, now, self.tables[self.cur], self.theta, self.B, self.cost,
                               tombstone=tombstone, out=self.out, ws=self.ws_step)
         n = length.numel()
-        if arrival is None or arrival.numel() != n or n > self.capacity or n > self.window:
-            raise ValueError("one step inserts at most min(capacity, window) arrivals")
+        if arrival is None or arrival.numel() != n or n > self.capacity:
+            raise ValueError("one step inserts at most capacity arrivals")
+        wpos = self._log_slot(n)
         out = ewsjf.ring_step(self.len, self.arr, self.ring_pos, length, arrival, now, self.tables[self.cur],
-                              self.theta, self.B, self.cost, window=self.win, wpos=self.win_pos, tombstone=tombstone,
-                              out=self.out, ws=self.ws_step, hist=self.hist)
+                              self.theta, self.B, self.cost, window=self.log, wpos=wpos, tombstone=tombstone,
+                              out=self.out, ws=self.ws_step)
         self.ring_pos = (self.ring_pos + n) % self.capacity
-        self.win_pos = (self.win_pos + n) % self.window
+        self.head += n
         return out
 
     def apply_tombstones(self, ids) -> None:

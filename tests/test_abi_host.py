@@ -116,8 +116,8 @@ def test_select_route_score_argument_errors():
 def test_ring_insert_argument_errors():
     lib = L.lib()
 
-    def ins(rl=FAKE, ra=FAKE, cap=100, pos=0, w=FAKE, wc=50, wpos=0, h=None, hm=0, nl=FAKE, na=FAKE, n=10):
-        return lib.ewsjf_ring_insert(rl, ra, cap, pos, w, wc, wpos, h, hm, nl, na, n, None)
+    def ins(rl=FAKE, ra=FAKE, cap=100, pos=0, w=FAKE, wc=50, wpos=0, nl=FAKE, na=FAKE, n=10):
+        return lib.ewsjf_ring_insert(rl, ra, cap, pos, w, wc, wpos, nl, na, n, None)
 
     assert ins(rl=None) == L.ERR_NULL
     assert ins(na=None) == L.ERR_NULL
@@ -131,12 +131,6 @@ def test_ring_insert_argument_errors():
     assert ins(w=None, wc=0, wpos=3) == L.ERR_ARG
     assert ins(n=0) == L.OK                     # nothing to do, no device touched
     assert ins(rl=None, ra=None, nl=None, na=None, n=0) == L.OK
-    # the window's histogram: needs a window and 1 <= max_len <= EWSJF_MAX_LEN
-    assert ins(h=FAKE, hm=4096, n=0) == L.OK
-    assert ins(h=FAKE, hm=4096, w=None, wc=0) == L.ERR_ARG
-    assert ins(h=FAKE, hm=0) == L.ERR_ARG
-    assert ins(h=FAKE, hm=L.MAX_LEN + 1) == L.ERR_ARG
-    assert ins(h=None, hm=7) == L.ERR_ARG
 
 
 def test_window_histogram_and_partition_hist_argument_errors():
@@ -145,14 +139,32 @@ def test_window_histogram_and_partition_hist_argument_errors():
     need = lib.ewsjf_workspace_bytes(L.OP_PARTITION, 0, 0, 0, C.byref(p))
     assert 0 < need <= lib.ewsjf_workspace_bytes(L.OP_PARTITION, 100, 0, 0, C.byref(p))
 
-    def wh(win=FAKE, n=100, m=4096, h=FAKE):
-        return lib.ewsjf_window_histogram(win, n, m, h, None)
+    def wh(ring=FAKE, cap=100, begin=0, n=100, m=4096, h=FAKE):
+        return lib.ewsjf_window_histogram(ring, cap, begin, n, m, h, None)
 
     assert wh(h=None) == L.ERR_NULL
-    assert wh(win=None) == L.ERR_NULL
+    assert wh(ring=None) == L.ERR_NULL
     assert wh(n=-1) == L.ERR_ARG
+    assert wh(n=101) == L.ERR_ARG               # more entries than the ring holds
+    assert wh(begin=100) == L.ERR_ARG
+    assert wh(begin=-1) == L.ERR_ARG
+    assert wh(cap=0, n=0, begin=1) == L.ERR_ARG
     assert wh(m=0) == L.ERR_ARG
     assert wh(m=L.MAX_LEN + 1) == L.ERR_ARG
+
+    def wa(ring=FAKE, cap=100, add=10, sub=60, n=20, m=4096, h=FAKE):
+        return lib.ewsjf_window_advance(ring, cap, add, sub, n, m, h, None)
+
+    assert wa(ring=None) == L.ERR_NULL
+    assert wa(h=None) == L.ERR_NULL
+    assert wa(cap=0) == L.ERR_ARG
+    assert wa(add=100) == L.ERR_ARG
+    assert wa(sub=-1) == L.ERR_ARG
+    assert wa(n=101) == L.ERR_ARG
+    assert wa(n=-1) == L.ERR_ARG
+    assert wa(m=0) == L.ERR_ARG
+    assert wa(n=0) == L.OK                      # nothing to do, no device touched
+    assert wa(ring=None, h=None, n=0) == L.OK
 
     def ph(h=FAKE, p=p, table=FAKE, ws=FAKE, wsb=need):
         return lib.ewsjf_partition_hist(h, C.byref(p) if p is not None else None, table, ws, wsb, None)
@@ -200,9 +212,9 @@ def test_ring_step_argument_errors():
     c = L.Cost(0.01, 1e-4, 0.0)
     need = lib.ewsjf_workspace_bytes(L.OP_STEP, 100, 1, 8, None)
 
-    def rs(rl=FAKE, ra=FAKE, cap=100, pos=0, w=FAKE, wc=50, wpos=0, h=None, hm=0, nl=FAKE, na=FAKE, n=10, now=1.0,
-           table=FAKE, theta=FAKE, cost=c, B=8, flags=0, ids=FAKE, top=FAKE, nsel=FAKE, ws=FAKE, wsb=need):
-        return lib.ewsjf_ring_step(rl, ra, cap, pos, w, wc, wpos, h, hm, nl, na, n, now, table, theta,
+    def rs(rl=FAKE, ra=FAKE, cap=100, pos=0, w=FAKE, wc=50, wpos=0, nl=FAKE, na=FAKE, n=10, now=1.0, table=FAKE,
+           theta=FAKE, cost=c, B=8, flags=0, ids=FAKE, top=FAKE, nsel=FAKE, ws=FAKE, wsb=need):
+        return lib.ewsjf_ring_step(rl, ra, cap, pos, w, wc, wpos, nl, na, n, now, table, theta,
                                    C.byref(cost) if cost is not None else None, B, flags, ids, top, nsel, ws, wsb, None)
 
     assert rs(rl=None) == L.ERR_NULL
@@ -219,9 +231,6 @@ def test_ring_step_argument_errors():
     assert rs(now=float("nan")) == L.ERR_ARG
     assert rs(wsb=need - 1) == L.ERR_WORKSPACE
     assert rs(ra=FAKE_MIS) == L.ERR_ALIGN
-    assert rs(h=FAKE, hm=4096, w=None, wc=0) == L.ERR_ARG
-    assert rs(h=FAKE, hm=0) == L.ERR_ARG
-    assert rs(h=None, hm=3) == L.ERR_ARG
 
 
 def test_partition_argument_errors():

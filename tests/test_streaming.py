@@ -69,12 +69,13 @@ def test_constructor_rejects_window_larger_than_ring():
 
 
 # ---- lockstep parity on the GPU ---------------------------------------------------
-def _lockstep(capacity, per_step, steps, window, rp_every, B, K, label, tombstone_check_every=0, fused=False):
+def _lockstep(capacity, per_step, steps, window, rp_every, B, K, label, tombstone_check_every=0, fused=False,
+              incremental=True):
     from paper_2601_21758_amd import ewsjf
     s = W.Streaming(seed=4, capacity=capacity, per_step=per_step, steps=steps, window=window, rp_every=rp_every,
                     B=B, K=K)
     prm = ewsjf.params(init_queues=K, max_queues=K)
-    gpu = StreamingScheduler(capacity, window, B, prm, s.theta[0], s.cost)
+    gpu = StreamingScheduler(capacity, window, B, prm, s.theta[0], s.cost, incremental=incremental)
     ref = OracleStream(capacity, window, B, K, K, s.theta, s.cost)
     L0, A0 = s.initial_fill()
     gpu.fill(L0, A0)
@@ -116,13 +117,29 @@ def _lockstep(capacity, per_step, steps, window, rp_every, B, K, label, tombston
             assert np.array_equal(gpu.len.cpu().numpy(), ref.len), f"{label}: ring lengths diverged at step {step}"
             print(f"{label}: step {step} ok (near-tie differences so far {near})", flush=True)
     assert np.array_equal(gpu.arr.cpu().numpy(), ref.arr)
-    return near
+    assert np.array_equal(np.sort(gpu.window_lengths().cpu().numpy()), np.sort(ref.win)), f"{label}: window differs"
+    return near, gpu
 
 
 @pytest.mark.gpu
-def test_streaming_lockstep_small():
-    _lockstep(capacity=1 << 14, per_step=512, steps=120, window=4096, rp_every=10, B=64, K=16, label="small",
-              tombstone_check_every=7)
+@pytest.mark.parametrize("incremental", [True, False])
+def test_streaming_lockstep_small(incremental):
+    # the window turns over between partitions: every partition but the first
+    # (one step after the fill) recounts it
+    _, gpu = _lockstep(capacity=1 << 14, per_step=512, steps=120, window=4096, rp_every=10, B=64, K=16,
+                       label="small", tombstone_check_every=7, incremental=incremental)
+    assert gpu.advanced == (1 if incremental else 0)
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("incremental", [True, False])
+def test_streaming_lockstep_slow_window(incremental):
+    # 100 arrivals per step and a partition every 7 steps over a 4,096-length
+    # window: the histogram moves forward by 700 entries per partition (or
+    # the window is recounted, without incremental)
+    _, gpu = _lockstep(capacity=1 << 13, per_step=100, steps=150, window=4096, rp_every=7, B=32, K=16,
+                       label="slow", tombstone_check_every=5, fused=incremental, incremental=incremental)
+    assert (gpu.advanced > 0) == incremental
 
 
 @pytest.mark.gpu

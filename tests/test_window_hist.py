@@ -1,9 +1,9 @@
 """The sliding-window partitioner input on the GPU: the window's length
-histogram (built once, then kept current by the ring inserts) and
-Refine-and-Prune started from it.  The histogram must equal a count of the
-window's clamped lengths bit for bit, and the table partitioned from it must
-equal, bit for bit, both the table partitioned from the window and the
-oracle's."""
+histogram (counted from a range of a ring of recent lengths, or moved
+forward as the window slides) and Refine-and-Prune started from it.  The
+histogram must equal a count of the window's clamped lengths bit for bit,
+and the table partitioned from it must equal, bit for bit, both the table
+partitioned from the window and the oracle's."""
 import sys
 
 import numpy as np
@@ -104,97 +104,102 @@ def test_partition_hist_of_an_empty_histogram(E, mode):
     assert host(q).tolist() == [0, 0, 0, 0, -1]
 
 
-def _steps(rng, cap, wcap, L, steps):
-    """(pos, wpos, new lengths, new arrivals) of a run of inserts that wraps
-    both rings several times; lengths include clamped values and repeats."""
-    pos = wpos = 0
-    out = []
-    for s in range(steps):
-        n = int(rng.choice([0, 1, 17, wcap // 3, wcap]))
-        nl = rng.integers(-3, L + 40, n).astype(np.int32)
-        if n > 4:
-            nl[:4] = [1, L, nl[4], nl[4]]
-        na = (s + rng.random(n)).astype(np.float32)
-        out.append((pos, wpos, nl, na))
-        pos = (pos + n) % cap
-        wpos = (wpos + n) % wcap
-    return out
+@pytest.mark.parametrize("cap,begin,n", [(1000, 0, 1000), (1000, 999, 1000), (1000, 600, 700), (1000, 300, 1),
+                                         (70001, 50000, 65536), (1 << 20, (1 << 20) - 5, 300000), (5, 4, 0)])
+def test_window_histogram_of_a_ring_range(E, cap, begin, n):
+    rng = np.random.default_rng(cap + begin + n)
+    L = 32768
+    ring = rng.integers(-2, L + 9, cap).astype(np.int32)
+    say(f"window histogram of ring[{begin}..+{n}) mod {cap}")
+    h = E.window_histogram(dev(ring), L, begin=begin, n=n)
+    assert np.array_equal(host(h), count(ring[(begin + np.arange(n)) % cap], L))
 
 
-@pytest.mark.parametrize("L", [32768, 600])
-def test_ring_insert_keeps_the_histogram(E, L):
-    rng = np.random.default_rng(11)
-    cap, wcap = 5000, 1201
-    win = rng.integers(1, L + 1, wcap).astype(np.int32)
-    g_rl = torch.zeros(cap, dtype=torch.int32, device="cuda")
-    g_ra = torch.zeros(cap, dtype=torch.float32, device="cuda")
-    g_w = dev(win.copy())
-    g_h = E.window_histogram(g_w, L)
-    say(f"ring_insert histogram L={L}")
-    for pos, wpos, nl, na in _steps(rng, cap, wcap, L, 60):
-        E.ring_insert(g_rl, g_ra, pos, dev(nl), dev(na), window=g_w, wpos=wpos, hist=g_h)
-        win[(wpos + np.arange(nl.size)) % wcap] = nl
-        assert np.array_equal(host(g_w), win)
-        assert np.array_equal(host(g_h), count(win, L)), "histogram drifted from the window"
+@pytest.mark.parametrize("L,W,R", [(32768, 4096, 8192), (32768, 1000, 1001), (700, 3001, 9000), (32768, 65536, 131072)])
+def test_window_advance_follows_the_window(E, L, W, R):
+    """A log ring of R recent lengths with the window its last W entries:
+    every few writes the histogram moves forward by the entries written since
+    (ewsjf_window_advance) and must equal a recount of the window."""
+    rng = np.random.default_rng(L + W + R)
+    log = np.zeros(R, np.int32)
+    log[:W] = rng.integers(1, L + 1, W)
+    g_log = dev(log)
+    h = E.window_histogram(g_log, L, begin=0, n=W)
+    head = hist_head = W
+    say(f"window advance L={L} W={W} R={R}")
+    for it in range(40):
+        # write a burst of lengths (clamped values and repeats included)
+        for _ in range(int(rng.integers(1, 4))):
+            n = int(rng.choice([1, 17, max(1, (R - W) // 5), R - W]))
+            n = min(n, R - W - (head - hist_head))  # the leaving entries must still be in the log
+            if n <= 0:
+                break
+            x = rng.integers(-3, L + 40, n).astype(np.int32)
+            if n > 4:
+                x[:2] = x[2]
+            slots = (head + np.arange(n)) % R
+            log[slots] = x
+            g_log[torch.from_numpy(slots).cuda()] = dev(x)
+            head += n
+        new = head - hist_head
+        E.window_advance(g_log, hist_head % R, (hist_head - W) % R, new, h)
+        hist_head = head
+        window = log[(head - W + np.arange(W)) % R]
+        assert np.array_equal(host(h), count(window, L)), f"histogram drifted at burst {it}"
 
 
-def test_ring_step_keeps_the_histogram_and_admits_the_same(E):
-    """ewsjf_ring_step with and without the histogram: same ring, window and
-    admissions; the kept histogram is the window's."""
-    rng = np.random.default_rng(12)
-    cap, wcap, B, L = 70001, 20000, 300, 32768
-    p = W.config(0)
-    t = oracle.partition(p.window, init_queues=16, max_queues=16)
-    tab = E.upload_table(t.bounds, t.mean, L, t.lo, t.hi, t.count, t.sum)
-    th = dev(W.THETA_MID.reshape(1, 6))
-    L0 = rng.integers(1, 9000, cap).astype(np.int32)
-    A0 = rng.random(cap).astype(np.float32)
-    a_rl, a_ra, b_rl, b_ra = dev(L0), dev(A0), dev(L0), dev(A0)
-    win = L0[:wcap].copy()
-    a_w, b_w = dev(win), dev(win)
-    h = E.window_histogram(a_w, L)
-    say("ring_step histogram")
-    for s, (pos, wpos, nl, na) in enumerate(_steps(rng, cap, wcap, L, 25)):
-        now = float(s + 1)
-        ga = E.ring_step(a_rl, a_ra, pos, dev(nl), dev(na), now, tab, th, B, window=a_w, wpos=wpos, tombstone=True,
-                         hist=h)
-        gb = E.ring_step(b_rl, b_ra, pos, dev(nl), dev(na), now, tab, th, B, window=b_w, wpos=wpos, tombstone=True)
-        for x, y in zip(ga, gb):
-            assert np.array_equal(host(x), host(y), equal_nan=True)
-        assert torch.equal(a_rl, b_rl) and torch.equal(a_w, b_w)
-        win[(wpos + np.arange(nl.size)) % wcap] = nl
-        assert np.array_equal(host(a_w), win)
-        assert np.array_equal(host(h), count(win, L)), f"histogram drifted at step {s}"
+def test_window_advance_of_nothing_and_of_a_whole_window(E):
+    L, W = 32768, 5000
+    rng = np.random.default_rng(3)
+    log = rng.integers(1, 9000, 2 * W).astype(np.int32)
+    g = dev(log)
+    h = E.window_histogram(g, L, begin=0, n=W)
+    E.window_advance(g, W, 0, 0, h)  # nothing moves
+    assert np.array_equal(host(h), count(log[:W], L))
+    E.window_advance(g, W, 0, W, h)  # the window becomes the second half
+    assert np.array_equal(host(h), count(log[W:], L))
 
 
-def test_streaming_scheduler_incremental_equals_window_mode(E):
-    """The streaming scheduler with the kept histogram and with the window
-    re-read at every repartition: the same tables after every repartition
-    and the same admissions at every step; the tables are the oracle's."""
+@pytest.mark.parametrize("per_step,rp_every", [(1024, 20), (200, 7)])
+def test_streaming_scheduler_incremental_equals_recount(E, per_step, rp_every):
+    """The streaming scheduler moving the window's histogram forward and
+    recounting the window at every repartition: the same tables after every
+    repartition and the same admissions at every step; the tables are the
+    oracle's partition of the window.  (1024, 20) turns the window over
+    between partitions, (200, 7) does not."""
     from paper_2601_21758_amd.streaming import StreamingScheduler
-    s = W.Streaming(seed=5, capacity=1 << 15, per_step=1024, steps=120, window=8192, rp_every=20, B=128, K=32)
+    steps = 120
+    s = W.Streaming(seed=5, capacity=1 << 15, per_step=per_step, steps=steps, window=8192, rp_every=rp_every, B=128,
+                    K=32)
     prm = E.params(init_queues=32, max_queues=32)
     a = StreamingScheduler(s.capacity, s.window_size, s.B, prm, s.theta[0], s.cost, incremental=True)
     b = StreamingScheduler(s.capacity, s.window_size, s.B, prm, s.theta[0], s.cost, incremental=False)
     L0, A0 = s.initial_fill()
     a.fill(L0, A0)
     b.fill(L0, A0)
-    hist_win = [L0[-s.window_size:]]
-    say("streaming incremental vs window re-read")
-    for i in range(120):
+    seen = [L0[-s.window_size:]]
+    say(f"streaming incremental vs recount per_step={per_step} rp_every={rp_every}")
+    for i in range(steps):
         Ln, An = s.arrivals(i)
         now = float(An[-1])
         ra = a.step(now, length=dev(Ln), arrival=dev(An))
         rb = b.step(now, length=dev(Ln), arrival=dev(An))
         for x, y in zip(ra, rb):
             assert np.array_equal(host(x), host(y), equal_nan=True), f"admissions differ at step {i}"
-        hist_win.append(Ln)
-        if i % 20 == 0:
+        seen.append(Ln)
+        if i % rp_every == 0:
             a.launch_repartition()
             b.launch_repartition()
             torch.cuda.synchronize()
             ta, tb = a.table(), b.table()
             assert torch.equal(ta, tb), f"tables differ after step {i}"
-            window = np.concatenate(hist_win)[-s.window_size:]
+            window = np.concatenate(seen)[-s.window_size:]
             assert np.array_equal(host(a.hist), count(window, prm.max_len))
+            assert np.array_equal(np.sort(host(a.window_lengths())), np.sort(window))
             check_table(E.read_table(ta), oracle.partition(window, init_queues=32, max_queues=32))
+    assert b.advanced == 0
+    # the histogram moves forward when fewer than `window` entries joined since
+    # the last count (the first partition follows one step; later ones follow
+    # rp_every steps); otherwise the window is recounted
+    joined = [per_step] + [per_step * rp_every] * ((steps - 1) // rp_every)
+    assert a.advanced == sum(j < s.window_size for j in joined)
