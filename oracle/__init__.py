@@ -54,15 +54,20 @@ def _declare(L):
     L.oracle_partition.restype = C.c_int
     L.oracle_route.argtypes = [_p(i32), i64, _p(i32), i32, _p(i32)]
     L.oracle_route.restype = None
-    L.oracle_score.argtypes = [_p(i32), _p(f32), i64, f32, i32, _p(i32), _p(f64), _p(f32), i32,
-                               f64, f64, f64, _p(f32)]
+    L.oracle_route_gapped.argtypes = [_p(i32), i64, _p(i32), _p(i32), i32, _p(i32)]
+    L.oracle_route_gapped.restype = None
+    L.oracle_score.argtypes = [_p(i32), _p(f32), i64, f32, i32, _p(i32), _p(i32), _p(i32), i32, _p(f64), _p(f32),
+                               i32, f64, f64, f64, _p(f32)]
     L.oracle_score.restype = None
     L.oracle_select.argtypes = [_p(f32), i64, i32, i32, _p(i32), _p(f32), _p(i32)]
     L.oracle_select.restype = None
     L.oracle_tactical_step.argtypes = [_p(i32), _p(f32), i64, f32, _p(i32), _p(i32), _p(i64), _p(i64), _p(i32),
-                                       _p(i32), _p(f64), _p(i32), _p(f32), f64, f64, f64, i32, i32, f64,
+                                       _p(i32), _p(f64), _p(i32), i32, _p(f32), f64, f64, f64, i32, i32, f64,
                                        _p(i32), _p(i32), _p(i32), _p(f32), _p(i32)]
     L.oracle_tactical_step.restype = C.c_int
+    L.oracle_dispatch.argtypes = [_p(i32), _p(f32), i64, _p(i32), _p(i32), _p(i64), _p(i64), _p(i32), _p(i32),
+                                  _p(f64), i32, i32, _p(i32)]
+    L.oracle_dispatch.restype = C.c_int
 
 
 def _ptr(a, t):
@@ -75,7 +80,10 @@ def _arr(a, dtype):
 
 @dataclass
 class Table:
-    """Queue table: k contiguous intervals; bounds[i] = lo of queue i+1."""
+    """Queue table: k intervals in length order; bounds[i] = lo of queue i+1.
+    Routing reads them as a contiguous cover of bounds, or (gapped, after a
+    dispatch with bubble queues) as the lengths [lo_i, hi_i] of each queue
+    with Algorithm 2's rule in the gaps."""
     k: int
     bounds: np.ndarray   # int32 [k-1]
     count: np.ndarray    # int64 [k]
@@ -86,6 +94,7 @@ class Table:
     n_distinct: int = 0
     n_coarse: int = 0
     n_leaves: int = 0
+    gapped: bool = False
 
 
 @dataclass
@@ -170,24 +179,60 @@ def partition(window, p: PartitionParams | None = None, **kw) -> Table:
 
 
 def route(length, table_or_bounds):
-    bounds = table_or_bounds.bounds if isinstance(table_or_bounds, Table) else table_or_bounds
-    b = _arr(bounds, np.int32)
     L = _arr(length, np.int32)
     q = np.zeros(L.size, np.int32)
+    if isinstance(table_or_bounds, Table) and table_or_bounds.gapped:
+        t = table_or_bounds
+        lo, hi = _arr(t.lo, np.int32), _arr(t.hi, np.int32)
+        lib().oracle_route_gapped(_ptr(L, C.c_int32), L.size, _ptr(lo, C.c_int32), _ptr(hi, C.c_int32), t.k,
+                                  _ptr(q, C.c_int32))
+        return q
+    bounds = table_or_bounds.bounds if isinstance(table_or_bounds, Table) else table_or_bounds
+    b = _arr(bounds, np.int32)
     lib().oracle_route(_ptr(L, C.c_int32), L.size, _ptr(b, C.c_int32), b.size + 1, _ptr(q, C.c_int32))
     return q
+
+
+def dispatch(length, arrival, table: Table, bubble_width: int, max_queues: int):
+    """The Dispatcher with on-demand bubble queues (Algorithm 2) over the
+    requests with length > 0 in arrival order: (qid per request in the final
+    queue set, the gapped table after the bubbles)."""
+    L = _arr(length, np.int32)
+    A = _arr(arrival, np.float32)
+    cap = max(int(max_queues), table.k)
+    k = np.array([table.k], np.int32)
+    bounds = np.zeros(cap, np.int32)
+    count, ssum = np.zeros(cap, np.int64), np.zeros(cap, np.int64)
+    lo, hi = np.zeros(cap, np.int32), np.zeros(cap, np.int32)
+    mean = np.zeros(cap, np.float64)
+    count[:table.k], ssum[:table.k] = table.count, table.sum
+    lo[:table.k], hi[:table.k], mean[:table.k] = table.lo, table.hi, table.mean
+    qid = np.zeros(L.size, np.int32)
+    r = lib().oracle_dispatch(_ptr(L, C.c_int32), _ptr(A, C.c_float), L.size, _ptr(k, C.c_int32),
+                              _ptr(bounds, C.c_int32), _ptr(count, C.c_int64), _ptr(ssum, C.c_int64),
+                              _ptr(lo, C.c_int32), _ptr(hi, C.c_int32), _ptr(mean, C.c_double), int(bubble_width),
+                              int(max_queues), _ptr(qid, C.c_int32))
+    if r != 0:
+        raise ValueError("bad dispatch arguments")
+    kk = int(k[0])
+    t2 = Table(kk, bounds[:kk - 1].copy(), count[:kk].copy(), ssum[:kk].copy(), lo[:kk].copy(), hi[:kk].copy(),
+               mean[:kk].copy(), table.n_distinct, table.n_coarse, table.n_leaves, True)
+    return qid, t2
 
 
 def score(length, arrival, now, table: Table, theta, cost=(0.01, 1e-4, 0.0)):
     L = _arr(length, np.int32)
     A = _arr(arrival, np.float32)
     th = _arr(theta, np.float32).reshape(-1, 6)
-    b = _arr(table.bounds, np.int32)
+    b = np.zeros(max(1, table.k - 1), np.int32)
+    b[:table.k - 1] = table.bounds
+    lo, hi = _arr(table.lo, np.int32), _arr(table.hi, np.int32)
     m = _arr(table.mean, np.float64)
     out = np.zeros((th.shape[0], L.size), np.float32)
     lib().oracle_score(_ptr(L, C.c_int32), _ptr(A, C.c_float), L.size, float(np.float32(now)), table.k,
-                       _ptr(b, C.c_int32), _ptr(m, C.c_double), _ptr(th, C.c_float), th.shape[0],
-                       float(cost[0]), float(cost[1]), float(cost[2]), _ptr(out, C.c_float))
+                       _ptr(b, C.c_int32), _ptr(lo, C.c_int32), _ptr(hi, C.c_int32), int(table.gapped),
+                       _ptr(m, C.c_double), _ptr(th, C.c_float), th.shape[0], float(cost[0]), float(cost[1]),
+                       float(cost[2]), _ptr(out, C.c_float))
     return out
 
 
@@ -246,7 +291,8 @@ def tactical_step(length, arrival, now, table: Table, empty_cnt, theta, B, empty
     r = lib().oracle_tactical_step(_ptr(L, C.c_int32), _ptr(A, C.c_float), L.size, float(np.float32(now)),
                                    _ptr(k, C.c_int32), _ptr(bounds, C.c_int32), _ptr(count, C.c_int64),
                                    _ptr(ssum, C.c_int64), _ptr(lo, C.c_int32), _ptr(hi, C.c_int32),
-                                   _ptr(mean, C.c_double), _ptr(ec, C.c_int32), _ptr(th, C.c_float),
+                                   _ptr(mean, C.c_double), _ptr(ec, C.c_int32), int(table.gapped),
+                                   _ptr(th, C.c_float),
                                    float(cost[0]), float(cost[1]), float(cost[2]), int(B), int(empty_threshold),
                                    float(eps), _ptr(ids, C.c_int32), _ptr(nsel, C.c_int32), _ptr(qp, C.c_int32),
                                    _ptr(hs, C.c_float), _ptr(rm, C.c_int32))
@@ -254,5 +300,5 @@ def tactical_step(length, arrival, now, table: Table, empty_cnt, theta, B, empty
         raise ValueError("bad tactical-step arguments")
     k1 = int(k[0])
     t2 = Table(k1, bounds[:k1 - 1].copy(), count[:k1].copy(), ssum[:k1].copy(), lo[:k1].copy(), hi[:k1].copy(),
-               mean[:k1].copy(), table.n_distinct, table.n_coarse, table.n_leaves)
+               mean[:k1].copy(), table.n_distinct, table.n_coarse, table.n_leaves, table.gapped)
     return TacticalResult(ids[:int(nsel[0])].copy(), int(qp[0]), hs, rm.astype(bool), t2, ec[:k1].copy())

@@ -267,6 +267,77 @@ int32_t route_one(int32_t b, const int32_t* bounds, int32_t k) {
   return (int32_t)(std::upper_bound(bounds, bounds + (k - 1), b) - bounds);
 }
 
+// ---------------------------------------------------------------------------
+// Algorithm 2 (Section 4.3 and the appendix algorithm "On-Demand Bubble Queue
+// Creation"): the Dispatcher's rule for a length that falls between two
+// queues, and the gapped reading of a queue table that it needs.
+//
+// Readings (the paper leaves these open):
+//   B1 Queue i holds the lengths [lo_i, hi_i]: for a partitioned table the
+//      smallest and largest window length that fell in it, for a bubble its
+//      interval.  In the algorithm's notation min_len = lo_i and max_len =
+//      hi_i + 1 (the half-open [min_len, max_len) of Section 4.2).
+//   B2 A length below the first queue goes to queue 0 and one above the last
+//      to queue k-1: the algorithm covers gaps between two queues only.
+//   B3 The tolerances in exact integer arithmetic: L <= 1.10 * max_len is
+//      10 L <= 11 max_len, and L >= 0.90 * min_len is 10 L >= 9 min_len.
+//   B4 range / 2 on integers: the bubble is [L - floor(range/2),
+//      L - floor(range/2) + range) (range lengths, L inside), clipped to the
+//      gap [max_len_i, min_len_{i+1}).
+//   B5 A bubble's profile is the request that created it: count 1, sum L,
+//      mean L; lo/hi are its interval (B1).
+//   B6 Requests are dispatched one at a time in arrival order (T1's FIFO
+//      order), each against the queue set the earlier ones left; empty slots
+//      (len <= 0) are not dispatched (qid -1).  A request's queue index is its
+//      queue's place in the final set (a bubble shifts the queues above it).
+//   B7 The set holds at most max_queues queues.  Once it is full, a request
+//      that would create a bubble joins the nearer neighbour (L - hi_i
+//      against lo_{i+1} - L; equal distances: the lower).
+//   B8 A length routed without being dispatched (a request already pending
+//      when the queue set changes) takes the algorithm's first two branches,
+//      and B7's nearer neighbour in place of a bubble.
+// ---------------------------------------------------------------------------
+
+// Where length b >= 1 lies: returns false with *q its queue (inside one, or
+// below the first / above the last, B2), or true with *q the queue below the
+// gap that holds b.
+bool in_gap(int32_t b, const int32_t* lo, const int32_t* hi, int32_t k, int32_t* q) {
+  const int32_t i = (int32_t)(std::upper_bound(lo, lo + k, b) - lo) - 1;  // last queue with lo <= b
+  if (i < 0) {
+    *q = 0;
+    return false;
+  }
+  *q = i;
+  return !(b <= hi[i] || i == k - 1);
+}
+
+// Algorithm 2's first two branches (B3) for b between queues i and i+1:
+// i, i + 1, or -1 for a true gap.
+int32_t tolerance(int64_t b, int64_t max_len_i, int64_t min_len_next, int32_t i) {
+  if (10 * b <= 11 * max_len_i) return i;
+  if (10 * b >= 9 * min_len_next) return i + 1;
+  return -1;
+}
+
+// B7: the nearer of queues i and i+1.
+int32_t nearer(int64_t b, int64_t hi_i, int64_t lo_next, int32_t i) { return b - hi_i <= lo_next - b ? i : i + 1; }
+
+// B8: the queue of length b in the gapped reading, without dispatch.
+int32_t route_gapped(int32_t b, const int32_t* lo, const int32_t* hi, int32_t k) {
+  if (b <= 0) return -1;
+  int32_t i;
+  if (!in_gap(b, lo, hi, k, &i)) return i;
+  const int32_t t = tolerance(b, (int64_t)hi[i] + 1, lo[i + 1], i);
+  return t >= 0 ? t : nearer(b, hi[i], lo[i + 1], i);
+}
+
+// The queue of length b under the table's reading: the contiguous cover of
+// bounds, or the gapped reading of lo/hi.
+int32_t route_table(int32_t b, const int32_t* bounds, const int32_t* lo, const int32_t* hi, int32_t k,
+                    int32_t gapped) {
+  return gapped ? route_gapped(b, lo, hi, k) : route_one(b, bounds, k);
+}
+
 
 // ---------------------------------------------------------------------------
 // Algorithm 1 (Section 3.2, "Tactical Loop"): the paper's own batch rule
@@ -439,18 +510,90 @@ void oracle_route(const int32_t* len, int64_t n, const int32_t* bounds, int32_t 
   for (int64_t i = 0; i < n; ++i) qid[i] = route_one(len[i], bounds, k);
 }
 
+void oracle_route_gapped(const int32_t* len, int64_t n, const int32_t* lo, const int32_t* hi, int32_t k,
+                         int32_t* qid) {
+  for (int64_t i = 0; i < n; ++i) qid[i] = route_gapped(len[i], lo, hi, k);
+}
+
+// The Dispatcher with on-demand bubble queues (Algorithm 2, readings B1-B7)
+// over the requests with len > 0, in arrival order.  The queue set (k,
+// bounds, count, sum, lo, hi, mean; arrays of max_queues entries) is read in
+// its gapped reading and updated in place: bubbles are inserted in length
+// order, bounds[i-1] = lo_i.  qid[i] = request i's queue in the final set.
+int oracle_dispatch(const int32_t* len, const float* arrival, int64_t n, int32_t* k_io, int32_t* bounds,
+                    int64_t* count, int64_t* sum, int32_t* lo, int32_t* hi, double* mean, int32_t bubble_width,
+                    int32_t max_queues, int32_t* qid) {
+  const int32_t k = *k_io;
+  if (k < 1 || n < 0 || bubble_width < 1 || max_queues < k) return kErrArg;
+  struct Q {
+    int32_t lo, hi;
+    int64_t n, S;
+    double mean;
+    int32_t ident;  // stable name of the queue while others are inserted
+  };
+  std::vector<Q> qs(k);
+  for (int32_t q = 0; q < k; ++q) qs[q] = {lo[q], hi[q], count[q], sum[q], mean[q], q};
+  std::vector<FifoKey> order;
+  for (int64_t i = 0; i < n; ++i)
+    if (len[i] > 0) order.push_back({canonical_arrival(arrival[i]), i});
+  std::stable_sort(order.begin(), order.end(), older);
+  std::vector<int32_t> who(n, -1);  // ident of each request's queue
+  int32_t next_ident = k;
+  for (const FifoKey& r : order) {
+    const int64_t b = len[r.id];
+    const int32_t m = (int32_t)qs.size();
+    std::vector<int32_t> clo(m), chi(m);
+    for (int32_t q = 0; q < m; ++q) {
+      clo[q] = qs[q].lo;
+      chi[q] = qs[q].hi;
+    }
+    int32_t i;
+    if (!in_gap((int32_t)b, clo.data(), chi.data(), m, &i)) {
+      who[r.id] = qs[i].ident;
+      continue;
+    }
+    const int64_t max_len = (int64_t)chi[i] + 1, min_len = clo[i + 1];
+    int32_t t = tolerance(b, max_len, min_len, i);
+    if (t < 0 && m < max_queues) {  // a true gap: create a bubble queue
+      const int64_t available = min_len - max_len;
+      const int64_t range = std::min<int64_t>(bubble_width, available);
+      const int64_t new_min = std::max(b - range / 2, max_len);
+      const int64_t new_max = std::min(b - range / 2 + range, min_len);
+      qs.insert(qs.begin() + i + 1, Q{(int32_t)new_min, (int32_t)(new_max - 1), 1, b, (double)b, next_ident});
+      who[r.id] = next_ident++;
+      continue;
+    }
+    if (t < 0) t = nearer(b, chi[i], clo[i + 1], i);
+    who[r.id] = qs[t].ident;
+  }
+  const int32_t k2 = (int32_t)qs.size();
+  std::vector<int32_t> place(next_ident);
+  for (int32_t q = 0; q < k2; ++q) place[qs[q].ident] = q;
+  for (int64_t i = 0; i < n; ++i) qid[i] = who[i] < 0 ? -1 : place[who[i]];
+  *k_io = k2;
+  for (int32_t q = 0; q < k2; ++q) {
+    if (q > 0) bounds[q - 1] = qs[q].lo;
+    count[q] = qs[q].n;
+    sum[q] = qs[q].S;
+    lo[q] = qs[q].lo;
+    hi[q] = qs[q].hi;
+    mean[q] = qs[q].mean;
+  }
+  return kOk;
+}
+
 // Density-Weighted Scoring (Eq. 1 / Eq. 4, defined in phi_key) for every
 // pending request and parameter vector.  theta is [n_theta][6].  Output
 // score[t * n + i] is Phi rounded once to binary32; a request whose Phi is
 // NaN gets -inf; an empty slot (len <= 0) gets NaN, which marks it as not
 // admissible.
 void oracle_score(const int32_t* len, const float* arrival, int64_t n, float now, int32_t k,
-                  const int32_t* bounds, const double* mean, const float* theta, int32_t n_theta,
-                  double c0, double c1, double c2, float* score) {
+                  const int32_t* bounds, const int32_t* lo, const int32_t* hi, int32_t gapped, const double* mean,
+                  const float* theta, int32_t n_theta, double c0, double c1, double c2, float* score) {
   for (int32_t t = 0; t < n_theta; ++t) {
     const float* th = theta + 6 * t;
     for (int64_t i = 0; i < n; ++i) {
-      const int32_t q = route_one(len[i], bounds, k);
+      const int32_t q = route_table(len[i], bounds, lo, hi, k, gapped);
       if (q < 0) {
         score[(int64_t)t * n + i] = std::numeric_limits<float>::quiet_NaN();
         continue;
@@ -484,10 +627,10 @@ void oracle_select(const float* score, int64_t n, int32_t n_theta, int32_t B, in
 // One scheduling step: route, score and select (the scratch score array is
 // [n_theta][n] floats supplied by the caller).
 void oracle_step(const int32_t* len, const float* arrival, int64_t n, float now, int32_t k,
-                 const int32_t* bounds, const double* mean, const float* theta, int32_t n_theta, double c0,
-                 double c1, double c2, int32_t B, float* score_scratch, int32_t* ids, float* top,
-                 int32_t* n_sel) {
-  oracle_score(len, arrival, n, now, k, bounds, mean, theta, n_theta, c0, c1, c2, score_scratch);
+                 const int32_t* bounds, const int32_t* lo, const int32_t* hi, int32_t gapped, const double* mean,
+                 const float* theta, int32_t n_theta, double c0, double c1, double c2, int32_t B,
+                 float* score_scratch, int32_t* ids, float* top, int32_t* n_sel) {
+  oracle_score(len, arrival, n, now, k, bounds, lo, hi, gapped, mean, theta, n_theta, c0, c1, c2, score_scratch);
   oracle_select(score_scratch, n, n_theta, B, ids, top, n_sel);
 }
 
@@ -500,15 +643,15 @@ void oracle_step(const int32_t* len, const float* arrival, int64_t n, float now,
 // at entry] (1 for the queues removed in this step).
 int oracle_tactical_step(const int32_t* len, const float* arrival, int64_t n, float now, int32_t* k_io,
                          int32_t* bounds, int64_t* count, int64_t* sum, int32_t* lo, int32_t* hi, double* mean,
-                         int32_t* empty_cnt, const float* theta, double c0, double c1, double c2, int32_t B,
-                         int32_t empty_threshold, double eps, int32_t* ids, int32_t* n_sel, int32_t* q_prim,
-                         float* head_score, int32_t* removed) {
+                         int32_t* empty_cnt, int32_t gapped, const float* theta, double c0, double c1, double c2,
+                         int32_t B, int32_t empty_threshold, double eps, int32_t* ids, int32_t* n_sel,
+                         int32_t* q_prim, float* head_score, int32_t* removed) {
   const int32_t k = *k_io;
   if (k < 1 || B < 0 || n < 0 || empty_threshold < 0) return kErrArg;
   // Dispatcher: every pending request joins the FIFO of its queue.
   std::vector<std::vector<FifoKey>> fifo(k);
   for (int64_t i = 0; i < n; ++i) {
-    const int32_t q = route_one(len[i], bounds, k);
+    const int32_t q = route_table(len[i], bounds, lo, hi, k, gapped);
     if (q >= 0) fifo[q].push_back({canonical_arrival(arrival[i]), i});
   }
   for (auto& f : fifo) std::stable_sort(f.begin(), f.end(), older);

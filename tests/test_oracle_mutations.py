@@ -52,6 +52,24 @@ MUTANTS = [
     ("absorber_highest_utility", "utility(qs[r - 1], qs[r], eps) <= utility(qs[r], qs[r + 1], eps)",
      "utility(qs[r - 1], qs[r], eps) > utility(qs[r], qs[r + 1], eps)"),
     ("absorber_drops_counts", "A = {A.n + qs[r].n, A.S + qs[r].S,", "A = {A.n, A.S + qs[r].S,"),
+    # Algorithm 2 (bubble queues)
+    ("bubble_lower_tolerance_strict", "if (10 * b <= 11 * max_len_i) return i;", "if (10 * b < 11 * max_len_i) return i;"),
+    ("bubble_upper_tolerance_factor", "if (10 * b >= 9 * min_len_next) return i + 1;",
+     "if (10 * b >= 8 * min_len_next) return i + 1;"),
+    ("bubble_max_len_is_hi", "const int64_t max_len = (int64_t)chi[i] + 1, min_len = clo[i + 1];",
+     "const int64_t max_len = (int64_t)chi[i], min_len = clo[i + 1];"),
+    ("bubble_available_off_by_one", "const int64_t available = min_len - max_len;",
+     "const int64_t available = min_len - max_len + 1;"),
+    ("bubble_not_centred", "const int64_t new_min = std::max(b - range / 2, max_len);",
+     "const int64_t new_min = std::max(b - range, max_len);"),
+    ("bubble_upper_edge_unclipped", "std::min(b - range / 2 + range, min_len)", "(b - range / 2 + range)"),
+    ("bubble_profile_is_its_width", "1, b, (double)b, next_ident", "1, range, (double)b, next_ident"),
+    ("bubble_cap_off_by_one", "if (t < 0 && m < max_queues)", "if (t < 0 && m <= max_queues)"),
+    ("nearer_tie_goes_high", "return b - hi_i <= lo_next - b ? i : i + 1;", "return b - hi_i < lo_next - b ? i : i + 1;"),
+    ("dispatch_in_id_order", "  std::stable_sort(order.begin(), order.end(), older);\n", "\n"),
+    ("gapped_route_without_tolerance", "const int32_t t = tolerance(b, (int64_t)hi[i] + 1, lo[i + 1], i);",
+     "const int32_t t = -1;"),
+    ("below_first_goes_up", "    *q = 0;\n    return false;", "    *q = k > 1 ? 1 : 0;\n    return false;"),
 ]
 
 
@@ -70,7 +88,8 @@ def _run_mutant(args):
         env = dict(os.environ, EWSJF_ORACLE_LIB=so)
         r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
                             os.path.join(ROOT, "tests", "test_oracle_pins.py"),
-                            os.path.join(ROOT, "tests", "test_oracle_tactical.py")],
+                            os.path.join(ROOT, "tests", "test_oracle_tactical.py"),
+                            os.path.join(ROOT, "tests", "test_oracle_bubble.py")],
                            cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
         return name, r.returncode
     finally:
