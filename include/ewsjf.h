@@ -7,6 +7,9 @@
  *   ewsjf_partition  Refine-and-Prune: an observation window of prompt lengths
  *                    -> contiguous queue intervals (Section 4.2, Stages 1-3,
  *                    Eq. 2 split test, Eq. 3 scheduling utility).
+ *   ewsjf_dispatch   the Dispatcher with on-demand bubble queues (Section 4.3,
+ *                    Algorithm 2): arriving requests in a gap between queues
+ *                    join a neighbour within tolerance or create a queue.
  *   ewsjf_route      Dynamic Queue Routing: each request -> the one queue whose
  *                    interval holds its prompt length (Section 3.2 Dispatcher;
  *                    Section 5, deterministic routing over contiguous,
@@ -77,7 +80,8 @@ enum {
   EWSJF_MAX_QUEUES = 256,    /* queue budget cap (the paper's example is 32) */
   EWSJF_MAX_LEN = 32768,     /* cap on the window clamp L */
   EWSJF_MAX_B = 4096,        /* admissions per step per parameter vector */
-  EWSJF_MAX_THETA = 1024     /* parameter vectors per call */
+  EWSJF_MAX_THETA = 1024,    /* parameter vectors per call */
+  EWSJF_MAX_DISPATCH = 4096  /* requests per ewsjf_dispatch call */
 };
 
 /* Stage-1 initializers (Section 4.2, Stage 1). */
@@ -132,19 +136,27 @@ typedef struct {
 
 /* Queue table: the queue structure of the active policy (Section 3.1).  A
  * fixed-size device blob of ewsjf_queue_table_bytes() bytes written by
- * ewsjf_partition or ewsjf_table_upload.  Queue i covers prompt lengths
- * [bounds[i-1], bounds[i]) with queue 0 open below and queue k-1 open above,
- * so the intervals cover every length exactly once.  lo/hi/count/sum/mean
- * describe the window lengths that fell in each queue; mean is the queue's
- * profile used by the meta-policy.  lut[b] = queue of length b for b in
- * [1, max_len] (longer lengths belong to queue k-1). */
+ * ewsjf_partition, ewsjf_table_upload or ewsjf_dispatch.  lo/hi/count/sum/mean
+ * describe the window lengths that fell in each queue (a bubble queue: its
+ * interval and its creating request, see ewsjf_dispatch); mean is the queue's
+ * profile used by the meta-policy.  Two routing readings:
+ *   gapped == 0  queue i covers prompt lengths [bounds[i-1], bounds[i]) with
+ *                queue 0 open below and queue k-1 open above, so the
+ *                intervals cover every length exactly once;
+ *   gapped == 1  queue i holds [lo_i, hi_i]; a length between queues i and
+ *                i+1 goes to queue i when 10 L <= 11 (hi_i + 1), to queue
+ *                i+1 when 10 L >= 9 lo_{i+1}, else to the nearer of the two
+ *                (L - hi_i against lo_{i+1} - L, ties to i); below the first
+ *                queue 0, above the last k-1 (Section 4.3).
+ * lut[b] = queue of length b for b in [1, max_len] under that reading
+ * (longer lengths belong to queue k-1). */
 typedef struct {
   int32_t k;
   int32_t max_len;
   int32_t n_distinct; /* diagnostics of the last partition (0 after upload) */
   int32_t n_coarse;
   int32_t n_leaves;
-  int32_t reserved0;
+  int32_t gapped;     /* routing reading: 0 contiguous bounds, 1 gapped intervals */
   int64_t n_window;
   int32_t bounds[EWSJF_MAX_QUEUES]; /* bounds[i] = lowest length of queue i+1, i < k-1 */
   int32_t lo[EWSJF_MAX_QUEUES];
@@ -164,10 +176,12 @@ size_t ewsjf_queue_table_bytes(void);
 size_t ewsjf_workspace_bytes(int op, int64_t n, int32_t n_theta, int32_t B, const ewsjf_partition_params* p);
 
 /* Install a queue structure computed elsewhere (for example a policy loaded
- * from storage).  host_table: host struct with k, max_len, bounds, lo, hi,
- * count, sum, mean filled in (lut and diagnostics are ignored).  Requires
+ * from storage).  host_table: host struct with k, max_len, gapped, bounds, lo,
+ * hi, count, sum, mean filled in (lut and diagnostics are ignored).  Requires
  * 1 <= k <= EWSJF_MAX_QUEUES, 1 <= max_len <= EWSJF_MAX_LEN and bounds strictly
- * increasing within [1, max_len], finite means.  The device copy and its
+ * increasing within [1, max_len], finite means; gapped is 0 or 1, and with 1
+ * the intervals [lo_i, hi_i] lie in [1, max_len] in increasing order without
+ * overlap.  The device copy and its
  * routing lut are written on `stream`; this set-up call then synchronizes
  * `stream` so the host struct may be released on return. */
 ewsjf_status ewsjf_table_upload(const ewsjf_queue_table* host_table, void* table, hipStream_t stream);
@@ -177,6 +191,32 @@ ewsjf_status ewsjf_table_upload(const ewsjf_queue_table* host_table, void* table
  * ewsjf_workspace_bytes(EWSJF_OP_PARTITION, n_window, 0, 0, p) bytes. */
 ewsjf_status ewsjf_partition(const int32_t* window, int64_t n_window, const ewsjf_partition_params* p,
                              void* table, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* The Dispatcher with on-demand bubble queues (Section 3.2, Dispatcher;
+ * Section 4.3 and the appendix's Algorithm 2): the requests with len > 0 join
+ * the table's queues one at a time in arrival order (arrival ascending, equal
+ * arrivals by index, a NaN arrival last, -0 as +0), each against the queue set
+ * the earlier ones left.  The set is read in its gapped form (queue i holds
+ * [lo_i, hi_i]; min_len = lo_i, max_len = hi_i + 1).  A length inside a queue
+ * joins it; below the first queue it joins queue 0, above the last queue k-1.
+ * A length L between queues i and i+1 joins queue i if 10 L <= 11 max_len_i,
+ * else queue i+1 if 10 L >= 9 min_len_{i+1}; otherwise it falls in a true gap
+ * and, while the set holds fewer than max_queues queues, creates a bubble
+ * queue [L - floor(r/2), L - floor(r/2) + r) clipped to [max_len_i,
+ * min_len_{i+1}), r = min(bubble_width, min_len_{i+1} - max_len_i), with
+ * count 1, sum L and mean L (its creating request is its profile); once the
+ * set is full it joins the nearer neighbour (L - hi_i against lo_{i+1} - L,
+ * ties to queue i).  qid[i] = request i's queue in the final set (bubbles
+ * shift the queues above them), -1 for len[i] <= 0.  The table is rewritten in
+ * place in its gapped reading (gapped = 1, bounds[i-1] = lo_i, lut rebuilt)
+ * unless it already was gapped and no bubble was created; a later
+ * ewsjf_partition replaces the bubbles with a fresh contiguous table.
+ * len, qid: device int32 [n]; arrival: device float32 [n];
+ * 0 <= n <= EWSJF_MAX_DISPATCH, bubble_width >= 1, 1 <= max_queues <=
+ * EWSJF_MAX_QUEUES (a set already holding max_queues or more queues gets no
+ * bubbles).  No alignment requirement; one workgroup, no workspace. */
+ewsjf_status ewsjf_dispatch(const int32_t* len, const float* arrival, int64_t n, void* table, int32_t bubble_width,
+                            int32_t max_queues, int32_t* qid, hipStream_t stream);
 
 /* Dynamic Queue Routing: qid[i] = queue of len[i], or -1 for len[i] <= 0.
  * len, qid: device int32 [n]. */

@@ -12,7 +12,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "libewsjf.so")
 
 OK, ERR_NULL, ERR_ARG, ERR_WORKSPACE, ERR_LAUNCH, ERR_ALIGN, ERR_DEVICE = 0, -1, -2, -3, -4, -5, -6
-MAX_QUEUES, MAX_LEN, MAX_B, MAX_THETA = 256, 32768, 4096, 1024
+MAX_QUEUES, MAX_LEN, MAX_B, MAX_THETA, MAX_DISPATCH = 256, 32768, 4096, 1024, 4096
 INIT_EQUAL_WIDTH, INIT_KMEANS3 = 0, 1
 GAPS_DISTINCT, GAPS_MULTISET = 0, 1
 STEP_TOMBSTONE = 1
@@ -21,7 +21,7 @@ OP_PARTITION, OP_SELECT, OP_STEP, OP_TACTICAL = 0, 1, 2, 3
 EXPORTED = ("ewsjf_queue_table_bytes", "ewsjf_workspace_bytes", "ewsjf_table_upload", "ewsjf_partition",
             "ewsjf_route", "ewsjf_score", "ewsjf_select", "ewsjf_step", "ewsjf_step_timed", "ewsjf_ring_insert",
             "ewsjf_tactical_step", "ewsjf_ring_step", "ewsjf_window_histogram", "ewsjf_window_advance",
-            "ewsjf_partition_hist", "ewsjf_status_string", "ewsjf_version")
+            "ewsjf_partition_hist", "ewsjf_dispatch", "ewsjf_status_string", "ewsjf_version")
 
 
 class PartitionParams(C.Structure):
@@ -36,7 +36,7 @@ class Cost(C.Structure):
 
 class QueueTable(C.Structure):
     _fields_ = [("k", C.c_int32), ("max_len", C.c_int32), ("n_distinct", C.c_int32), ("n_coarse", C.c_int32),
-                ("n_leaves", C.c_int32), ("reserved0", C.c_int32), ("n_window", C.c_int64),
+                ("n_leaves", C.c_int32), ("gapped", C.c_int32), ("n_window", C.c_int64),
                 ("bounds", C.c_int32 * MAX_QUEUES), ("lo", C.c_int32 * MAX_QUEUES),
                 ("hi", C.c_int32 * MAX_QUEUES), ("count", C.c_int64 * MAX_QUEUES),
                 ("sum", C.c_int64 * MAX_QUEUES), ("mean", C.c_double * MAX_QUEUES),
@@ -91,6 +91,8 @@ def lib():
         L.ewsjf_window_histogram.restype = C.c_int
         L.ewsjf_window_advance.argtypes = [vp, i64, i64, i64, i64, i32, vp, vp]
         L.ewsjf_window_advance.restype = C.c_int
+        L.ewsjf_dispatch.argtypes = [vp, vp, i64, vp, i32, i32, vp, vp]
+        L.ewsjf_dispatch.restype = C.c_int
         L.ewsjf_partition_hist.argtypes = [vp, C.POINTER(PartitionParams), vp, vp, sz, vp]
         L.ewsjf_partition_hist.restype = C.c_int
         L.ewsjf_status_string.argtypes = [C.c_int]

@@ -106,10 +106,15 @@ ewsjf_status ewsjf_table_upload(const ewsjf_queue_table* host_table, void* table
   }
   for (int i = 0; i < h.k; ++i)
     if (!std::isfinite(h.mean[i])) return EWSJF_ERR_ARG;
+  if (h.gapped != 0 && h.gapped != 1) return EWSJF_ERR_ARG;
+  if (h.gapped)
+    for (int i = 0; i < h.k; ++i)
+      if (h.lo[i] < 1 || h.hi[i] < h.lo[i] || h.hi[i] > h.max_len || (i > 0 && h.lo[i] <= h.hi[i - 1]))
+        return EWSJF_ERR_ARG;
   const ewsjf_status ds = check_device();
   if (ds != EWSJF_OK) return ds;
   std::unique_ptr<ewsjf_queue_table> copy(new ewsjf_queue_table(h));
-  copy->n_distinct = copy->n_coarse = copy->n_leaves = copy->reserved0 = 0;
+  copy->n_distinct = copy->n_coarse = copy->n_leaves = 0;
   const size_t head = offsetof(ewsjf_queue_table, lut);
   if (hipMemcpyAsync(table, copy.get(), head, hipMemcpyHostToDevice, stream) != hipSuccess) return EWSJF_ERR_LAUNCH;
   if (ewsjf::launch_build_lut(static_cast<ewsjf_queue_table*>(table), stream) != hipSuccess)
@@ -180,6 +185,17 @@ ewsjf_status ewsjf_partition_hist(const uint32_t* hist, const ewsjf_partition_pa
   const ewsjf_status ds = check_device();
   if (ds != EWSJF_OK) return ds;
   return launched(ewsjf::launch_partition_hist(hist, *p, static_cast<ewsjf_queue_table*>(table), ws, stream));
+}
+
+ewsjf_status ewsjf_dispatch(const int32_t* len, const float* arrival, int64_t n, void* table, int32_t bubble_width,
+                            int32_t max_queues, int32_t* qid, hipStream_t stream) {
+  if (table == nullptr || (n > 0 && (len == nullptr || arrival == nullptr || qid == nullptr))) return EWSJF_ERR_NULL;
+  if (n < 0 || n > EWSJF_MAX_DISPATCH || bubble_width < 1 || max_queues < 1 || max_queues > EWSJF_MAX_QUEUES)
+    return EWSJF_ERR_ARG;
+  const ewsjf_status ds = check_device();
+  if (ds != EWSJF_OK) return ds;
+  return launched(ewsjf::launch_dispatch(len, arrival, (int)n, static_cast<ewsjf_queue_table*>(table), bubble_width,
+                                         max_queues, qid, stream));
 }
 
 ewsjf_status ewsjf_route(const int32_t* len, int64_t n, const void* table, int32_t* qid, hipStream_t stream) {

@@ -91,6 +91,10 @@ hipError_t launch_ring_insert(int32_t* ring_len, float* ring_arrival, int64_t ca
                               int64_t window_cap, int64_t wpos, const int32_t* new_len, const float* new_arrival,
                               int64_t n, hipStream_t stream);
 
+// Dispatcher with on-demand bubble queues (n <= EWSJF_MAX_DISPATCH).
+hipError_t launch_dispatch(const int32_t* len, const float* arrival, int n, ewsjf_queue_table* table,
+                           int32_t bubble_width, int32_t max_queues, int32_t* qid, hipStream_t stream);
+
 // Refine-and-Prune.
 size_t partition_ws_bytes(int64_t n_window, const ewsjf_partition_params& p);
 hipError_t launch_partition(const int32_t* window, int64_t n_window, const ewsjf_partition_params& p,

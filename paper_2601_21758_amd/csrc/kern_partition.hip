@@ -480,7 +480,7 @@ __global__ __launch_bounds__(kBlock) void rp_refine_prune(PartWs w, ewsjf_partit
       w.meta[3] = 0;
       tab->k = 1;
       tab->max_len = L;
-      tab->n_distinct = tab->n_coarse = tab->n_leaves = tab->reserved0 = 0;
+      tab->n_distinct = tab->n_coarse = tab->n_leaves = tab->gapped = 0;
       tab->n_window = 0;
       tab->lo[0] = tab->hi[0] = 0;
       tab->count[0] = tab->sum[0] = 0;
@@ -601,7 +601,7 @@ __global__ __launch_bounds__(kBlock) void rp_refine_prune(PartWs w, ewsjf_partit
     tab->n_distinct = V;
     tab->n_coarse = n_coarse;
     tab->n_leaves = n_leaves;
-    tab->reserved0 = 0;
+    tab->gapped = 0;
     tab->n_window = n_window >= 0 ? n_window : w.PN[V];
   }
   // Within the queue budget: the leaves are the queues.  Otherwise Stage 3

@@ -4,27 +4,19 @@
 
 #include "ewsjf_device.h"
 #include "ewsjf_launch.h"
+#include "ewsjf_lut.h"
 
 namespace ewsjf {
 
-// lut[b] = number of bounds <= b, i.e. the queue holding length b (contiguous
-// cover of the length axis; Section 3.2 Dispatcher).
+// lut[b] = the queue holding length b under the table's reading: the number
+// of bounds <= b (contiguous cover; Section 3.2 Dispatcher), or the gapped
+// rule of lo/hi (Section 4.3).
 __global__ void build_lut_kernel(ewsjf_queue_table* tab) {
   const int L = tab->max_len;
-  const int nb = tab->k - 1;
-  for (int b = blockIdx.x * blockDim.x + threadIdx.x; b < kLutBytes; b += gridDim.x * blockDim.x) {
-    int q = 0;
-    if (b >= 1 && b <= L) {
-      int lo = 0, hi = nb;  // first index with bounds[i] > b
-      while (lo < hi) {
-        const int mid = (lo + hi) >> 1;
-        if (tab->bounds[mid] <= b) lo = mid + 1;
-        else hi = mid;
-      }
-      q = lo;
-    }
-    tab->lut[b] = (uint8_t)q;
-  }
+  const int k = tab->k;
+  const bool gapped = tab->gapped != 0;
+  for (int b = blockIdx.x * blockDim.x + threadIdx.x; b < kLutBytes; b += gridDim.x * blockDim.x)
+    tab->lut[b] = lut_entry(b, L, gapped, tab->bounds, tab->lo, tab->hi, k);
 }
 
 hipError_t launch_build_lut(ewsjf_queue_table* table, hipStream_t stream) {

@@ -26,6 +26,7 @@
 
 #include "ewsjf_device.h"
 #include "ewsjf_launch.h"
+#include "ewsjf_lut.h"
 
 namespace ewsjf {
 namespace {
@@ -375,22 +376,11 @@ __global__ __launch_bounds__(kBlock) void tac_finish(const TacticalPlan* __restr
     empty_cnt[tid] = qec[tid];
   }
   if (tid == 0) tab->k = k2;
-  // Routing lut of the new bounds: the queue of length b is the number of
-  // bounds <= b.
+  // Routing lut of the new set, in the table's reading (contiguous bounds or
+  // gapped intervals).
   const int L = tab->max_len;
-  for (int b = tid; b < kLutBytes; b += kBlock) {
-    int q = 0;
-    if (b >= 1 && b <= L) {
-      int lo = 0, hi = k2 - 1;  // first i with qb[i] > b
-      while (lo < hi) {
-        const int mid = (lo + hi) >> 1;
-        if (qb[mid] <= b) lo = mid + 1;
-        else hi = mid;
-      }
-      q = lo;
-    }
-    tab->lut[b] = (uint8_t)q;
-  }
+  const bool gapped = tab->gapped != 0;
+  for (int b = tid; b < kLutBytes; b += kBlock) tab->lut[b] = lut_entry(b, L, gapped, qb, qlo, qhi, k2);
 }
 
 }  // namespace

@@ -129,16 +129,31 @@ def partition_hist(hist: torch.Tensor, p: L.PartitionParams, table: torch.Tensor
     return table
 
 
+def dispatch(length: torch.Tensor, arrival: torch.Tensor, table: torch.Tensor, bubble_width: int, max_queues: int,
+             qid: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """The Dispatcher with on-demand bubble queues (ewsjf_dispatch): int32
+    queue of each request in the updated (gapped) table, -1 for empty slots."""
+    _need(length, torch.int32, "length")
+    _need(arrival, torch.float32, "arrival")
+    if arrival.numel() != length.numel():
+        raise ValueError("length and arrival differ in size")
+    qid = qid if qid is not None else torch.empty_like(length)
+    L.check(L.lib().ewsjf_dispatch(_vp(length), _vp(arrival), length.numel(), _vp(table), int(bubble_width),
+                                   int(max_queues), _vp(qid), _stream(stream)), "ewsjf_dispatch")
+    return qid
+
+
 def upload_table(bounds, mean, max_len: int = L.MAX_LEN, lo=None, hi=None, count=None, sum=None,
-                 device=None, stream=None) -> torch.Tensor:
-    """Install a queue structure given on the host (bounds: k-1 ints, mean: k floats)."""
+                 device=None, stream=None, gapped: bool = False) -> torch.Tensor:
+    """Install a queue structure given on the host (bounds: k-1 ints, mean: k
+    floats; gapped: route by the lo/hi intervals)."""
     bounds = np.asarray(bounds, np.int64).reshape(-1)
     mean = np.asarray(mean, np.float64).reshape(-1)
     k = mean.size
     if bounds.size != k - 1:
         raise ValueError("need k-1 bounds for k means")
     h = L.QueueTable()
-    h.k, h.max_len = k, int(max_len)
+    h.k, h.max_len, h.gapped = k, int(max_len), int(bool(gapped))
     for i, b in enumerate(bounds):
         h.bounds[i] = int(b)
     for i in range(k):
@@ -159,7 +174,7 @@ def read_table(table: torch.Tensor) -> dict:
     k = h.k
     return {
         "k": k, "max_len": h.max_len, "n_distinct": h.n_distinct, "n_coarse": h.n_coarse,
-        "n_leaves": h.n_leaves, "n_window": h.n_window,
+        "n_leaves": h.n_leaves, "n_window": h.n_window, "gapped": bool(h.gapped),
         "bounds": np.array(h.bounds[:max(k - 1, 0)], np.int32),
         "lo": np.array(h.lo[:k], np.int32), "hi": np.array(h.hi[:k], np.int32),
         "count": np.array(h.count[:k], np.int64), "sum": np.array(h.sum[:k], np.int64),

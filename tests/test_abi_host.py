@@ -266,6 +266,38 @@ def test_table_upload_argument_errors():
     h.k = 0
     assert lib.ewsjf_table_upload(C.byref(h), FAKE, None) == L.ERR_ARG
     assert lib.ewsjf_table_upload(None, FAKE, None) == L.ERR_NULL
+    # the gapped reading: 0 or 1, intervals in [1, max_len], increasing, disjoint
+    h.k, h.bounds[0], h.bounds[1] = 3, 100, 500
+    for q, (a, b) in enumerate([(10, 50), (100, 300), (500, 900)]):
+        h.lo[q], h.hi[q], h.mean[q] = a, b, (a + b) / 2
+    h.gapped = 2
+    assert lib.ewsjf_table_upload(C.byref(h), FAKE, None) == L.ERR_ARG
+    h.gapped = 1
+    h.hi[1] = 500                        # overlaps the next interval
+    assert lib.ewsjf_table_upload(C.byref(h), FAKE, None) == L.ERR_ARG
+    h.hi[1], h.hi[2] = 300, 1001         # beyond max_len
+    assert lib.ewsjf_table_upload(C.byref(h), FAKE, None) == L.ERR_ARG
+    h.hi[2], h.lo[0] = 900, 0            # below 1
+    assert lib.ewsjf_table_upload(C.byref(h), FAKE, None) == L.ERR_ARG
+    h.lo[0], h.hi[0] = 60, 50            # empty interval
+    assert lib.ewsjf_table_upload(C.byref(h), FAKE, None) == L.ERR_ARG
+
+
+def test_dispatch_argument_errors():
+    lib = L.lib()
+
+    def dsp(length=FAKE, arr=FAKE, n=100, table=FAKE, width=64, mq=32, qid=FAKE):
+        return lib.ewsjf_dispatch(length, arr, n, table, width, mq, qid, None)
+
+    assert dsp(table=None) == L.ERR_NULL
+    assert dsp(length=None) == L.ERR_NULL
+    assert dsp(arr=None) == L.ERR_NULL
+    assert dsp(qid=None) == L.ERR_NULL
+    assert dsp(n=-1) == L.ERR_ARG
+    assert dsp(n=L.MAX_DISPATCH + 1) == L.ERR_ARG
+    assert dsp(width=0) == L.ERR_ARG
+    assert dsp(mq=0) == L.ERR_ARG
+    assert dsp(mq=L.MAX_QUEUES + 1) == L.ERR_ARG
 
 
 def test_valid_call_without_gpu_reports_no_device():

@@ -1,0 +1,228 @@
+"""GPU parity of the Dispatcher with on-demand bubble queues (Algorithm 2,
+ewsjf_dispatch) against the oracle: request queues and the updated table
+bit for bit, the gapped routing lut for every length, state carried across
+calls, and the step, routing and tactical kernels on a gapped table."""
+import json
+import math
+import os
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2601_21758_amd import workloads as W
+from parity_util import check_admission
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+WE6 = json.load(open(os.path.join(HERE, "golden", "we6_bubble.json")))
+COST = (0.01, 1e-4, 0.0)
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def E():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2601_21758_amd import ewsjf
+    ewsjf.table_bytes()  # loads libewsjf.so or raises
+    return ewsjf
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def host(t):
+    return t.detach().cpu().numpy()
+
+
+def upload(E, t: oracle.Table, gapped=None, max_len=32768):
+    return E.upload_table(t.bounds, t.mean, max_len, t.lo, t.hi, t.count, t.sum,
+                          gapped=t.gapped if gapped is None else gapped)
+
+
+def check_table(E, tab, ref: oracle.Table, max_len=32768):
+    g = E.read_table(tab)
+    assert g["k"] == ref.k and g["gapped"] == ref.gapped
+    assert np.array_equal(g["bounds"], ref.bounds), "bounds"
+    assert np.array_equal(g["lo"], ref.lo) and np.array_equal(g["hi"], ref.hi), "intervals"
+    assert np.array_equal(g["count"], ref.count) and np.array_equal(g["sum"], ref.sum), "counts"
+    assert np.array_equal(g["mean"].view(np.uint64), ref.mean.view(np.uint64)), "means"
+    assert np.array_equal(g["lut"][1:], oracle.route(np.arange(1, max_len + 1, dtype=np.int32), ref)), "lut"
+
+
+def table_of(d):
+    lo = np.asarray(d["lo"], np.int32)
+    count = np.asarray(d["count"], np.int64)
+    ssum = np.asarray(d["sum"], np.int64)
+    return oracle.Table(d["k"], lo[1:].copy(), count, ssum, lo, np.asarray(d["hi"], np.int32),
+                        ssum.astype(np.float64) / count)
+
+
+def run(E, length, arrival, t, width, mq, gapped_upload=False):
+    tab = upload(E, t, gapped=gapped_upload)
+    q = E.dispatch(dev(length), dev(arrival), tab, width, mq)
+    rq, rt = oracle.dispatch(length, arrival, t, width, mq)
+    assert np.array_equal(host(q), rq), "request queues differ"
+    check_table(E, tab, rt)
+    return tab, rt
+
+
+@pytest.mark.parametrize("sc", WE6["scenarios"], ids=[s["name"] for s in WE6["scenarios"]])
+def test_we6_on_the_gpu(E, sc):
+    say(f"dispatch WE-6 {sc['name']}")
+    arr = np.array([math.nan if x == "nan" else x for x in sc["arrival"]], np.float32)
+    length = np.asarray(WE6["len"], np.int32)
+    tab = upload(E, table_of(WE6["table"]))
+    q = E.dispatch(dev(length), dev(arr), tab, WE6["bubble_width"], sc["max_queues"])
+    assert host(q).tolist() == sc["expected_qid"]
+    g = E.read_table(tab)
+    exp = sc["expected_table"]
+    assert g["k"] == exp["k"] and g["gapped"]
+    assert g["lo"].tolist() == exp["lo"] and g["hi"].tolist() == exp["hi"] and g["bounds"].tolist() == exp["bounds"]
+    assert g["count"].tolist() == exp["count"] and g["sum"].tolist() == exp["sum"]
+    assert g["mean"].tolist() == exp["mean"]
+    if sc is WE6["scenarios"][0]:
+        r = WE6["routing"]
+        assert host(E.route(dev(np.asarray(r["len"], np.int32)), tab)).tolist() == r["expected"]
+
+
+def gapped_base(rng, k=12, L=32768):
+    edges = np.sort(rng.choice(np.arange(2, L), 2 * k, replace=False))
+    lo, hi = edges[0::2].astype(np.int32), edges[1::2].astype(np.int32)
+    count = rng.integers(1, 1000, k).astype(np.int64)
+    ssum = np.array([c * ((a + b) // 2) for c, a, b in zip(count, lo, hi)], np.int64)
+    return oracle.Table(k, lo[1:].copy(), count, ssum, lo, hi, ssum.astype(np.float64) / count)
+
+
+def requests(rng, n, L=32768, ties=False, empty=0.05):
+    length = rng.integers(1, L + 50, n).astype(np.int32)
+    length[rng.random(n) < empty] = 0
+    arrival = (rng.integers(0, 40, n) if ties else rng.random(n) * 100).astype(np.float32)
+    arrival[rng.random(n) < 0.02] = np.nan
+    arrival[rng.random(n) < 0.01] = -0.0
+    return length, arrival
+
+
+CASES = [  # (seed, k, n, width, extra queues allowed, arrival ties)
+    (1, 12, 4096, 64, 200, False), (2, 3, 1, 64, 10, False), (3, 20, 17, 7, 5, True), (4, 8, 1000, 1, 256, True),
+    (5, 40, 4096, 1 << 20, 256, False), (6, 100, 3000, 500, 3, False), (7, 1, 500, 64, 10, False),
+    (8, 255, 4096, 16, 1, True), (9, 30, 2049, 40, 0, False),
+]
+
+
+@pytest.mark.parametrize("seed,k,n,width,extra,ties", CASES)
+def test_dispatch_matches_oracle(E, seed, k, n, width, extra, ties):
+    rng = np.random.default_rng(seed)
+    t = gapped_base(rng, k=k)
+    length, arrival = requests(rng, n, ties=ties)
+    mq = min(256, k + extra)
+    say(f"dispatch seed={seed} k={k} n={n} width={width} max_queues={mq}")
+    run(E, length, arrival, t, width, mq, gapped_upload=bool(seed % 2))
+
+
+def test_dispatch_over_a_partitioned_table(E):
+    # the workload's 16-queue policy: the gaps are where no window length fell
+    p = W.config(0)
+    t = oracle.partition(p.window, init_queues=p.init_queues, max_queues=p.max_queues)
+    rng = np.random.default_rng(21)
+    length = rng.choice(p.length[p.length > 0], 4096).astype(np.int32)
+    length[:64] = rng.integers(1, 32768, 64)  # a few novel lengths
+    arrival = rng.random(4096).astype(np.float32) * 50
+    say(f"dispatch over the cfg0 partition k={t.k}")
+    run(E, length, arrival, t, 64, 64)
+
+
+def test_state_carries_across_calls(E):
+    """Five batches in a row on the same device table (bubbles from earlier
+    batches shape later ones), then the same table with no true gaps: the
+    set and lut stay as they are."""
+    rng = np.random.default_rng(31)
+    t = gapped_base(rng, k=10)
+    tab = upload(E, t)
+    ref = t
+    say("dispatch batches")
+    for s in range(5):
+        length, arrival = requests(rng, int(rng.integers(1, 4097)))
+        arrival += 100.0 * s
+        q = E.dispatch(dev(length), dev(arrival), tab, 80, 60)
+        rq, ref = oracle.dispatch(length, arrival, ref, 80, 60)
+        assert np.array_equal(host(q), rq), f"batch {s}"
+        check_table(E, tab, ref)
+    inside = np.concatenate([rng.integers(a, b + 1, 4) for a, b in zip(ref.lo, ref.hi)]).astype(np.int32)[:4096]
+    before = tab.clone()
+    q = E.dispatch(dev(inside), dev(rng.random(inside.size).astype(np.float32)), tab, 80, 60)
+    assert np.array_equal(host(q), oracle.route(inside, ref))
+    assert torch.equal(before, tab)
+
+
+def test_dispatch_of_nothing_converts_the_table(E):
+    p = W.config(0)
+    t = oracle.partition(p.window, init_queues=p.init_queues, max_queues=p.max_queues)
+    tab = upload(E, t)
+    assert not E.read_table(tab)["gapped"]
+    E.dispatch(torch.zeros(0, dtype=torch.int32, device="cuda"), torch.zeros(0, dtype=torch.float32, device="cuda"),
+               tab, 64, 64)
+    t.gapped = True
+    check_table(E, tab, t)
+
+
+@pytest.mark.parametrize("mq", [256, 20])
+def test_one_gap_flooded_with_novel_lengths(E, mq):
+    # 4,096 requests in one wide gap, width-1 bubbles: the 10% tolerances
+    # around each bubble leave room for about 45 of them on this range (the cap
+    # of 256 does not bind); with room for 20 queues it binds and the rest join
+    # the nearer neighbour
+    t = oracle.Table(2, np.array([30000], np.int32), np.array([5, 5], np.int64), np.array([50, 150000], np.int64),
+                     np.array([10, 30000], np.int32), np.array([10, 30000], np.int32), np.array([10.0, 30000.0]))
+    rng = np.random.default_rng(41)
+    length = rng.integers(20, 26000, 4096).astype(np.int32)
+    arrival = rng.random(4096).astype(np.float32)
+    say(f"dispatch flood max_queues={mq}")
+    tab, rt = run(E, length, arrival, t, 1, mq)
+    assert rt.k == 20 if mq == 20 else 30 < rt.k < mq
+
+
+def test_step_route_and_score_on_a_gapped_table(E):
+    rng = np.random.default_rng(51)
+    t = gapped_base(rng, k=24)
+    length, arrival = requests(rng, 4096)
+    tab, rt = run(E, length, arrival, t, 200, 48)
+    p = W.config(0)
+    say("step on a gapped table")
+    assert np.array_equal(host(E.route(dev(p.length), tab)), oracle.route(p.length, rt))
+    th = dev(p.theta)
+    ids, top, nsel = E.step(dev(p.length), dev(p.arrival), p.now, tab, th, p.B)
+    rids, rtop, rnsel, rs = oracle.step(p.length, p.arrival, p.now, rt, p.theta, p.B)
+    check_admission(host(ids)[0], host(top)[0], host(nsel)[0], rids[0], rtop[0], rnsel[0], rs[0])
+
+
+def test_tactical_removal_keeps_the_gapped_reading(E):
+    rng = np.random.default_rng(61)
+    t = gapped_base(rng, k=10, L=5000)
+    length, arrival = requests(rng, 2000, L=5000)
+    tab, rt = run(E, length, arrival, t, 100, 30)
+    # a pool whose lengths lie in three of the queues: the others are empty,
+    # so the step removes them
+    n = 20000
+    live = rng.random(n) < 0.01
+    pick = rng.choice([0, rt.k // 2, rt.k - 1], n)
+    L = np.where(live, rng.integers(rt.lo[pick], rt.hi[pick] + 1), 0).astype(np.int32)
+    A = rng.random(n).astype(np.float32) * 10
+    th = dev(W.THETA_MID.reshape(1, 6))
+    ec = E.new_empty_counters("cuda")
+    say(f"tactical on a gapped table k={rt.k}")
+    ids, nsel, qp, hs, rm = E.tactical_step(dev(L), dev(A), 20.0, tab, th, 64, 0, ec)
+    ref = oracle.tactical_step(L, A, 20.0, rt, np.zeros(rt.k, np.int32), W.THETA_MID, 64, 0, COST)
+    assert ref.removed.any()
+    assert int(host(qp)[0]) == ref.q_prim and int(host(nsel)[0]) == ref.ids.size
+    assert np.array_equal(host(ids)[:ref.ids.size], ref.ids)
+    check_table(E, tab, ref.table)
