@@ -215,6 +215,81 @@ def tactical_bench(hip, pool, table, lens, arrs, steps: int = 50):
             "n_sel": int(got[0]), "q_prim": int(got[1]), "steps": steps}
 
 
+def window_and_dispatch_bench(hip, reps: int = 50):
+    """The sliding-window histogram and the Dispatcher with bubble queues on
+    the streaming workload's shapes: a 65,536-length window in a 131,072-entry
+    length log, 4,096 arrivals per step, its 64-queue partition."""
+    import numpy as np
+    import torch
+
+    from paper_2601_21758_amd import ewsjf as E
+    from paper_2601_21758_amd import workloads as W
+    dev = torch.device("cuda:0")
+    sw = W.Streaming(steps=8)
+    L0, _ = sw.initial_fill()
+    W_, R = sw.window_size, 2 * sw.window_size
+    log = torch.zeros(R, dtype=torch.int32, device=dev)
+    log[:W_] = torch.from_numpy(L0[-W_:]).to(dev)
+    arr = [sw.arrivals(i) for i in range(8)]
+    for i, (ln, _) in enumerate(arr):
+        log[W_ + i * sw.per_step:W_ + (i + 1) * sw.per_step] = torch.from_numpy(ln).to(dev)
+    prm = E.params(init_queues=sw.K, max_queues=sw.K)
+    hist = E.window_histogram(log, prm.max_len, begin=0, n=W_)
+    ws = E.Workspace(dev)
+    table = E.partition_hist(hist, prm, ws=ws)
+    torch.cuda.synchronize()
+    s = torch.cuda.current_stream()
+
+    def timed(fn, prep=None):
+        tot = 0.0
+        e0, e1 = hip.event(), hip.event()
+        for _ in range(reps):
+            if prep is not None:
+                prep()
+            hip.rt.hipEventRecord(e0, C.c_void_p(s.cuda_stream))
+            fn()
+            hip.rt.hipEventRecord(e1, C.c_void_p(s.cuda_stream))
+            hip.rt.hipEventSynchronize(e1)
+            tot += hip.elapsed_ms(e0, e1)
+        return tot / reps * 1e3
+
+    h2 = hist.clone()
+    out = {"recount_us": timed(lambda: E.window_histogram(log, prm.max_len, hist=h2, begin=0, n=W_))}
+    for n in (sw.per_step, 8 * sw.per_step):
+        h3 = hist.clone()
+        out[f"advance_{n}_us"] = timed(lambda: E.window_advance(log, W_, 0, n, h3), prep=lambda: h3.copy_(hist))
+    t2 = E.new_table(dev)
+    out["partition_from_histogram_us"] = timed(lambda: E.partition_hist(hist, prm, table=t2, ws=ws))
+    # the Dispatcher over one step's arrivals.  Steady state: the table is in
+    # its gapped reading already and the arrivals open no new queue (the set
+    # and lut stay as they are).  Bubbles: 5% of the arrivals have novel
+    # lengths; the table is restored before each call, so every call opens
+    # bubbles and rebuilds the lut.  First conversion of a fresh partition:
+    # no arrivals, the lut rebuilt in the gapped reading.
+    rng = np.random.default_rng(7)
+    ln, an = arr[0]
+    novel = np.where(rng.random(ln.size) < 0.05, rng.integers(1, 32769, ln.size), ln).astype(np.int32)
+    qid = torch.empty(ln.size, dtype=torch.int32, device=dev)
+    dl, da, dn = (torch.from_numpy(x).to(dev) for x in (ln, an, novel))
+    empty_l = torch.zeros(0, dtype=torch.int32, device=dev)
+    empty_a = torch.zeros(0, dtype=torch.float32, device=dev)
+    work = table.clone()
+    out["dispatch_convert_us"] = timed(lambda: E.dispatch(empty_l, empty_a, work, 64, 128),
+                                       prep=lambda: work.copy_(table))
+    E.dispatch(dl, da, work, 64, 128, qid=qid)  # converts and opens whatever these arrivals open
+    steady = E.read_table(work)["k"]
+    out["dispatch_steady_us"] = timed(lambda: E.dispatch(dl, da, work, 64, 128, qid=qid))
+    if E.read_table(work)["k"] != steady:
+        raise RuntimeError("repeated arrivals opened new queues")
+    saved = work.clone()
+    out["dispatch_novel_5pct_us"] = timed(lambda: E.dispatch(dn, da, work, 64, 128, qid=qid),
+                                          prep=lambda: work.copy_(saved))
+    out["bubbles_created_novel_5pct"] = int(E.read_table(work)["k"]) - int(steady)
+    out["workload"] = ("streaming_drift_1m shapes: 65,536-length window in a 131,072-entry length log, 4,096 "
+                       "arrivals per step, 64-queue partition; dispatch with bubble width 64, at most 128 queues")
+    return out
+
+
 def streaming_bench(steps: int):
     """Config-4 shape: per-step device latency of the streaming scheduler."""
     import numpy as np
@@ -450,6 +525,7 @@ def main() -> int:
         out["tactical"] = tactical_bench(hip, pool, table, lens, arrs)
         out["batched_theta"] = batched_theta_bench(hip)
         out["streaming"] = streaming_bench(args.stream_steps)
+        out["window_and_dispatch"] = window_and_dispatch_bench(hip)
     if not args.no_cpu:
         import oracle
         ref_table = oracle.partition(pool.window, init_queues=pool.init_queues, max_queues=pool.max_queues)

@@ -60,4 +60,51 @@ __device__ __forceinline__ uint8_t lut_entry(int e, int L, bool gapped, P bounds
   return (uint8_t)(gapped ? lut_gapped(e, lo, hi, k) : count_le(bounds, k - 1, e));
 }
 
+constexpr int kLutWords = (EWSJF_MAX_LEN + 16) / 4;
+
+// Thread t of nthreads writes its share of the lut's 32-bit words: one
+// search places its first length, then the walk up the length axis moves to
+// the next queue start (or bound) as it is passed, and four entries go out
+// per store.  The same entries as lut_entry.
+template <class P>
+__device__ void lut_fill(uint8_t* lut, int t, int nthreads, int L, bool gapped, P bounds, P lo, P hi, int k) {
+  const int per = (kLutWords + nthreads - 1) / nthreads;
+  const int w0 = t * per, w1 = min(kLutWords, w0 + per);
+  if (w0 >= w1) return;
+  const int big = 0x7fffffff;
+  const int b0 = max(4 * w0, 1);
+  // gapped: i = last queue starting at or below the length, nxt = the next start;
+  // contiguous: i = bounds passed, nxt = the next bound
+  int i = gapped ? count_le(lo, k, b0) - 1 : count_le(bounds, k - 1, b0);
+  int hi_i = gapped && i >= 0 ? hi[i] : 0;
+  int nxt = gapped ? (i + 1 < k ? lo[i + 1] : big) : (i < k - 1 ? bounds[i] : big);
+  for (int w = w0; w < w1; ++w) {
+    uint32_t word = 0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int x = 4 * w + j;
+      int q = 0;
+      if (x >= 1 && x <= L) {
+        if (x >= nxt) {  // starts and bounds strictly increase, so at most one per length
+          ++i;
+          if (gapped) {
+            hi_i = hi[i];
+            nxt = i + 1 < k ? lo[i + 1] : big;
+          } else {
+            nxt = i < k - 1 ? bounds[i] : big;
+          }
+        }
+        if (!gapped || i < 0 || x <= hi_i || i == k - 1) {
+          q = i < 0 ? 0 : i;
+        } else {
+          const int tq = gap_tolerance(x, hi_i, nxt, i);
+          q = tq >= 0 ? tq : gap_nearer(x, hi_i, nxt, i);
+        }
+      }
+      word |= (uint32_t)q << (8 * j);
+    }
+    *reinterpret_cast<uint32_t*>(lut + 4 * w) = word;
+  }
+}
+
 }  // namespace ewsjf

@@ -200,7 +200,7 @@ __global__ __launch_bounds__(kBlock) void dispatch_kernel(const int32_t* __restr
     tab->k = k1;
     tab->gapped = 1;
   }
-  for (int e = tid; e < kLutBytes; e += kBlock) tab->lut[e] = lut_entry(e, L, true, sm.lo, sm.lo, sm.hi, k1);
+  lut_fill(tab->lut, tid, kBlock, L, true, sm.lo, sm.lo, sm.hi, k1);
 }
 
 }  // namespace

@@ -11,16 +11,14 @@ namespace ewsjf {
 // lut[b] = the queue holding length b under the table's reading: the number
 // of bounds <= b (contiguous cover; Section 3.2 Dispatcher), or the gapped
 // rule of lo/hi (Section 4.3).
-__global__ void build_lut_kernel(ewsjf_queue_table* tab) {
-  const int L = tab->max_len;
-  const int k = tab->k;
-  const bool gapped = tab->gapped != 0;
-  for (int b = blockIdx.x * blockDim.x + threadIdx.x; b < kLutBytes; b += gridDim.x * blockDim.x)
-    tab->lut[b] = lut_entry(b, L, gapped, tab->bounds, tab->lo, tab->hi, k);
+__global__ __launch_bounds__(256) void build_lut_kernel(ewsjf_queue_table* tab) {
+  const int t = blockIdx.x * blockDim.x + threadIdx.x;
+  lut_fill(tab->lut, t, gridDim.x * blockDim.x, tab->max_len, tab->gapped != 0, tab->bounds, tab->lo, tab->hi,
+           tab->k);
 }
 
 hipError_t launch_build_lut(ewsjf_queue_table* table, hipStream_t stream) {
-  hipLaunchKernelGGL(build_lut_kernel, dim3((kLutBytes + 255) / 256), dim3(256), 0, stream, table);
+  hipLaunchKernelGGL(build_lut_kernel, dim3(8), dim3(256), 0, stream, table);  // 4 words per thread
   return hipGetLastError();
 }
 

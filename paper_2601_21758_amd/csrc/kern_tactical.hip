@@ -380,7 +380,7 @@ __global__ __launch_bounds__(kBlock) void tac_finish(const TacticalPlan* __restr
   // gapped intervals).
   const int L = tab->max_len;
   const bool gapped = tab->gapped != 0;
-  for (int b = tid; b < kLutBytes; b += kBlock) tab->lut[b] = lut_entry(b, L, gapped, qb, qlo, qhi, k2);
+  lut_fill(tab->lut, tid, kBlock, L, gapped, qb, qlo, qhi, k2);
 }
 
 }  // namespace

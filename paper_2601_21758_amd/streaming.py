@@ -23,9 +23,16 @@ their multiplicities).  The new table takes effect at step s + 1.  A step
 whose log writes would overwrite entries a queued side-stream read still
 needs waits for that read first.
 
+With bubbles=(width, max_queues), the Dispatcher's on-demand bubble queues
+(Section 4.3, Algorithm 2) place each step's arrivals in the table the step
+is about to use (the new one, at a hand-over) before the step, so an arrival
+in a gap between queues can open a queue of its own until the next
+repartition replaces the set.
+
 Every step runs in libewsjf.so's kernels: ewsjf_ring_step (or
-ewsjf_ring_insert and ewsjf_step) on the caller's stream; ewsjf_window_advance
-or ewsjf_window_histogram, then ewsjf_partition_hist, on the side stream.
+ewsjf_ring_insert and ewsjf_step), and ewsjf_dispatch with bubbles, on the
+caller's stream; ewsjf_window_advance or ewsjf_window_histogram, then
+ewsjf_partition_hist, on the side stream.
 """
 from __future__ import annotations
 
@@ -50,11 +57,14 @@ class StreamingScheduler:
     vector (6 floats); cost: (c0, c1, c2); incremental: move the window's
     histogram forward when the log allows it (False: recount the window at
     every repartition); log_capacity: length-log entries (default 2 *
-    window).
+    window); bubbles: (bubble_width, max_queues) to dispatch each step's
+    arrivals with on-demand bubble queues (ewsjf_dispatch) into the table the
+    step uses, before the step (None: the table's contiguous routing).
     """
 
     def __init__(self, capacity: int, window: int, B: int, params: L.PartitionParams, theta, cost=ewsjf.DEFAULT_COST,
-                 device="cuda", incremental: bool = True, log_capacity: int | None = None):
+                 device="cuda", incremental: bool = True, log_capacity: int | None = None,
+                 bubbles: tuple[int, int] | None = None):
         if capacity <= 0 or window <= 0 or window > capacity:
             raise ValueError("need 0 < window <= capacity")
         log_capacity = 2 * int(window) if log_capacity is None else int(log_capacity)
@@ -85,6 +95,9 @@ class StreamingScheduler:
         self.read_lo = None    # oldest log entry a queued side-stream read still needs
         self.read_done = None  # event after that read
         self.advanced = 0      # repartitions that moved the histogram (the rest recounted the window)
+        self.bubbles = None if bubbles is None else (int(bubbles[0]), int(bubbles[1]))
+        self.undispatched = []  # (length, arrival) inserted since the last step, in order
+        self.qid = torch.empty(L.MAX_DISPATCH, dtype=torch.int32, device=self.device)
 
     # -- state ----------------------------------------------------------------
     def table(self) -> torch.Tensor:
@@ -140,6 +153,17 @@ class StreamingScheduler:
         ewsjf.ring_insert(self.len, self.arr, self.ring_pos, length, arrival, window=self.log, wpos=wpos)
         self.ring_pos = (self.ring_pos + n) % self.capacity
         self.head += n
+        if self.bubbles is not None:
+            self.undispatched.append((length, arrival))
+
+    def _dispatch(self, batches) -> None:
+        """Arrivals through the Dispatcher with bubble queues into the current
+        table, batch by batch in arrival order."""
+        width, mq = self.bubbles
+        for length, arrival in batches:
+            for a in range(0, length.numel(), L.MAX_DISPATCH):
+                b = min(length.numel(), a + L.MAX_DISPATCH)
+                ewsjf.dispatch(length[a:b], arrival[a:b], self.tables[self.cur], width, mq, qid=self.qid[:b - a])
 
     def launch_repartition(self) -> None:
         """Partition the window as of the last step on the side stream; the
@@ -180,6 +204,11 @@ class StreamingScheduler:
             main.wait_event(self.pending)
             self.cur = 1 - self.cur
             self.pending = None
+        if self.bubbles is not None:
+            batches, self.undispatched = self.undispatched, []
+            if length is not None:
+                batches.append((length, arrival))
+            self._dispatch(batches)
         if length is None:
             return ewsjf.step(self.len, self.arr, now, self.tables[self.cur], self.theta, self.B, self.cost,
                               tombstone=tombstone, out=self.out, ws=self.ws_step)

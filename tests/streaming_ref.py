@@ -9,7 +9,8 @@ import oracle
 
 
 class OracleStream:
-    def __init__(self, capacity: int, window: int, B: int, init_queues: int, max_queues: int, theta, cost):
+    def __init__(self, capacity: int, window: int, B: int, init_queues: int, max_queues: int, theta, cost,
+                 bubbles=None):
         self.capacity, self.window, self.B = capacity, window, B
         self.kw = dict(init_queues=init_queues, max_queues=max_queues)
         self.theta = np.asarray(theta, np.float32).reshape(1, 6)
@@ -21,6 +22,9 @@ class OracleStream:
         self.win_pos = 0
         self.table = None
         self.next_table = None
+        self.bubbles = bubbles  # (width, max_queues): arrivals dispatched before each step (Algorithm 2)
+        self.undispatched = []
+        self.created = 0  # bubble queues created so far
 
     def fill(self, length, arrival):
         self.len[:] = length
@@ -39,6 +43,8 @@ class OracleStream:
         self.win[wslots] = length
         self.ring_pos = (self.ring_pos + n) % self.capacity
         self.win_pos = (self.win_pos + n) % self.window
+        if self.bubbles is not None:
+            self.undispatched.append((np.asarray(length, np.int32), np.asarray(arrival, np.float32)))
 
     def repartition(self):
         self.next_table = oracle.partition(self.win, **self.kw)
@@ -50,6 +56,11 @@ class OracleStream:
         step) takes effect here first."""
         if self.next_table is not None:
             self.table, self.next_table = self.next_table, None
+        for length, arrival in self.undispatched:
+            k0 = self.table.k
+            _, self.table = oracle.dispatch(length, arrival, self.table, *self.bubbles)
+            self.created += self.table.k - k0
+        self.undispatched = []
         ids, top, nsel, sc = oracle.step(self.len, self.arr, now, self.table, self.theta, self.B, self.cost)
         return ids[0], top[0], int(nsel[0]), sc[0]
 

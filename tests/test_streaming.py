@@ -70,20 +70,25 @@ def test_constructor_rejects_window_larger_than_ring():
 
 # ---- lockstep parity on the GPU ---------------------------------------------------
 def _lockstep(capacity, per_step, steps, window, rp_every, B, K, label, tombstone_check_every=0, fused=False,
-              incremental=True):
+              incremental=True, bubbles=None, novel=0.0):
     from paper_2601_21758_amd import ewsjf
     s = W.Streaming(seed=4, capacity=capacity, per_step=per_step, steps=steps, window=window, rp_every=rp_every,
                     B=B, K=K)
     prm = ewsjf.params(init_queues=K, max_queues=K)
-    gpu = StreamingScheduler(capacity, window, B, prm, s.theta[0], s.cost, incremental=incremental)
-    ref = OracleStream(capacity, window, B, K, K, s.theta, s.cost)
+    gpu = StreamingScheduler(capacity, window, B, prm, s.theta[0], s.cost, incremental=incremental, bubbles=bubbles)
+    ref = OracleStream(capacity, window, B, K, K, s.theta, s.cost, bubbles=bubbles)
     L0, A0 = s.initial_fill()
     gpu.fill(L0, A0)
     ref.fill(L0, A0)
     check_table(ewsjf.read_table(gpu.table()), ref.table)
     near = 0
+    grown = 0
+    novel_rng = np.random.default_rng(99)
     for step in range(steps):
         L, A = s.arrivals(step)
+        if novel:  # a fraction of the arrivals are of lengths the window has not seen
+            pick = novel_rng.random(L.size) < novel
+            L = np.where(pick, novel_rng.integers(1, 32769, L.size), L).astype(np.int32)
         Lg, Ag = torch.from_numpy(L).cuda(), torch.from_numpy(A).cuda()
         ref.insert(L, A)
         now = float(A[-1])
@@ -103,6 +108,10 @@ def _lockstep(capacity, per_step, steps, window, rp_every, B, K, label, tombston
         near += check_admission(gi, top.cpu().numpy()[0], nsel.cpu().numpy()[0], rids, rtop, rnsel, rsc)
         if step % rp_every == 0:
             check_table(ewsjf.read_table(gpu.table()), rt)
+        if bubbles is not None:
+            g = ewsjf.read_table(gpu.tables[gpu.cur])
+            assert g["k"] == ref.table.k and np.array_equal(g["lo"], ref.table.lo), f"{label}: bubbles differ"
+            assert np.array_equal(g["hi"], ref.table.hi) and g["gapped"]
         if tomb:
             # the step tombstoned its own admitted set; restore the slots the
             # oracle did not admit (near-ties only) before applying the oracle's
@@ -118,6 +127,9 @@ def _lockstep(capacity, per_step, steps, window, rp_every, B, K, label, tombston
             print(f"{label}: step {step} ok (near-tie differences so far {near})", flush=True)
     assert np.array_equal(gpu.arr.cpu().numpy(), ref.arr)
     assert np.array_equal(np.sort(gpu.window_lengths().cpu().numpy()), np.sort(ref.win)), f"{label}: window differs"
+    if bubbles is not None:
+        print(f"{label}: bubble queues created {ref.created}", flush=True)
+        assert ref.created > 0, f"{label}: no bubble queue was created"
     return near, gpu
 
 
@@ -158,6 +170,16 @@ def test_streaming_lockstep_fused_insert():
               tombstone_check_every=2, fused=True)
     _lockstep(capacity=1 << 16, per_step=700, steps=60, window=8192, rp_every=10, B=64, K=16, label="fused",
               tombstone_check_every=5, fused=True)
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("fused", [True, False])
+def test_streaming_lockstep_with_bubble_queues(fused):
+    # every step's arrivals go through the Dispatcher (Algorithm 2) before the
+    # step; long arrivals in the gaps of the sparse tail open bubble queues
+    # that the next partition replaces
+    _lockstep(capacity=1 << 14, per_step=300, steps=60, window=512, rp_every=15, B=64, K=64, label="bubbles",
+              tombstone_check_every=4, fused=fused, bubbles=(64, 128), novel=0.05)
 
 
 @pytest.mark.gpu
