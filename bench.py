@@ -15,14 +15,17 @@ launch cost does not bound the loop; an eager pass with per-kernel events
 gives each kernel's own duration (start/end events bound to the kernel's
 dispatch) for the roofline figure.
 
-Three more workloads ride along in the same JSON line (skip them with
+More workloads ride along in the same JSON line (skip them with
 --no-extra): "tactical" -- Algorithm 1's own batch rule on the same 4M pool
 (ewsjf_tactical_step); "batched_theta" -- one 1,048,576-request pool scored and
 selected under 256 parameter vectors per step (top-256 each); "streaming"
 -- 10,000 steps of the streaming scheduler (1,048,576-slot ring, 4,096
 arrivals and 512 admissions per step, Refine-and-Prune over the last
 65,536 arrivals every 100 steps on a side stream), per-step device latency
-p50/p99 over steps 100..9,999.
+p50/p99 over steps 100..9,999; "window_and_dispatch" -- the sliding-window
+histogram kernels and the Dispatcher with bubble queues on the streaming
+shapes; "trial" -- trials of 16 scoring-parameter proposals, each on its own
+1,048,576-slot ring with common arrivals (ewsjf_trial_step).
 
 Prints one JSON line.  Flags: --gpus (only 1 is supported), --steps,
 --warmup, --rotate, --no-cpu (skip the oracle baseline), --no-extra,
@@ -290,6 +293,54 @@ def window_and_dispatch_bench(hip, reps: int = 50):
     return out
 
 
+def trial_bench(hip, steps: int = 100, P: int = 16):
+    """Trials of P scoring-parameter proposals on the streaming workload's
+    shapes: every proposal its own 1,048,576-slot ring, 4,096 common arrivals
+    and B=512 admissions per step, the 64-queue partition of the starting
+    window held for the trial."""
+    import numpy as np
+    import torch
+
+    from paper_2601_21758_amd import ewsjf as E
+    from paper_2601_21758_amd import workloads as W
+    from paper_2601_21758_amd.trial import Trial
+    dev = torch.device("cuda:0")
+    sw = W.Streaming(steps=steps)
+    L0, A0 = sw.initial_fill()
+    prm = E.params(init_queues=sw.K, max_queues=sw.K)
+    table = E.partition(torch.from_numpy(L0[-sw.window_size:]).to(dev), prm)
+    rng = np.random.default_rng(11)
+    th = np.tile(W.THETA_MID.reshape(1, 6), (P, 1)).astype(np.float32)
+    th[1:] *= rng.uniform(0.3, 3.0, (P - 1, 6)).astype(np.float32)
+    arr = [sw.arrivals(i) for i in range(steps)]
+    dl = torch.from_numpy(np.stack([a[0] for a in arr])).to(dev)
+    da = torch.from_numpy(np.stack([a[1] for a in arr])).to(dev)
+    nows = [float(a[1][-1]) for a in arr]
+    tr = Trial(sw.capacity, th, sw.B, table, sw.cost, device=dev)
+    tr.start(L0, A0)
+    for i in range(3):  # warm-up steps, then a fresh start
+        tr.step(dl[i], da[i], nows[i])
+    tr.start(L0, A0)
+    torch.cuda.synchronize()
+    s = torch.cuda.current_stream()
+    e0, e1 = hip.event(), hip.event()
+    torch.cuda._sleep(int(2.4e9 * 0.02))
+    hip.rt.hipEventRecord(e0, C.c_void_p(s.cuda_stream))
+    for i in range(steps):
+        tr.step(dl[i], da[i], nows[i])
+    hip.rt.hipEventRecord(e1, C.c_void_p(s.cuda_stream))
+    ms = hip.elapsed_ms(e0, e1) / steps
+    R = tr.finish((1.0, 1.0, 1.0, 1.0)).cpu().numpy()
+    st = tr.stats.cpu().numpy()
+    pool_bytes = 8 * sw.capacity * P
+    return {"workload": f"trial_{P}x1m: {P} scoring-parameter proposals, each on its own 1,048,576-slot ring, "
+                        "4,096 common arrivals and B=512 admissions per step, the 64-queue partition held",
+            "proposals": P, "steps": steps, "ms_per_step": ms, "proposal_steps_per_s": P / (ms * 1e-3),
+            "pool_bytes_per_step": pool_bytes, "hbm_frac_pool_pass": pool_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+            "mean_wait_s": [float(x) for x in st[:, 2] / np.maximum(st[:, 0], 1)],
+            "reward_unit_lambda": [float(x) for x in R], "best_proposal": int(np.argmax(R))}
+
+
 def streaming_bench(steps: int):
     """Config-4 shape: per-step device latency of the streaming scheduler."""
     import numpy as np
@@ -526,6 +577,7 @@ def main() -> int:
         out["batched_theta"] = batched_theta_bench(hip)
         out["streaming"] = streaming_bench(args.stream_steps)
         out["window_and_dispatch"] = window_and_dispatch_bench(hip)
+        out["trial"] = trial_bench(hip)
     if not args.no_cpu:
         import oracle
         ref_table = oracle.partition(pool.window, init_queues=pool.init_queues, max_queues=pool.max_queues)

@@ -7,6 +7,9 @@
  *   ewsjf_partition  Refine-and-Prune: an observation window of prompt lengths
  *                    -> contiguous queue intervals (Section 4.2, Stages 1-3,
  *                    Eq. 2 split test, Eq. 3 scheduling utility).
+ *   ewsjf_trial_step / ewsjf_trial_finish  trials of batched scoring-parameter
+ *                    proposals, each on its own pool with common arrivals, and
+ *                    the Eq. 5 reward of each (the meta-optimizer's evaluator).
  *   ewsjf_dispatch   the Dispatcher with on-demand bubble queues (Section 4.3,
  *                    Algorithm 2): arriving requests in a gap between queues
  *                    join a neighbour within tolerance or create a queue.
@@ -81,7 +84,8 @@ enum {
   EWSJF_MAX_LEN = 32768,     /* cap on the window clamp L */
   EWSJF_MAX_B = 4096,        /* admissions per step per parameter vector */
   EWSJF_MAX_THETA = 1024,    /* parameter vectors per call */
-  EWSJF_MAX_DISPATCH = 4096  /* requests per ewsjf_dispatch call */
+  EWSJF_MAX_DISPATCH = 4096, /* requests per ewsjf_dispatch call */
+  EWSJF_TRIAL_STATS = 8      /* statistics per trial proposal (ewsjf_trial_step) */
 };
 
 /* Stage-1 initializers (Section 4.2, Stage 1). */
@@ -102,7 +106,7 @@ enum {
 };
 
 /* Operations for ewsjf_workspace_bytes(). */
-enum { EWSJF_OP_PARTITION = 0, EWSJF_OP_SELECT = 1, EWSJF_OP_STEP = 2, EWSJF_OP_TACTICAL = 3 };
+enum { EWSJF_OP_PARTITION = 0, EWSJF_OP_SELECT = 1, EWSJF_OP_STEP = 2, EWSJF_OP_TACTICAL = 3, EWSJF_OP_TRIAL = 4 };
 
 /* Refine-and-Prune parameters (host struct).  Section 4.2: Stage 1 picks the
  * initializer; Stage 2 splits at gaps larger than alpha * mean gap (alpha > 1,
@@ -191,6 +195,46 @@ ewsjf_status ewsjf_table_upload(const ewsjf_queue_table* host_table, void* table
  * ewsjf_workspace_bytes(EWSJF_OP_PARTITION, n_window, 0, 0, p) bytes. */
 ewsjf_status ewsjf_partition(const int32_t* window, int64_t n_window, const ewsjf_partition_params* p,
                              void* table, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Trials of scoring-parameter proposals: the simulator side of the
+ * meta-optimizer (Section 4.4.2), which runs each candidate Theta for a trial
+ * interval, collects statistics and scores them with the reward of Eq. 5.
+ * Proposal t has its own pool: slots [t * capacity, (t + 1) * capacity) of
+ * len/arrival (device [n_pools][capacity], 16-byte aligned, capacity a
+ * multiple of 4), and parameter vector theta[t].  One call is one step of the
+ * trial for every proposal: the n_new arrivals go into ring slots (pos + i)
+ * mod capacity of every pool (the same requests for all: common arrivals),
+ * each pool admits its top B under its own vector (as ewsjf_step; ids/top
+ * [n_pools][B], n_sel [n_pools]), then the statistics of the admitted
+ * requests are added to stats[t] (device double [n_pools][EWSJF_TRIAL_STATS]:
+ * 0 admitted, 1 tokens = sum of their prompt lengths, 2 sum and 3 sum of
+ * squares of their waits W = max(0, now - arrival) in seconds (a NaN arrival
+ * waits 0), 4 largest such wait, 7 steps; entries 5 and 6 belong to
+ * ewsjf_trial_finish) and their queues counted in queue_admits (device int64
+ * [n_pools][EWSJF_MAX_QUEUES]), and the admitted slots are emptied.  The
+ * caller zeroes stats and queue_admits at the trial's start; sums are
+ * reduced in a fixed order, so trials are reproducible.  Workspace
+ * ewsjf_workspace_bytes(EWSJF_OP_TRIAL, capacity, n_pools, B, NULL).
+ * 1 <= n_pools <= EWSJF_MAX_THETA, 0 <= pos < capacity, 0 <= n_new <=
+ * capacity, 1 <= B <= EWSJF_MAX_B. */
+ewsjf_status ewsjf_trial_step(int32_t* len, float* arrival, int64_t capacity, int32_t n_pools, int64_t pos,
+                              const int32_t* new_len, const float* new_arrival, int64_t n_new, float now,
+                              const void* table, const ewsjf_theta* theta, const ewsjf_cost* cost, int32_t B,
+                              int32_t* ids, float* top, int32_t* n_sel, double* stats, int64_t* queue_admits,
+                              void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* The end of a trial: stats[t][5] = pending requests of pool t and
+ * stats[t][6] = their largest wait at `now`, and reward[t] (device double
+ * [n_pools]) = Eq. 5, R = lambda[0] C + lambda[1] L - lambda[2] S - lambda[3] U
+ * (lambda: host double [4]), with the terms read as: C (compact, homogeneous
+ * queues) = minus the mean over queues of (hi - lo) / (hi + lo); L (load
+ * imbalance) = minus the coefficient of variation of pool t's admissions per
+ * queue (0 without admissions); S (queue proliferation) = k /
+ * EWSJF_MAX_QUEUES; U (latency) = the mean wait of pool t's admitted requests
+ * (0 without admissions). */
+ewsjf_status ewsjf_trial_finish(const int32_t* len, const float* arrival, int64_t capacity, int32_t n_pools, float now,
+                                const void* table, const int64_t* queue_admits, const double* lambda, double* stats,
+                                double* reward, hipStream_t stream);
 
 /* The Dispatcher with on-demand bubble queues (Section 3.2, Dispatcher;
  * Section 4.3 and the appendix's Algorithm 2): the requests with len > 0 join

@@ -16,12 +16,14 @@ MAX_QUEUES, MAX_LEN, MAX_B, MAX_THETA, MAX_DISPATCH = 256, 32768, 4096, 1024, 40
 INIT_EQUAL_WIDTH, INIT_KMEANS3 = 0, 1
 GAPS_DISTINCT, GAPS_MULTISET = 0, 1
 STEP_TOMBSTONE = 1
-OP_PARTITION, OP_SELECT, OP_STEP, OP_TACTICAL = 0, 1, 2, 3
+OP_PARTITION, OP_SELECT, OP_STEP, OP_TACTICAL, OP_TRIAL = 0, 1, 2, 3, 4
+TRIAL_STATS = 8
 
 EXPORTED = ("ewsjf_queue_table_bytes", "ewsjf_workspace_bytes", "ewsjf_table_upload", "ewsjf_partition",
             "ewsjf_route", "ewsjf_score", "ewsjf_select", "ewsjf_step", "ewsjf_step_timed", "ewsjf_ring_insert",
             "ewsjf_tactical_step", "ewsjf_ring_step", "ewsjf_window_histogram", "ewsjf_window_advance",
-            "ewsjf_partition_hist", "ewsjf_dispatch", "ewsjf_status_string", "ewsjf_version")
+            "ewsjf_partition_hist", "ewsjf_dispatch", "ewsjf_trial_step", "ewsjf_trial_finish",
+            "ewsjf_status_string", "ewsjf_version")
 
 
 class PartitionParams(C.Structure):
@@ -91,6 +93,11 @@ def lib():
         L.ewsjf_window_histogram.restype = C.c_int
         L.ewsjf_window_advance.argtypes = [vp, i64, i64, i64, i64, i32, vp, vp]
         L.ewsjf_window_advance.restype = C.c_int
+        L.ewsjf_trial_step.argtypes = [vp, vp, i64, i32, i64, vp, vp, i64, f32, vp, vp, C.POINTER(Cost), i32, vp, vp,
+                                       vp, vp, vp, vp, sz, vp]
+        L.ewsjf_trial_step.restype = C.c_int
+        L.ewsjf_trial_finish.argtypes = [vp, vp, i64, i32, f32, vp, vp, C.POINTER(C.c_double), vp, vp, vp]
+        L.ewsjf_trial_finish.restype = C.c_int
         L.ewsjf_dispatch.argtypes = [vp, vp, i64, vp, i32, i32, vp, vp]
         L.ewsjf_dispatch.restype = C.c_int
         L.ewsjf_partition_hist.argtypes = [vp, C.POINTER(PartitionParams), vp, vp, sz, vp]

@@ -18,7 +18,7 @@ INC = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libewsjf.so")
 BUILD = os.path.join(PKG, "_build")
 SOURCES = ["abi.hip", "kern_policy.hip", "kern_select.hip", "kern_partition.hip", "kern_tactical.hip",
-           "kern_dispatch.hip"]
+           "kern_dispatch.hip", "kern_trial.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-ffp-contract=off",

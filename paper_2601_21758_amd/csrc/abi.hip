@@ -89,6 +89,10 @@ size_t ewsjf_workspace_bytes(int op, int64_t n, int32_t n_theta, int32_t B, cons
     if (n_theta < 1 || n_theta > EWSJF_MAX_THETA || B < 1 || B > EWSJF_MAX_B) return 0;
     return op == EWSJF_OP_STEP ? ewsjf::plan_step(n, n_theta, B).ws_bytes : ewsjf::plan_select(n, n_theta, B).ws_bytes;
   }
+  if (op == EWSJF_OP_TRIAL) {
+    if (n_theta < 1 || n_theta > EWSJF_MAX_THETA || B < 1 || B > EWSJF_MAX_B) return 0;
+    return ewsjf::plan_trial(n, n_theta, B).ws_bytes;
+  }
   if (op == EWSJF_OP_TACTICAL) {
     if (B < 1 || B > EWSJF_MAX_B) return 0;
     return ewsjf::tactical_ws_bytes(n, B);
@@ -185,6 +189,49 @@ ewsjf_status ewsjf_partition_hist(const uint32_t* hist, const ewsjf_partition_pa
   const ewsjf_status ds = check_device();
   if (ds != EWSJF_OK) return ds;
   return launched(ewsjf::launch_partition_hist(hist, *p, static_cast<ewsjf_queue_table*>(table), ws, stream));
+}
+
+ewsjf_status ewsjf_trial_step(int32_t* len, float* arrival, int64_t capacity, int32_t n_pools, int64_t pos,
+                              const int32_t* new_len, const float* new_arrival, int64_t n_new, float now,
+                              const void* table, const ewsjf_theta* theta, const ewsjf_cost* cost, int32_t B,
+                              int32_t* ids, float* top, int32_t* n_sel, double* stats, int64_t* queue_admits, void* ws,
+                              size_t ws_bytes, hipStream_t stream) {
+  if (len == nullptr || arrival == nullptr || table == nullptr || theta == nullptr || cost == nullptr ||
+      ids == nullptr || top == nullptr || n_sel == nullptr || stats == nullptr || queue_admits == nullptr ||
+      ws == nullptr || (n_new > 0 && (new_len == nullptr || new_arrival == nullptr)))
+    return EWSJF_ERR_NULL;
+  if (capacity < 4 || capacity > kMaxN || capacity % 4 != 0 || n_pools < 1 || n_pools > EWSJF_MAX_THETA ||
+      pos < 0 || pos >= capacity || n_new < 0 || n_new > capacity || B < 1 || B > EWSJF_MAX_B || !cost_ok(cost) ||
+      !std::isfinite(now))
+    return EWSJF_ERR_ARG;
+  if (ws_bytes < ewsjf::plan_trial(capacity, n_pools, B).ws_bytes) return EWSJF_ERR_WORKSPACE;
+  if (!aligned16(len) || !aligned16(arrival) || !aligned16(ws)) return EWSJF_ERR_ALIGN;
+  const ewsjf_status ds = check_device();
+  if (ds != EWSJF_OK) return ds;
+  const auto* tab = static_cast<const ewsjf_queue_table*>(table);
+  const hipError_t e = ewsjf::launch_trial_select(len, arrival, capacity, n_pools, pos, new_len, new_arrival, n_new,
+                                                  now, tab, theta, *cost, B, ids, top, n_sel, ws, stream);
+  if (e != hipSuccess) return EWSJF_ERR_LAUNCH;
+  return launched(ewsjf::launch_trial_stats(len, arrival, capacity, n_pools, now, tab, B, ids, n_sel, stats,
+                                            queue_admits, stream));
+}
+
+ewsjf_status ewsjf_trial_finish(const int32_t* len, const float* arrival, int64_t capacity, int32_t n_pools, float now,
+                                const void* table, const int64_t* queue_admits, const double* lambda, double* stats,
+                                double* reward, hipStream_t stream) {
+  if (len == nullptr || arrival == nullptr || table == nullptr || queue_admits == nullptr || lambda == nullptr ||
+      stats == nullptr || reward == nullptr)
+    return EWSJF_ERR_NULL;
+  if (capacity < 4 || capacity > kMaxN || capacity % 4 != 0 || n_pools < 1 || n_pools > EWSJF_MAX_THETA ||
+      !std::isfinite(now))
+    return EWSJF_ERR_ARG;
+  for (int i = 0; i < 4; ++i)
+    if (!std::isfinite(lambda[i])) return EWSJF_ERR_ARG;
+  const ewsjf_status ds = check_device();
+  if (ds != EWSJF_OK) return ds;
+  return launched(ewsjf::launch_trial_finish(len, arrival, capacity, n_pools, now,
+                                             static_cast<const ewsjf_queue_table*>(table), queue_admits, lambda, stats,
+                                             reward, stream));
 }
 
 ewsjf_status ewsjf_dispatch(const int32_t* len, const float* arrival, int64_t n, void* table, int32_t bubble_width,

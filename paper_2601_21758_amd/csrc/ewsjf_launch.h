@@ -33,7 +33,8 @@ struct CandBufs {
 };
 
 // packed: each workgroup takes a full pass of chunks (the many-vector step).
-SelectPlan plan_select(int64_t n, int32_t n_theta, int32_t B, bool packed = false);
+// max_grid > 0 caps the streaming workgroups per row (default: one per CU).
+SelectPlan plan_select(int64_t n, int32_t n_theta, int32_t B, bool packed = false, int max_grid = 0);
 // The plan ewsjf_step uses: packed for several vectors over a pool that fits
 // one pass per workgroup.
 SelectPlan plan_step(int64_t n, int32_t n_theta, int32_t B);
@@ -61,6 +62,25 @@ hipError_t launch_ring_step(int32_t* ring_len, float* ring_arrival, int64_t capa
                             int64_t n_new, float now, const ewsjf_queue_table* table, const ewsjf_theta* theta,
                             const ewsjf_cost& cost, int32_t B, int32_t* tomb_len, int32_t* ids, float* top,
                             int32_t* n_sel, void* ws, hipStream_t stream);
+
+SelectPlan plan_trial(int64_t capacity, int32_t n_pools, int32_t B);
+// Trials: the step's two kernels over n_pools pools of `capacity` slots
+// (pool t = proposal t, slots [t * capacity, (t + 1) * capacity)), each taking
+// the same arrivals at ring position pos; no tombstones (the statistics
+// kernel reads the admitted requests first).  Workspace plan_trial(capacity,
+// n_pools, B).
+hipError_t launch_trial_select(int32_t* len, float* arrival, int64_t capacity, int32_t n_pools, int64_t pos,
+                               const int32_t* new_len, const float* new_arrival, int64_t n_new, float now,
+                               const ewsjf_queue_table* table, const ewsjf_theta* theta, const ewsjf_cost& cost,
+                               int32_t B, int32_t* ids, float* top, int32_t* n_sel, void* ws, hipStream_t stream);
+// Trial statistics of the admitted requests (then tombstoned), and the
+// trial's end: pending statistics and the reward.
+hipError_t launch_trial_stats(int32_t* len, const float* arrival, int64_t capacity, int32_t n_pools, float now,
+                              const ewsjf_queue_table* table, int32_t B, const int32_t* ids, const int32_t* n_sel,
+                              double* stats, int64_t* queue_admits, hipStream_t stream);
+hipError_t launch_trial_finish(const int32_t* len, const float* arrival, int64_t capacity, int32_t n_pools,
+                               float now, const ewsjf_queue_table* table, const int64_t* queue_admits,
+                               const double* lambda, double* stats, double* reward, hipStream_t stream);
 
 size_t tactical_ws_bytes(int64_t n, int32_t B);
 hipError_t launch_tactical_step(int32_t* len, const float* arrival, int64_t n, float now, ewsjf_queue_table* table,

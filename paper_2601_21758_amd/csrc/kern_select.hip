@@ -279,6 +279,13 @@ struct RingSource : PoolSource {
   }
 };
 
+// Trials of scoring-parameter proposals: row t of the grid is proposal t
+// with its own pool, the t-th block of `stride` slots of every pool array,
+// and every pool takes the same arrivals (bind_theta moves the pointers).
+struct TrialSource : RingSource {
+  int64_t stride;
+};
+
 struct ScoreSource {
   const float* score;  // [n_theta][n]
   int64_t n;
@@ -351,6 +358,16 @@ struct ScoreSource {
 template <class Src>
 __device__ __forceinline__ Src bind_theta(const Src& s, int) {
   return s;
+}
+template <>
+__device__ __forceinline__ TrialSource bind_theta<TrialSource>(const TrialSource& s, int t) {
+  TrialSource r = s;
+  const int64_t o = (int64_t)t * s.stride;
+  r.len += o;
+  r.arrival += o;
+  r.ring_len += o;
+  r.ring_arrival += o;
+  return r;
 }
 template <>
 __device__ __forceinline__ ScoreSource bind_theta<ScoreSource>(const ScoreSource& s, int t) {
@@ -1266,14 +1283,15 @@ __global__ __launch_bounds__(kBlock) void merge_candidates(Src src0, int64_t n, 
 // ---------------------------------------------------------------------------
 // Host-side launch helpers.
 // ---------------------------------------------------------------------------
-SelectPlan plan_select(int64_t n, int32_t n_theta, int32_t B, bool packed) {
+SelectPlan plan_select(int64_t n, int32_t n_theta, int32_t B, bool packed, int max_grid) {
   SelectPlan p;
   const int64_t nchunks = (n + kChunk - 1) / kChunk;
   // Packed: every wave holds all four chunks of its one pass.
   const int64_t per_wg = packed ? (int64_t)kWavesPerBlock * kChunksPerPass : (int64_t)kWavesPerBlock;
   int64_t G = (nchunks + per_wg - 1) / per_wg;
   if (G < 1) G = 1;
-  if (G > kMaxGrid) G = kMaxGrid;
+  const int gmax = max_grid > 0 ? max_grid : kMaxGrid;
+  if (G > gmax) G = gmax;
   p.G = (int)G;
   const int per = (int)((B + p.G - 1) / p.G);
   // Each wave leaves at least 2^lg elements at or above its bar: the largest
@@ -1329,6 +1347,14 @@ static bool step_packed(int64_t n, int32_t n_theta) {
 
 SelectPlan plan_step(int64_t n, int32_t n_theta, int32_t B) {
   return plan_select(n, n_theta, B, step_packed(n, n_theta));
+}
+
+// Trials: each pool gets the workgroups that give every wave one full pass
+// (four chunks in flight), the shape of the 4M-pool step, rather than one per
+// CU and row: a workgroup's table staging and list publication are then paid
+// once per 16,384 requests.
+SelectPlan plan_trial(int64_t capacity, int32_t n_pools, int32_t B) {
+  return plan_select(capacity, n_pools, B, true);
 }
 
 hipError_t launch_step(const int32_t* len, const float* arrival, int64_t n, float now,
@@ -1404,6 +1430,39 @@ hipError_t launch_ring_step(int32_t* ring_len, float* ring_arrival, int64_t capa
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(merge_candidates<RingSource>, dim3(1), dim3(kBlock), 0, stream, src, capacity, p.G, p.M, B, cb,
                      ids, top, n_sel, tomb_len);
+  return hipGetLastError();
+}
+
+hipError_t launch_trial_select(int32_t* len, float* arrival, int64_t capacity, int32_t n_pools, int64_t pos,
+                               const int32_t* new_len, const float* new_arrival, int64_t n_new, float now,
+                               const ewsjf_queue_table* table, const ewsjf_theta* theta, const ewsjf_cost& cost,
+                               int32_t B, int32_t* ids, float* top, int32_t* n_sel, void* ws, hipStream_t stream) {
+  const SelectPlan p = plan_trial(capacity, n_pools, B);
+  const CandBufs cb = carve(p, ws);
+  TrialSource src;
+  src.len = len;
+  src.arrival = arrival;
+  src.table = table;
+  src.theta = theta;
+  src.now = now;
+  src.cost = CostF{(float)cost.c0, (float)cost.c1, (float)cost.c2};
+  src.ring_len = len;
+  src.ring_arrival = arrival;
+  src.capacity = capacity;
+  src.pos = pos;
+  src.window = nullptr;
+  src.window_cap = 0;
+  src.wpos = 0;
+  src.new_len = new_len;
+  src.new_arrival = new_arrival;
+  src.n_new = n_new;
+  src.stride = capacity;
+  hipLaunchKernelGGL(local_candidates<TrialSource>, dim3(p.G, n_pools), dim3(kBlock), 0, stream, src, capacity, p.G,
+                     p.lg, p.M, cb);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(merge_candidates<TrialSource>, dim3(n_pools), dim3(kBlock), 0, stream, src, capacity, p.G, p.M,
+                     B, cb, ids, top, n_sel, nullptr);
   return hipGetLastError();
 }
 

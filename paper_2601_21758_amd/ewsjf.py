@@ -129,6 +129,50 @@ def partition_hist(hist: torch.Tensor, p: L.PartitionParams, table: torch.Tensor
     return table
 
 
+def trial_step(len_pools: torch.Tensor, arr_pools: torch.Tensor, pos: int, new_len: torch.Tensor,
+               new_arrival: torch.Tensor, now: float, table: torch.Tensor, theta: torch.Tensor, B: int,
+               stats: torch.Tensor, queue_admits: torch.Tensor, cost_=DEFAULT_COST, out=None,
+               ws: Workspace | None = None, stream=None):
+    """One step of a trial for every proposal (ewsjf_trial_step): pools are
+    [P][capacity]; stats float64 [P][8] and queue_admits int64 [P][256]
+    accumulate.  Returns (ids[P,B], top[P,B], n_sel[P])."""
+    _need(len_pools, torch.int32, "len_pools")
+    _need(arr_pools, torch.float32, "arr_pools")
+    _need(new_len, torch.int32, "new_len")
+    _need(new_arrival, torch.float32, "new_arrival")
+    _need(stats, torch.float64, "stats")
+    _need(queue_admits, torch.int64, "queue_admits")
+    P, cap = len_pools.shape
+    theta = _theta(theta)
+    if theta.shape[0] != P or stats.shape != (P, L.TRIAL_STATS) or queue_admits.shape != (P, L.MAX_QUEUES):
+        raise ValueError("one parameter vector, one statistics row and one queue row per pool")
+    ids, top, nsel = _outs(P, B, len_pools.device, out)
+    ws = ws or Workspace(len_pools.device)
+    buf = ws.get(workspace_bytes(L.OP_TRIAL, cap, P, B))
+    c = _cost(cost_)
+    L.check(L.lib().ewsjf_trial_step(_vp(len_pools), _vp(arr_pools), cap, P, int(pos), _vp(new_len),
+                                     _vp(new_arrival), new_len.numel(), float(now), _vp(table), _vp(theta),
+                                     C.byref(c), int(B), _vp(ids), _vp(top), _vp(nsel), _vp(stats),
+                                     _vp(queue_admits), _vp(buf), buf.numel(), _stream(stream)), "ewsjf_trial_step")
+    return ids, top, nsel
+
+
+def trial_finish(len_pools: torch.Tensor, arr_pools: torch.Tensor, now: float, table: torch.Tensor,
+                 stats: torch.Tensor, queue_admits: torch.Tensor, lam=(1.0, 1.0, 1.0, 1.0), reward=None,
+                 stream=None) -> torch.Tensor:
+    """The trial's end (ewsjf_trial_finish): pending statistics into stats,
+    Eq. 5 per pool (float64 [P])."""
+    _need(len_pools, torch.int32, "len_pools")
+    _need(arr_pools, torch.float32, "arr_pools")
+    P, cap = len_pools.shape
+    reward = reward if reward is not None else torch.empty(P, dtype=torch.float64, device=len_pools.device)
+    lam_h = (C.c_double * 4)(*[float(x) for x in lam])
+    L.check(L.lib().ewsjf_trial_finish(_vp(len_pools), _vp(arr_pools), cap, P, float(now), _vp(table),
+                                       _vp(queue_admits), lam_h, _vp(stats), _vp(reward), _stream(stream)),
+            "ewsjf_trial_finish")
+    return reward
+
+
 def dispatch(length: torch.Tensor, arrival: torch.Tensor, table: torch.Tensor, bubble_width: int, max_queues: int,
              qid: torch.Tensor | None = None, stream=None) -> torch.Tensor:
     """The Dispatcher with on-demand bubble queues (ewsjf_dispatch): int32

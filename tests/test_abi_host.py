@@ -283,6 +283,40 @@ def test_table_upload_argument_errors():
     assert lib.ewsjf_table_upload(C.byref(h), FAKE, None) == L.ERR_ARG
 
 
+def test_trial_argument_errors():
+    lib = L.lib()
+    c = L.Cost(0.01, 1e-4, 0.0)
+    need = lib.ewsjf_workspace_bytes(L.OP_TRIAL, 1000, 4, 64, None)
+    assert need > 0 and lib.ewsjf_workspace_bytes(L.OP_TRIAL, 1000, 0, 64, None) == 0
+
+    def ts(ln=FAKE, ar=FAKE, cap=1000, P=4, pos=0, nl=FAKE, na=FAKE, n=10, now=1.0, table=FAKE, theta=FAKE, cost=c,
+           B=64, ids=FAKE, top=FAKE, nsel=FAKE, st=FAKE, qa=FAKE, ws=FAKE, wsb=need):
+        return lib.ewsjf_trial_step(ln, ar, cap, P, pos, nl, na, n, now, table, theta,
+                                    C.byref(cost) if cost is not None else None, B, ids, top, nsel, st, qa, ws, wsb,
+                                    None)
+
+    assert ts(ln=None) == L.ERR_NULL
+    assert ts(st=None) == L.ERR_NULL
+    assert ts(qa=None) == L.ERR_NULL
+    assert ts(nl=None) == L.ERR_NULL
+    assert ts(cost=None) == L.ERR_NULL
+    assert ts(cap=1002) == L.ERR_ARG           # pools must stay 16-byte aligned
+    assert ts(P=0) == L.ERR_ARG
+    assert ts(P=L.MAX_THETA + 1) == L.ERR_ARG
+    assert ts(pos=1000) == L.ERR_ARG
+    assert ts(n=1001) == L.ERR_ARG
+    assert ts(B=0) == L.ERR_ARG
+    assert ts(now=float("inf")) == L.ERR_ARG
+    assert ts(wsb=need - 1) == L.ERR_WORKSPACE
+    assert ts(ar=FAKE_MIS) == L.ERR_ALIGN
+    lam = (C.c_double * 4)(1, 1, 1, 1)
+    bad = (C.c_double * 4)(1, float("nan"), 1, 1)
+    assert lib.ewsjf_trial_finish(None, FAKE, 1000, 4, 1.0, FAKE, FAKE, lam, FAKE, FAKE, None) == L.ERR_NULL
+    assert lib.ewsjf_trial_finish(FAKE, FAKE, 1000, 4, 1.0, FAKE, FAKE, None, FAKE, FAKE, None) == L.ERR_NULL
+    assert lib.ewsjf_trial_finish(FAKE, FAKE, 1000, 4, 1.0, FAKE, FAKE, bad, FAKE, FAKE, None) == L.ERR_ARG
+    assert lib.ewsjf_trial_finish(FAKE, FAKE, 1001, 4, 1.0, FAKE, FAKE, lam, FAKE, FAKE, None) == L.ERR_ARG
+
+
 def test_dispatch_argument_errors():
     lib = L.lib()
 
