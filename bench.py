@@ -341,7 +341,7 @@ def trial_bench(hip, steps: int = 100, P: int = 16):
             "reward_unit_lambda": [float(x) for x in R], "best_proposal": int(np.argmax(R))}
 
 
-def streaming_bench(steps: int):
+def streaming_bench(steps: int, handover: str = "next_step"):
     """Config-4 shape: per-step device latency of the streaming scheduler."""
     import numpy as np
     import torch
@@ -361,15 +361,18 @@ def streaming_bench(steps: int):
     dl = torch.from_numpy(lens).to(dev)
     da = torch.from_numpy(arrs).to(dev)
     prm = E.params(init_queues=sw.K, max_queues=sw.K)
-    sched = StreamingScheduler(sw.capacity, sw.window_size, sw.B, prm, sw.theta[0], sw.cost, device=dev)
+    sched = StreamingScheduler(sw.capacity, sw.window_size, sw.B, prm, sw.theta[0], sw.cost, device=dev,
+                               handover=handover)
     sched.fill(L0, A0)
     torch.cuda.synchronize()
     block = 100
     lat = np.zeros(steps)
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(block)]
+    hold = handover == "next_step"
     for b0 in range(0, steps, block):
         nb = min(block, steps - b0)
-        torch.cuda._sleep(int(2.4e9 * 0.03))  # hold the stream while the block is enqueued
+        if hold:  # hold the stream while the block is enqueued
+            torch.cuda._sleep(int(2.4e9 * 0.03))
         for j in range(nb):
             i = b0 + j
             ev[j][0].record()
@@ -381,11 +384,20 @@ def streaming_bench(steps: int):
         for j in range(nb):
             lat[b0 + j] = ev[j][0].elapsed_time(ev[j][1]) * 1e3
     steady = lat[100:] if steps > 100 else lat
-    rp = lat[101::sw.rp_every] if steps > 101 else np.zeros(0)  # the steps that take a new table
+    swaps = np.asarray(sched.swaps, np.int64)
+    rp = lat[swaps[swaps > 100]] if swaps.size else np.zeros(0)  # the steps that take a new table
+    if hold:
+        how = ("effective the next step, which waits for it; steps issued in blocks of 100 behind a held stream, "
+               "so the device runs them back to back")
+    else:
+        how = ("effective at the first step issued after it finished, no step waits; steps issued one by one at "
+               "the host's pace, so the partition runs between and beside them")
     return {"workload": "streaming_drift_1m: 1,048,576-slot ring, 4,096 arrivals and B=512 admissions per step, "
                         "64-queue Refine-and-Prune over the last 65,536 arrivals every 100 steps (side stream, "
-                        "effective the next step), short-request weight drifting 0.9 -> 0.3",
-            "steps": steps, "p50_us": float(np.percentile(steady, 50)), "p99_us": float(np.percentile(steady, 99)),
+                        f"{how}), short-request weight drifting 0.9 -> 0.3",
+            "handover": handover, "steps": steps,
+            "swap_delay_steps": (float(np.median(swaps[1:] % sw.rp_every)) if swaps.size > 1 else None),
+            "repartitions_skipped": sched.skipped, "p50_us": float(np.percentile(steady, 50)), "p99_us": float(np.percentile(steady, 99)),
             "mean_us": float(steady.mean()), "max_us": float(steady.max()),
             "after_repartition_p50_us": float(np.median(rp)) if rp.size else None,
             "latency": "device time of one step (arrivals inserted and admission, ewsjf_ring_step), steps 100.. "
@@ -576,6 +588,7 @@ def main() -> int:
         out["tactical"] = tactical_bench(hip, pool, table, lens, arrs)
         out["batched_theta"] = batched_theta_bench(hip)
         out["streaming"] = streaming_bench(args.stream_steps)
+        out["streaming_nonblocking"] = streaming_bench(args.stream_steps // 2, "when_ready")
         out["window_and_dispatch"] = window_and_dispatch_bench(hip)
         out["trial"] = trial_bench(hip)
     if not args.no_cpu:

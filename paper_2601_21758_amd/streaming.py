@@ -19,9 +19,12 @@ the log still holds both; otherwise ewsjf_window_histogram recounts the
 window from the log) and runs Refine-and-Prune from the histogram
 (ewsjf_partition_hist: the same table, bit for bit, as partitioning the
 window, since Refine-and-Prune sees it only through its distinct lengths and
-their multiplicities).  The new table takes effect at step s + 1.  A step
-whose log writes would overwrite entries a queued side-stream read still
-needs waits for that read first.
+their multiplicities).  The new table takes effect at step s + 1 (handover
+"next_step", which makes that step wait for the partition), or at the first
+step issued after the partition has finished on the device (handover
+"when_ready": the paper's non-blocking background optimizer, where no step
+waits).  A step whose log writes would overwrite entries a queued
+side-stream read still needs waits for that read first.
 
 With bubbles=(width, max_queues), the Dispatcher's on-demand bubble queues
 (Section 4.3, Algorithm 2) place each step's arrivals in the table the step
@@ -59,12 +62,18 @@ class StreamingScheduler:
     every repartition); log_capacity: length-log entries (default 2 *
     window); bubbles: (bubble_width, max_queues) to dispatch each step's
     arrivals with on-demand bubble queues (ewsjf_dispatch) into the table the
-    step uses, before the step (None: the table's contiguous routing).
+    step uses, before the step (None: the table's contiguous routing);
+    handover: "next_step" (a partition launched after step s takes effect at
+    step s + 1, which waits for it) or "when_ready" (it takes effect at the
+    first step issued after it has finished on the device; no step waits,
+    and a repartition requested while one is still running is skipped).
     """
 
     def __init__(self, capacity: int, window: int, B: int, params: L.PartitionParams, theta, cost=ewsjf.DEFAULT_COST,
                  device="cuda", incremental: bool = True, log_capacity: int | None = None,
-                 bubbles: tuple[int, int] | None = None):
+                 bubbles: tuple[int, int] | None = None, handover: str = "next_step"):
+        if handover not in ("next_step", "when_ready"):
+            raise ValueError("handover is 'next_step' or 'when_ready'")
         if capacity <= 0 or window <= 0 or window > capacity:
             raise ValueError("need 0 < window <= capacity")
         log_capacity = 2 * int(window) if log_capacity is None else int(log_capacity)
@@ -98,6 +107,10 @@ class StreamingScheduler:
         self.bubbles = None if bubbles is None else (int(bubbles[0]), int(bubbles[1]))
         self.undispatched = []  # (length, arrival) inserted since the last step, in order
         self.qid = torch.empty(L.MAX_DISPATCH, dtype=torch.int32, device=self.device)
+        self.handover = handover
+        self.skipped = 0     # repartitions skipped while one was still running (when_ready)
+        self.swaps = []      # step numbers at which a new table took effect
+        self.steps_done = 0
 
     # -- state ----------------------------------------------------------------
     def table(self) -> torch.Tensor:
@@ -169,6 +182,9 @@ class StreamingScheduler:
         """Partition the window as of the last step on the side stream; the
         new table takes effect at the next step()."""
         if self.pending is not None:
+            if self.handover == "when_ready":
+                self.skipped += 1  # the strategic loop is still busy with the previous one
+                return
             raise RuntimeError("a partition is already pending")
         main = torch.cuda.current_stream(self.device)
         self.side.wait_stream(main)  # the log holds every step so far
@@ -200,10 +216,12 @@ class StreamingScheduler:
         With length/arrival, the step's arrivals are inserted first, inside
         the step's kernels (same effect as insert() then step())."""
         main = torch.cuda.current_stream(self.device)
-        if self.pending is not None:
-            main.wait_event(self.pending)
+        if self.pending is not None and (self.handover == "next_step" or self.pending.query()):
+            main.wait_event(self.pending)  # free once the partition has finished (when_ready)
             self.cur = 1 - self.cur
             self.pending = None
+            self.swaps.append(self.steps_done)
+        self.steps_done += 1
         if self.bubbles is not None:
             batches, self.undispatched = self.undispatched, []
             if length is not None:

@@ -50,11 +50,11 @@ class OracleStream:
         self.next_table = oracle.partition(self.win, **self.kw)
         return self.next_table
 
-    def step(self, now):
+    def step(self, now, take_new=None):
         """Route, score and select over the ring with the current table; the
-        partition of the previous repartition() (called after the previous
-        step) takes effect here first."""
-        if self.next_table is not None:
+        partition of the last repartition() takes effect here first (at the
+        step after it, or, with take_new given, when take_new is true)."""
+        if self.next_table is not None and (take_new is None or take_new):
             self.table, self.next_table = self.next_table, None
         for length, arrival in self.undispatched:
             k0 = self.table.k

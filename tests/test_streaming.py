@@ -17,6 +17,7 @@ from paper_2601_21758_amd import workloads as W  # noqa: E402
 from paper_2601_21758_amd.streaming import StreamingScheduler  # noqa: E402
 from parity_util import check_admission, check_table  # noqa: E402
 from streaming_ref import OracleStream  # noqa: E402
+import oracle  # noqa: E402
 
 
 # ---- host-side logic (CPU) ------------------------------------------------------
@@ -180,6 +181,46 @@ def test_streaming_lockstep_with_bubble_queues(fused):
     # that the next partition replaces
     _lockstep(capacity=1 << 14, per_step=300, steps=60, window=512, rp_every=15, B=64, K=64, label="bubbles",
               tombstone_check_every=4, fused=fused, bubbles=(64, 128), novel=0.05)
+
+
+@pytest.mark.gpu
+def test_streaming_nonblocking_handover():
+    """handover="when_ready": a partition takes effect at the first step
+    issued after it finished, and a repartition requested while one runs is
+    skipped.  The reference takes each new table at the step the scheduler
+    recorded; tables and admissions agree throughout."""
+    from paper_2601_21758_amd import ewsjf
+    s = W.Streaming(seed=8, capacity=1 << 15, per_step=1024, steps=80, window=8192, rp_every=3, B=64, K=16)
+    prm = ewsjf.params(init_queues=16, max_queues=16)
+    gpu = StreamingScheduler(s.capacity, s.window_size, s.B, prm, s.theta[0], s.cost, handover="when_ready")
+    ref = OracleStream(s.capacity, s.window_size, s.B, 16, 16, s.theta, s.cost)
+    L0, A0 = s.initial_fill()
+    gpu.fill(L0, A0)
+    ref.fill(L0, A0)
+    launched_for = None  # the oracle's partition of the window the running repartition saw
+    for step in range(80):
+        L, A = s.arrivals(step)
+        Lg, Ag = torch.from_numpy(L).cuda(), torch.from_numpy(A).cuda()
+        ref.insert(L, A)
+        n_swaps = len(gpu.swaps)
+        ids, top, nsel = gpu.step(float(A[-1]), tombstone=False, length=Lg, arrival=Ag)
+        took = len(gpu.swaps) > n_swaps
+        if took:
+            ref.next_table, launched_for = launched_for, None
+        rids, rtop, rnsel, rsc = ref.step(float(A[-1]), take_new=took)
+        if step % 3 == 0:
+            before = gpu.skipped
+            gpu.launch_repartition()
+            if gpu.skipped == before:
+                launched_for = oracle.partition(ref.win, init_queues=16, max_queues=16)
+        torch.cuda.synchronize()
+        check_admission(ids.cpu().numpy()[0], top.cpu().numpy()[0], nsel.cpu().numpy()[0], rids, rtop, rnsel, rsc)
+        gpu.apply_tombstones(rids[:rnsel])  # both sides drop the oracle's admitted set
+        ref.tombstone(rids[:rnsel])
+        g = ewsjf.read_table(gpu.tables[gpu.cur])
+        assert np.array_equal(g["bounds"], ref.table.bounds), f"step {step}: tables differ"
+    assert gpu.swaps, "no partition took effect"
+    print(f"nonblocking: {len(gpu.swaps)} swaps, {gpu.skipped} skipped", flush=True)
 
 
 @pytest.mark.gpu
