@@ -118,3 +118,37 @@ def test_identical_proposals_agree(E):
     R = host(tr.finish())
     st = host(tr.stats)
     assert np.array_equal(st[0], st[1]) and np.array_equal(st[0], st[2]) and R[0] == R[1] == R[2]
+
+
+def test_full_size_trial_prefix(E):
+    """The bench's trial at full size (16 proposals on 1,048,576-slot rings,
+    4,096 common arrivals and B=512 per step) for three steps."""
+    from paper_2601_21758_amd.trial import Trial
+    sw = W.Streaming(steps=3)
+    L0, A0 = sw.initial_fill()
+    t = oracle.partition(L0[-sw.window_size:], init_queues=sw.K, max_queues=sw.K)
+    tab = E.upload_table(t.bounds, t.mean, 32768, t.lo, t.hi, t.count, t.sum)
+    rng = np.random.default_rng(11)
+    th = np.tile(W.THETA_MID.reshape(1, 6), (16, 1)).astype(np.float32)
+    th[1:] *= rng.uniform(0.3, 3.0, (15, 6)).astype(np.float32)
+    batches = []
+    for i in range(3):
+        nl, na = sw.arrivals(i)
+        batches.append((nl, na, float(na[-1])))
+    tr = Trial(sw.capacity, th, sw.B, tab, sw.cost)
+    tr.start(L0, A0)
+    say("trial full size: 16 x 1,048,576, 3 steps")
+    got = []
+    for nl, na, now in batches:
+        ids, top, nsel = tr.step(dev(nl), dev(na), now)
+        got.append((host(ids), host(nsel)))
+    R = host(tr.finish((1.0, 1.0, 1.0, 1.0)))
+    rs, rq, hist = OT.trial(L0, A0, t, th, batches, sw.B, sw.cost)
+    for s, ((ids, nsel), ref) in enumerate(zip(got, hist)):
+        for p in range(16):
+            assert int(nsel[p]) == ref[p].size and np.array_equal(np.sort(ids[p][:ref[p].size]), np.sort(ref[p])), \
+                f"step {s} proposal {p}"
+    st = host(tr.stats)
+    assert np.array_equal(st[:, [0, 1, 4, 5, 6, 7]], rs[:, [0, 1, 4, 5, 6, 7]])
+    assert np.allclose(st[:, 2:4], rs[:, 2:4], rtol=1e-12, atol=0)
+    assert np.allclose(R, OT.reward(rs, rq, t, (1.0, 1.0, 1.0, 1.0)), rtol=1e-12, atol=1e-15)
