@@ -922,6 +922,7 @@ struct MergeShared {
   uint64_t red[kWavesPerBlock];
   uint64_t wmax[kWavesPerBlock];
   uint64_t wmin[kWavesPerBlock];
+  uint64_t wbound[kWavesPerBlock];  // largest completeness bound of each wave's shares
   int iscan[kWavesPerBlock];
   int wtot[kWavesPerBlock];
   int cntX;
@@ -1074,17 +1075,22 @@ __global__ __launch_bounds__(kBlock) void merge_candidates(Src src0, int64_t n, 
   mx = wave_max_u64(mx);
   mn = wave_min_u64(mn);
   nz = (int)__ockl_wfred_add_u32((uint32_t)nz);
+  const uint64_t tb = wave_max_u64(Tw);
   for (int i = tid; i < 4096; i += kBlock) ms.cnt[i] = 0u;
   if (lane == 0) {
     ms.wmax[wv] = mx;
     ms.wmin[wv] = mn;
     ms.iscan[wv] = nz;
+    ms.wbound[wv] = tb;
   }
   __syncthreads();
   // Every wave reduces the kWavesPerBlock partials itself, one per lane.
   static_assert(kWavesPerBlock <= kWave, "one partial per lane");
   const bool pl = lane < kWavesPerBlock;
   const int total = (int)__ockl_wfred_add_u32(pl ? (uint32_t)ms.iscan[lane] : 0u);
+  // The largest bound of all shares: the recovery below runs only when it
+  // lies above the cut (it usually does not).
+  const uint64_t max_bound = wave_max_u64(pl ? ms.wbound[lane] : 0ull);
   int U = 0;
   if (total > 0) {
     const uint64_t hi = wave_max_u64(pl ? ms.wmax[lane] : 0ull);
@@ -1158,8 +1164,11 @@ __global__ __launch_bounds__(kBlock) void merge_candidates(Src src0, int64_t n, 
   // reaches down to the cut, else re-read from the pool -- and the cut is
   // raised right away, so later shares often drop out.  X[0..U) is sorted.
   bool staged = false;
-  for (;;) {
+  // The loop sits behind a test of the largest bound so that its set-up is
+  // not paid when no share is at risk (the usual case).
+  if (max_bound > (tau > 1ull ? tau : 1ull)) for (;;) {
     const uint64_t thr = tau > 1ull ? tau : 1ull;
+    if (max_bound <= thr) break;  // bounds only fall and the cut only rises
     // The share with the largest bound; every wave finds it from LDS itself,
     // so the decision is uniform without a barrier.
     uint64_t bl = 0;
