@@ -57,26 +57,25 @@ struct PoolSource {
   struct Stage {
     i32x4 v[kLutPerThread];
     double mean;
-    ewsjf_theta th;
-    int k, L;
+    int t;
   };
 
   // Run by the first kStageThreads threads.  Branch-free on purpose: every
   // load is issued unconditionally (the lookup table and the mean array are
-  // read whole, indices clamped into them), and the table's scalars are read
-  // here too, so the LDS stores in stage_store wait only for these loads.
+  // read whole, indices clamped into them).  The table's scalars and the
+  // parameter vector are read in stage_store: read here, their first use
+  // (hoisted by the compiler) put a wait for them ahead of the barrier that
+  // releases the pool loads, which then started one memory round trip late.
   __device__ __forceinline__ void stage_load(Stage& st, int t) const {
     const i32x4* src = reinterpret_cast<const i32x4*>(table->lut);
 #pragma unroll
     for (int r = 0; r < kLutPerThread; ++r) {
       const int i = threadIdx.x + r * kStageThreads;
-      st.v[r] = src[i < kLutVecs ? i : kLutVecs - 1];
+      st.v[r] = src[i < kLutVecs ? i : i - kStageThreads];  // a past-the-end slot reloads an earlier one
     }
     static_assert(EWSJF_MAX_QUEUES == kStageThreads, "one mean per staging thread");
     st.mean = table->mean[threadIdx.x];
-    st.th = theta[t];
-    st.k = table->k;
-    st.L = table->max_len;
+    st.t = t;
   }
 
   __device__ __forceinline__ void stage_store(Shared& sh, const Stage& st) const {
@@ -86,8 +85,8 @@ struct PoolSource {
       const int i = threadIdx.x + r * kStageThreads;
       if (r + 1 < kLutPerThread || i < kLutVecs) dst[i] = st.v[r];
     }
-    if ((int)threadIdx.x < st.k) sh.qp[threadIdx.x] = make_qparams(st.th, st.mean, threadIdx.x);
-    if (threadIdx.x == 0) sh.L = st.L;
+    if ((int)threadIdx.x < table->k) sh.qp[threadIdx.x] = make_qparams(theta[st.t], st.mean, threadIdx.x);
+    if (threadIdx.x == 0) sh.L = table->max_len;
   }
 
   __device__ __forceinline__ Raw load4(int64_t base, int64_t n) const {
@@ -157,7 +156,7 @@ struct FifoSource {
   };
   struct Stage {
     i32x4 v[kLutPerThread];
-    int L, qsel;
+    int t;
   };
 
   __device__ __forceinline__ void stage_load(Stage& st, int t) const {
@@ -165,10 +164,9 @@ struct FifoSource {
 #pragma unroll
     for (int r = 0; r < kLutPerThread; ++r) {
       const int i = threadIdx.x + r * kStageThreads;
-      st.v[r] = src[i < kLutVecs ? i : kLutVecs - 1];
+      st.v[r] = src[i < kLutVecs ? i : i - kStageThreads];  // a past-the-end slot reloads an earlier one
     }
-    st.L = table->max_len;
-    st.qsel = plan->q_sel[t];
+    st.t = t;
   }
 
   __device__ __forceinline__ void stage_store(Shared& sh, const Stage& st) const {
@@ -179,8 +177,8 @@ struct FifoSource {
       if (r + 1 < kLutPerThread || i < kLutVecs) dst[i] = st.v[r];
     }
     if (threadIdx.x == 0) {
-      sh.L = st.L;
-      sh.qsel = st.qsel;
+      sh.L = table->max_len;
+      sh.qsel = plan->q_sel[st.t];
     }
   }
 
