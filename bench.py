@@ -13,7 +13,10 @@ the 256 MiB Infinity Cache) are stepped in turn so each step reads HBM.
 Steps run from a captured HIP graph (chunks of up to 50 steps) so host
 launch cost does not bound the loop; an eager pass with per-kernel events
 gives each kernel's own duration (start/end events bound to the kernel's
-dispatch) for the roofline figure.
+dispatch) for the roofline figure.  "step_percentiles_us" gives p10/p50/p90
+of the step per graph replay and per eager step, and of each kernel;
+"copy_reference" is a plain device-to-device copy's bandwidth on the same
+GPU.
 
 More workloads ride along in the same JSON line (skip them with
 --no-extra): "tactical" -- Algorithm 1's own batch rule on the same 4M pool
@@ -97,6 +100,39 @@ class Hip:
         assert self.rt.hipEventSynchronize(b) == 0
         assert self.rt.hipEventElapsedTime(C.byref(ms), a, b) == 0
         return float(ms.value)
+
+
+def pct(xs) -> dict:
+    """p10 / p50 / p90 of a list of timings."""
+    import numpy as np
+    a = np.asarray(xs, dtype=np.float64)
+    return {"p10": float(np.percentile(a, 10)), "p50": float(np.median(a)), "p90": float(np.percentile(a, 90)),
+            "n": int(a.size)}
+
+
+def copy_reference(dev, mib: int = 512, reps: int = 20) -> dict:
+    """Device-to-device copy bandwidth on the same GPU, for reference: two
+    pairs of 512 MiB buffers (2 GiB together, beyond the 256 MiB Infinity
+    Cache), alternated, bytes read plus bytes written per copy."""
+    import numpy as np
+    import torch
+    n = mib << 20
+    bufs = [torch.empty(n, dtype=torch.uint8, device=dev) for _ in range(4)]
+    for b in bufs:
+        b.fill_(1)
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+    for i in range(reps):
+        src, dst = (bufs[0], bufs[1]) if i % 2 == 0 else (bufs[2], bufs[3])
+        ev[i][0].record()
+        dst.copy_(src)
+        ev[i][1].record()
+    torch.cuda.synchronize()
+    ms = float(np.median([a.elapsed_time(b) for a, b in ev[2:]]))
+    del bufs
+    torch.cuda.empty_cache()
+    return {"GB_per_s": 2 * n / (ms * 1e-3) / 1e9, "bytes_per_copy": 2 * n,
+            "method": f"torch copy_ between device buffers of {mib} MiB, median of {reps - 2}"}
 
 
 def cpu_baseline(pool, table_ref, budget_s: float):
@@ -528,6 +564,7 @@ def main() -> int:
     eager_ms = hip.elapsed_ms(e0, e1) / K
     k1 = [hip.elapsed_ms(m[0], m[1]) for m in marks]
     k2 = [hip.elapsed_ms(m[2], m[3]) for m in marks]
+    eager_steps = [hip.elapsed_ms(m[0], m[3]) for m in marks]  # first kernel's start to second kernel's end
     k1_ms = float(np.mean(k1))
     k2_ms = float(np.mean(k2))
     eager_ids = ids.clone()
@@ -552,12 +589,19 @@ def main() -> int:
         g.replay()
     torch.cuda.synchronize()
     gs = vp(torch.cuda.current_stream().cuda_stream)
-    rt.hipEventRecord(e0, gs)
-    for _ in range(K // chunk):
+    # One event per replay boundary: the whole interval gives the mean, the
+    # replays give the spread (each replay is `chunk` back-to-back steps).
+    reps = K // chunk
+    bounds_ev = [hip.event() for _ in range(reps + 1)]
+    rt.hipEventRecord(bounds_ev[0], gs)
+    for r in range(reps):
         g.replay()
-    rt.hipEventRecord(e1, gs)
-    graph_ms = hip.elapsed_ms(e0, e1) / K
+        rt.hipEventRecord(bounds_ev[r + 1], gs)
     torch.cuda.synchronize()
+    graph_ms = hip.elapsed_ms(bounds_ev[0], bounds_ev[reps]) / K
+    replay_step_us = [hip.elapsed_ms(bounds_ev[r], bounds_ev[r + 1]) * 1e3 / chunk for r in range(reps)]
+    for e in bounds_ev:
+        rt.hipEventDestroy(e)
     graph_ok = bool(torch.equal(ids, eager_ids))
 
     ms_per_step = graph_ms
@@ -580,6 +624,13 @@ def main() -> int:
                      "traffic": traffic, "bytes_per_launch": alg_bytes, "kernel_ms": k1_ms},
         "step_hbm_frac": alg_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
         "kernels_ms": {"local_candidates": k1_ms, "merge_candidates": k2_ms},
+        "step_percentiles_us": {
+            "graph_per_replay": pct(replay_step_us),
+            "eager_per_step": pct([x * 1e3 for x in eager_steps]),
+            "local_candidates": pct([x * 1e3 for x in k1]),
+            "merge_candidates": pct([x * 1e3 for x in k2]),
+        },
+        "copy_reference": copy_reference(dev),
         "eager_ms_per_step": eager_ms, "graph_matches_eager": graph_ok,
         "partition_ms": partition_ms,
         "partition_from_histogram_ms": partition_hist_ms,
