@@ -621,7 +621,8 @@ def main() -> int:
                    "execution": f"HIP graph, {chunk} steps per graph", "input_sha256": pool.digest()[:16]},
         "roofline": {"bound": "hbm", "kernel": "local_candidates (route+score+local top-B)",
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": traffic, "bytes_per_launch": alg_bytes, "kernel_ms": k1_ms},
+                     "traffic": traffic, "bytes_per_launch": alg_bytes, "kernel_ms": k1_ms,
+                     "traffic_frac": (traffic / (k1_ms * 1e-3) / 1e9 / HBM_PEAK_GBS) if traffic else None},
         "step_hbm_frac": alg_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
         "kernels_ms": {"local_candidates": k1_ms, "merge_candidates": k2_ms},
         "step_percentiles_us": {
