@@ -219,45 +219,72 @@ __device__ int64_t block_exclusive_scan64(int64_t x, int64_t* scratch, int64_t* 
   return base + incl - x;
 }
 
-// Distinct values and exact prefix sums, one workgroup.
+// Distinct values and exact prefix sums, one workgroup.  Wave w covers the
+// bins [2048 w, 2048 w + 2048) and its lane l the 32 bins from
+// 2048 w + 32 l (bin 0 is not a length; the last thread also takes bin
+// 32768), so the distinct values come out in thread order.  The bins arrive
+// by coalesced loads, 64 consecutive bins per load, all issued before any is
+// used (bounded: past bin L they read 0), and are transposed through the
+// wave's region of LDS, where each lane reads its 32 bins twice: for its
+// totals, and after the scans for its outputs (nothing is held in registers
+// across the scans).
+constexpr int kDistinctRegion = kBinsPerThread * kWave + kWave;  // 2048 bins, one pad word per 32
+
+__device__ __forceinline__ int pad32(int i) { return i + (i >> 5); }
+
 __global__ __launch_bounds__(kBlock) void rp_distinct(PartWs w, int L) {
+  static_assert(kBinsPerThread * kBlock == EWSJF_MAX_LEN, "every bin below the largest length has one owner");
+  __shared__ uint32_t stage[kWavesPerBlock * kDistinctRegion];
   __shared__ int64_t scr[kWavesPerBlock];
   __shared__ int iscr[kWavesPerBlock];
-  const int t = threadIdx.x;
-  const int b0 = 1 + t * kBinsPerThread;
-  int nz = 0;
-  int64_t cn = 0, cs = 0;
-  for (int q = 0; q < kBinsPerThread; ++q) {
-    const int b = b0 + q;
-    if (b <= L) {
-      const uint32_t h = w.hist[b];
-      if (h) {
-        ++nz;
-        cn += h;
-        cs += (int64_t)h * b;
-      }
-    }
+  const int t = threadIdx.x, lane = t & (kWave - 1), wv = t / kWave;
+  uint32_t* reg = stage + wv * kDistinctRegion;
+  const int wbin = wv * kBinsPerThread * kWave;
+  {
+    const __amdgpu_buffer_rsrc_t rs =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<uint32_t*>(w.hist), (short)0, (L + 1) * 4, kBufferWord3);
+    uint32_t x[kBinsPerThread];
+#pragma unroll
+    for (int q = 0; q < kBinsPerThread; ++q)
+      x[q] = __builtin_amdgcn_raw_buffer_load_b32(rs, (wbin + q * kWave + lane) * 4, 0, 0);
+#pragma unroll
+    for (int q = 0; q < kBinsPerThread; ++q) reg[pad32(q * kWave + lane)] = x[q];
+    if (t == 0) reg[0] = 0u;  // bin 0 is not a length
+  }
+  // Bin EWSJF_MAX_LEN, the last thread's extra bin (read only when it is a length).
+  const uint32_t hx = (t == kBlock - 1 && L >= EWSJF_MAX_LEN) ? w.hist[EWSJF_MAX_LEN] : 0u;
+  __syncthreads();
+  const int b0 = wbin + lane * kBinsPerThread;  // this thread's first bin
+  const uint32_t* mine = reg + pad32(lane * kBinsPerThread);  // its 32 bins, contiguous after padding
+  int nz = hx != 0u;
+  int64_t cn = hx, cs = (int64_t)hx * EWSJF_MAX_LEN;
+#pragma unroll
+  for (int k = 0; k < kBinsPerThread; ++k) {
+    const uint32_t h = mine[k];
+    nz += h != 0u;
+    cn += h;
+    cs += (int64_t)h * (b0 + k);
   }
   int V = 0;
   int64_t totN = 0, totS = 0;
   int pos = block_exclusive_scan(nz, iscr, &V);
   int64_t pn = block_exclusive_scan64(cn, scr, &totN);
   int64_t ps = block_exclusive_scan64(cs, scr, &totS);
-  for (int q = 0; q < kBinsPerThread; ++q) {
-    const int b = b0 + q;
-    if (b <= L) {
-      const uint32_t h = w.hist[b];
-      if (h) {
-        w.v[pos] = b;
-        w.c[pos] = h;
-        w.PN[pos] = pn;
-        w.PS[pos] = ps;
-        pn += h;
-        ps += (int64_t)h * b;
-        ++pos;
-      }
+  // Outputs, each lane's run of positions in bin order.
+  auto put = [&](uint32_t h, int b) {
+    if (h != 0u) {
+      w.v[pos] = b;
+      w.c[pos] = h;
+      w.PN[pos] = pn;
+      w.PS[pos] = ps;
+      pn += h;
+      ps += (int64_t)h * b;
+      ++pos;
     }
-  }
+  };
+#pragma unroll
+  for (int k = 0; k < kBinsPerThread; ++k) put(mine[k], b0 + k);
+  put(hx, EWSJF_MAX_LEN);
   if (t == 0) {
     w.PN[V] = totN;
     w.PS[V] = totS;
