@@ -423,11 +423,15 @@ __device__ ArgMin block_argmin(ArgMin x, double* su, int* si) {
   return r;
 }
 
+// The distinct values and the cluster-start flags sit in LDS padded by 4
+// bytes per 32 entries (vat / sat): a thread owns 32 consecutive entries,
+// and without the padding the lanes of a wave read them 64 (values) or 32
+// (flags) bytes apart, 16- and 8-way bank conflicts.
 struct RpShared {
   union {
     struct {
-      uint16_t v[EWSJF_MAX_LEN];
-      uint8_t start[EWSJF_MAX_LEN];
+      uint16_t v[EWSJF_MAX_LEN + 2 * (EWSJF_MAX_LEN / 32)];
+      uint8_t start[EWSJF_MAX_LEN + 4 * (EWSJF_MAX_LEN / 32)];
     } a;
   } u;
   int64_t scr64[kWavesPerBlock];
@@ -437,6 +441,9 @@ struct RpShared {
   int flag;
 };
 
+__device__ __forceinline__ uint16_t& vat(RpShared& sm, int j) { return sm.u.a.v[j + 2 * (j >> 5)]; }
+__device__ __forceinline__ uint8_t& sat(RpShared& sm, int j) { return sm.u.a.start[j + 4 * (j >> 5)]; }
+
 // For thread-owned index ranges [j0, j0 + 32): carry_s = the last segment
 // start before j0 (-1 if none), carry_e = the first segment start after the
 // range (V if none).
@@ -445,7 +452,7 @@ __device__ void segment_carries(RpShared& sm, int V, int j0, int* carry_s, int* 
   int last = -1, first = 0x7fffffff;
   for (int q = 0; q < kBinsPerThread; ++q) {
     const int j = j0 + q;
-    if (j < V && sm.u.a.start[j]) {
+    if (j < V && sat(sm, j)) {
       last = j;
       if (first == 0x7fffffff) first = j;
     }
@@ -517,19 +524,31 @@ __global__ __launch_bounds__(kBlock) void rp_refine_prune(PartWs w, ewsjf_partit
   }
 
   // ---- Stage 1: coarse cluster starts -------------------------------------
-  for (int j = tid; j < V; j += kBlock) sm.u.a.v[j] = (uint16_t)w.v[j];
+  {
+    // Every load is issued before the first store (bounded: past V they read 0).
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(w.v, (short)0, V * 4, kBufferWord3);
+    uint32_t x[kBinsPerThread];
+#pragma unroll
+    for (int k = 0; k < kBinsPerThread; ++k)
+      x[k] = __builtin_amdgcn_raw_buffer_load_b32(rs, (tid + k * kBlock) * 4, 0, 0);
+#pragma unroll
+    for (int k = 0; k < kBinsPerThread; ++k)
+      if (tid + k * kBlock < V) vat(sm, tid + k * kBlock) = (uint16_t)x[k];
+  }
   __syncthreads();
-  const int64_t vlo = sm.u.a.v[0], vhi = sm.u.a.v[V - 1];
+  const int64_t vlo = vat(sm, 0), vhi = vat(sm, V - 1);
   if (p.init_mode == EWSJF_INIT_EQUAL_WIDTH) {
     const int64_t width = vhi - vlo + 1;
     for (int j = tid; j < V; j += kBlock) {
       uint8_t s = 1;
       if (j > 0) {
-        const int64_t b1 = ((int64_t)sm.u.a.v[j] - vlo) * (int64_t)p.init_queues / width;
-        const int64_t b0 = ((int64_t)sm.u.a.v[j - 1] - vlo) * (int64_t)p.init_queues / width;
+        // (v - lo) K < 2^30 (values and K are at most 32768): the 32-bit
+        // quotient is the exact floor of the int64 definition.
+        const uint32_t b1 = (uint32_t)(vat(sm, j) - vlo) * (uint32_t)p.init_queues / (uint32_t)width;
+        const uint32_t b0 = (uint32_t)(vat(sm, j - 1) - vlo) * (uint32_t)p.init_queues / (uint32_t)width;
         s = b1 != b0;
       }
-      sm.u.a.start[j] = s;
+      sat(sm, j) = s;
     }
   } else {
     const int ki = w.meta[1], kj = w.meta[2];
@@ -537,14 +556,14 @@ __global__ __launch_bounds__(kBlock) void rp_refine_prune(PartWs w, ewsjf_partit
       uint8_t s;
       if (V <= 3) s = 1;
       else s = (j == 0 || j == ki || j == kj) ? 1 : 0;
-      sm.u.a.start[j] = s;
+      sat(sm, j) = s;
     }
   }
   __syncthreads();
   int n_coarse = 0;
   {
     int cnt = 0;
-    for (int j = tid; j < V; j += kBlock) cnt += sm.u.a.start[j];
+    for (int j = tid; j < V; j += kBlock) cnt += sat(sm, j);
     int tot = 0;
     block_exclusive_scan(cnt, sm.iscr, &tot);
     n_coarse = tot;
@@ -557,66 +576,70 @@ __global__ __launch_bounds__(kBlock) void rp_refine_prune(PartWs w, ewsjf_partit
   int carry_s = -1, carry_e = V;
   for (;;) {
     segment_carries(sm, V, j0, &carry_s, &carry_e);
-    int ends[kBinsPerThread];
-    {
-      int nxt = carry_e;
-      for (int q = kBinsPerThread - 1; q >= 0; --q) {
-        const int j = j0 + q;
-        ends[q] = nxt;
-        if (j < V && sm.u.a.start[j]) nxt = j;
-      }
-    }
+    // This thread's segment starts as a bit mask (bit q: index j0 + q); the
+    // segment [s, e) holding index j0 + q starts at the highest set bit <= q
+    // (else carry_s) and ends at the lowest set bit > q (else carry_e).
+    // Branch-free and unrolled, so the LDS reads of all 32 gaps are issued
+    // together; indices of gaps that are not tested are clamped to 0.
+    uint32_t mask = 0u;
+#pragma unroll
+    for (int q = 0; q < kBinsPerThread; ++q) mask |= (uint32_t)(j0 + q < V && sat(sm, j0 + q)) << q;
     uint32_t newcuts = 0;
-    int s = carry_s;
+#pragma unroll
     for (int q = 0; q < kBinsPerThread; ++q) {
       const int j = j0 + q;
-      if (j >= V) break;
-      if (sm.u.a.start[j]) s = j;
-      // the gap between j and j+1 inside the current segment [s, e)
-      const int e = ends[q];
-      if (j + 1 >= e) continue;
+      const uint32_t below = mask & (0xFFFFFFFFu >> (31 - q));
+      const int s = below ? j0 + 31 - __clz((int)below) : carry_s;
+      const uint32_t above = q < 31 ? mask >> (q + 1) : 0u;
+      const int e = above ? j + __ffs((int)above) : carry_e;
+      // the gap between j and j+1 inside the segment [s, e)
+      const bool gap = j + 1 < e;  // (e <= V, so j + 1 < V)
       const int VC = e - s;
-      const int64_t span = (int64_t)sm.u.a.v[e - 1] - (int64_t)sm.u.a.v[s];
-      if (VC < min_distinct || span < (int64_t)p.min_width) continue;
-      int64_t mm1;
-      if (p.gap_mode == EWSJF_GAPS_DISTINCT) mm1 = VC - 1;
-      else mm1 = (w.PN[e] - w.PN[s]) - 1;
-      const double rhs = p.alpha * (double)span;
-      const double lhs = (double)((int64_t)sm.u.a.v[j + 1] - (int64_t)sm.u.a.v[j]) * (double)mm1;
-      if (lhs > rhs) newcuts |= 1u << q;
+      const int64_t span = (int64_t)vat(sm, gap ? e - 1 : 0) - (int64_t)vat(sm, gap ? s : 0);
+      const bool test = gap && VC >= min_distinct && span >= (int64_t)p.min_width;
+      // span, the gap and VC - 1 fit in int32 (values are at most 32768), so
+      // they convert to binary64 in one exact step; the count-mode m - 1 is
+      // an int64 count.
+      const double mm1 = p.gap_mode == EWSJF_GAPS_DISTINCT ? (double)(VC - 1)
+                                                           : (double)(test ? (w.PN[e] - w.PN[s]) - 1 : 0);
+      const double rhs = p.alpha * (double)(int)span;
+      const double lhs = (double)((int)vat(sm, gap ? j + 1 : 0) - (int)vat(sm, gap ? j : 0)) * mm1;
+      if (test && lhs > rhs) newcuts |= 1u << q;
     }
     const int any = __syncthreads_or(newcuts != 0);
     if (!any) break;
     for (int q = 0; q < kBinsPerThread; ++q)
-      if (newcuts & (1u << q)) sm.u.a.start[j0 + q + 1] = 1;
+      if (newcuts & (1u << q)) sat(sm, j0 + q + 1) = 1;
     __syncthreads();
   }
 
   // ---- Leaves: one per segment, aggregates from the exact prefix sums -------
+  // The segment starts are listed in order (in the Stage-3 workspace, which
+  // rp_merge rewrites later), then each thread builds whole leaves: four
+  // independent prefix-sum loads per leaf instead of a chain per thread.
   int nl = 0;
   {
-    segment_carries(sm, V, j0, &carry_s, &carry_e);
     int cnt = 0;
     for (int q = 0; q < kBinsPerThread; ++q) {
       const int j = j0 + q;
-      if (j < V) cnt += sm.u.a.start[j];
+      if (j < V) cnt += sat(sm, j);
     }
     int tot = 0;
     int pos = block_exclusive_scan(cnt, sm.iscr, &tot);
     nl = tot;
-    int e = carry_e;
-    // walk owned indices from the right so each start knows its segment end
-    int ends_pos = pos + cnt;
-    for (int q = kBinsPerThread - 1; q >= 0; --q) {
+    int32_t* starts = reinterpret_cast<int32_t*>(w.gU);
+    for (int q = 0; q < kBinsPerThread; ++q) {
       const int j = j0 + q;
-      if (j < V && sm.u.a.start[j]) {
-        --ends_pos;
-        w.gn[ends_pos] = w.PN[e] - w.PN[j];
-        w.gS[ends_pos] = w.PS[e] - w.PS[j];
-        w.glo[ends_pos] = sm.u.a.v[j];
-        w.ghi[ends_pos] = sm.u.a.v[e - 1];
-        e = j;
-      }
+      if (j < V && sat(sm, j)) starts[pos++] = j;
+    }
+    __syncthreads();
+    for (int i = tid; i < nl; i += kBlock) {
+      const int s = starts[i];
+      const int e = i + 1 < nl ? starts[i + 1] : V;
+      w.gn[i] = w.PN[e] - w.PN[s];
+      w.gS[i] = w.PS[e] - w.PS[s];
+      w.glo[i] = vat(sm, s);
+      w.ghi[i] = vat(sm, e - 1);
     }
   }
   __threadfence();
