@@ -340,6 +340,12 @@ PART_CASES = {
     "clamped": lambda: (np.array([-5, 0, 1, 40000, 32768, 7, 7, 100000], np.int32),
                         dict(init_queues=4, max_queues=4, min_width=0)),
     "max_len_1000": lambda: (W.config(0).window, dict(init_queues=16, max_queues=16, max_len=1000)),
+    # the top of the length range: the largest regular bin, no bin 32768
+    "max_len_32767": lambda: (np.concatenate([W.config(0).window, np.arange(32700, 32800, dtype=np.int32)]),
+                              dict(init_queues=16, max_queues=16, max_len=32767)),
+    # a cap just past one wave's 2048 bins of the distinct-value scan
+    "max_len_2049": lambda: (np.arange(1990, 2110, 3, dtype=np.int32), dict(init_queues=4, max_queues=8, min_width=0,
+                                                                           max_len=2049)),
     "dense_all_values": lambda: (np.arange(1, 32769, dtype=np.int32), dict(init_queues=256, max_queues=256)),
     "alternating_gaps_8000_leaves": lambda: (np.cumsum(np.tile([1, 3], 8000)).astype(np.int32),
                                             dict(init_queues=1, max_queues=64, min_width=0, alpha=1.05)),
