@@ -677,6 +677,22 @@ __global__ __launch_bounds__(kBlock) void rp_refine_prune(PartWs w, ewsjf_partit
 // ---------------------------------------------------------------------------
 constexpr int kMergeThreads = 256;
 
+// Lowest lane holding the wave's minimum of x, and that minimum (*m).  The
+// high words are reduced first, the low words only when several lanes share
+// the smallest high word (utilities rarely do).
+__device__ __forceinline__ int wave_argmin_u64(uint64_t x, uint64_t* m) {
+  const uint32_t xh = (uint32_t)(x >> 32);
+  const uint32_t mh = __ockl_wfred_min_u32(xh);
+  uint64_t cand = __ballot(xh == mh);
+  if (__popcll(cand) > 1) {
+    const uint32_t ml = __ockl_wfred_min_u32(xh == mh ? (uint32_t)x : 0xFFFFFFFFu);
+    cand = __ballot(xh == mh && (uint32_t)x == ml);
+  }
+  const int src = (int)__builtin_ctzll(cand);
+  *m = ((uint64_t)mh << 32) | (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)x, src);
+  return src;
+}
+
 template <bool kInLds>
 __device__ __forceinline__ void stage3(Leaf* rec, uint64_t* U, const PartWs& w, int nl0,
                                        const ewsjf_partition_params& p, ewsjf_queue_table* tab, int* iscr) {
@@ -703,14 +719,17 @@ __device__ __forceinline__ void stage3(Leaf* rec, uint64_t* U, const PartWs& w, 
   __syncthreads();
   if (tid < kWave) {
     const int lane = tid;
-    const int P = (nl0 + kWave - 1) / kWave;
+    // Each lane owns P slots, P the power of two >= nl0 / 64 (owners by shift).
+    int lgP = 0;
+    while ((kWave << lgP) < nl0) ++lgP;
+    const int P = 1 << lgP;
     // This lane's minimum (first index on ties) over its P slots.
     auto scan_own = [&](uint64_t& mu, int& mi) {
       mu = kInfBits + 1;  // above every utility, +inf included
       mi = 0x7fffffff;
 #pragma unroll 8
       for (int q = 0; q < P; ++q) {
-        const int i = lane * P + q;
+        const int i = (lane << lgP) + q;
         const uint64_t u = i < nl0 ? U[i] : ~0ull;
         if (u < mu) {
           mu = u;
@@ -725,22 +744,21 @@ __device__ __forceinline__ void stage3(Leaf* rec, uint64_t* U, const PartWs& w, 
     // (P <= kWave when the records are in LDS).
     auto rescan = [&](int owner) {
       if constexpr (kInLds) {
-        const int i = owner * P + lane;
+        const int i = (owner << lgP) + lane;
         const uint64_t u = (lane < P && i < nl0) ? U[i] : ~0ull;
-        const uint64_t m = wave_min_u64(u);
-        const uint64_t bal = __ballot(u == m);
+        uint64_t m;
+        const int src = wave_argmin_u64(u, &m);
         if (lane == owner) {
           lane_u = m == ~0ull ? kInfBits + 1 : m;
-          lane_i = m == ~0ull ? 0x7fffffff : owner * P + (int)__builtin_ctzll(bal);
+          lane_i = m == ~0ull ? 0x7fffffff : (owner << lgP) + src;
         }
       } else {
         if (lane == owner) scan_own(lane_u, lane_i);
       }
     };
     for (int alive = nl0; alive > p.max_queues; --alive) {
-      const uint64_t mu = wave_min_u64(lane_u);
-      const uint64_t bal = __ballot(lane_u == mu);
-      const int a = __builtin_amdgcn_readlane(lane_i, (int)__builtin_ctzll(bal));
+      uint64_t mu;
+      const int a = __builtin_amdgcn_readlane(lane_i, wave_argmin_u64(lane_u, &mu));
       const int b = rec[a].nxt, pr = rec[a].prv;
       const int64_t na = rec[a].n + rec[b].n;
       const int64_t Sa = rec[a].S + rec[b].S;
@@ -777,7 +795,7 @@ __device__ __forceinline__ void stage3(Leaf* rec, uint64_t* U, const PartWs& w, 
       // Ua), b's owner if its minimum was b (now removed), pr's owner if its
       // minimum was pr (now Upr).  A value that improves a minimum is taken
       // directly; otherwise the owner's slots are rescanned.
-      const int oa = a / P, ob = b / P, op = pr >= 0 ? pr / P : -1;
+      const int oa = a >> lgP, ob = b >> lgP, op = pr >= 0 ? pr >> lgP : -1;
       const bool lower_a = Ua < mu;  // still the global minimum: a keeps it
       bool stale = false;
       if (lane == oa) {
