@@ -457,8 +457,8 @@ def main() -> int:
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py: this build runs on one GPU only (the scheduler core has no multi-GPU path here); "
-              "use --gpus 1", file=sys.stderr)
+        print("bench.py: the scheduler core runs on one GPU; runs on several GPUs are not supported "
+              "(use --gpus 1)", file=sys.stderr)
         return 2
 
     import numpy as np
