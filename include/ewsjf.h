@@ -85,7 +85,8 @@ enum {
   EWSJF_MAX_B = 4096,        /* admissions per step per parameter vector */
   EWSJF_MAX_THETA = 1024,    /* parameter vectors per call */
   EWSJF_MAX_DISPATCH = 4096, /* requests per ewsjf_dispatch call */
-  EWSJF_TRIAL_STATS = 8      /* statistics per trial proposal (ewsjf_trial_step) */
+  EWSJF_TRIAL_STATS = 8,     /* statistics per trial proposal (ewsjf_trial_step) */
+  EWSJF_ROUTE_WORDS = EWSJF_MAX_LEN / 32 + 2 /* 64-bit words of the compact routing map */
 };
 
 /* Stage-1 initializers (Section 4.2, Stage 1). */
@@ -153,7 +154,14 @@ typedef struct {
  *                (L - hi_i against lo_{i+1} - L, ties to i); below the first
  *                queue 0, above the last k-1 (Section 4.3).
  * lut[b] = queue of length b for b in [1, max_len] under that reading
- * (longer lengths belong to queue k-1). */
+ * (longer lengths belong to queue k-1).  route[] holds the same map in
+ * 8 KiB, the form the per-step kernels stage: under either reading the queue
+ * of a length never falls and rises by at most one from one length to the
+ * next, so word w covers lengths [32 w, 32 w + 32) as the queue of length
+ * 32 w - 1 (high 32 bits; 0 for w = 0) and a mask of the lengths where the
+ * queue rises by one (low 32 bits): the queue of b in [1, max_len] is
+ * (route[b / 32] >> 32) + popcount of the mask bits 0 .. b % 32.  Lengths
+ * past max_len keep the queue of max_len.  Both are written with the table. */
 typedef struct {
   int32_t k;
   int32_t max_len;
@@ -169,6 +177,7 @@ typedef struct {
   int64_t sum[EWSJF_MAX_QUEUES];
   double mean[EWSJF_MAX_QUEUES];
   uint8_t lut[EWSJF_MAX_LEN + 16];
+  uint64_t route[EWSJF_ROUTE_WORDS];
 } ewsjf_queue_table;
 
 /* Size in bytes of the device queue table. */

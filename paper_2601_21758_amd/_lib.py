@@ -13,6 +13,7 @@ LIB_PATH = os.path.join(PKG, "libewsjf.so")
 
 OK, ERR_NULL, ERR_ARG, ERR_WORKSPACE, ERR_LAUNCH, ERR_ALIGN, ERR_DEVICE = 0, -1, -2, -3, -4, -5, -6
 MAX_QUEUES, MAX_LEN, MAX_B, MAX_THETA, MAX_DISPATCH = 256, 32768, 4096, 1024, 4096
+ROUTE_WORDS = MAX_LEN // 32 + 2
 INIT_EQUAL_WIDTH, INIT_KMEANS3 = 0, 1
 GAPS_DISTINCT, GAPS_MULTISET = 0, 1
 STEP_TOMBSTONE = 1
@@ -42,7 +43,7 @@ class QueueTable(C.Structure):
                 ("bounds", C.c_int32 * MAX_QUEUES), ("lo", C.c_int32 * MAX_QUEUES),
                 ("hi", C.c_int32 * MAX_QUEUES), ("count", C.c_int64 * MAX_QUEUES),
                 ("sum", C.c_int64 * MAX_QUEUES), ("mean", C.c_double * MAX_QUEUES),
-                ("lut", C.c_uint8 * (MAX_LEN + 16))]
+                ("lut", C.c_uint8 * (MAX_LEN + 16)), ("route", C.c_uint64 * ROUTE_WORDS)]
 
 
 class EwsjfError(RuntimeError):

@@ -17,6 +17,9 @@ CSRC = os.path.join(PKG, "csrc")
 INC = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libewsjf.so")
 BUILD = os.path.join(PKG, "_build")
+# The instrumented variant (phase stamps, read by phase_stamps.py).
+LIB_STAMPS = os.path.join(PKG, "libewsjf_stamps.so")
+BUILD_STAMPS = os.path.join(PKG, "_build_stamps")
 SOURCES = ["abi.hip", "kern_policy.hip", "kern_select.hip", "kern_partition.hip", "kern_tactical.hip",
            "kern_dispatch.hip", "kern_trial.hip"]
 
@@ -26,9 +29,9 @@ FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-ffp-contract=o
          "-Wall", "-Wno-unused-result", "-I", INC, "-I", CSRC]
 
 
-def _compile(src: str, verbose: bool) -> str:
-    obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-    cmd = [HIPCC, *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+def _compile(src: str, verbose: bool, stamps: bool = False) -> str:
+    obj = os.path.join(BUILD_STAMPS if stamps else BUILD, os.path.splitext(src)[0] + ".o")
+    cmd = [HIPCC, *FLAGS, *(["-DEWSJF_STAMPS"] if stamps else []), "-c", os.path.join(CSRC, src), "-o", obj]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
@@ -40,18 +43,21 @@ def _compile(src: str, verbose: bool) -> str:
     return obj
 
 
-def build(verbose: bool = False) -> str:
-    os.makedirs(BUILD, exist_ok=True)
+def build(verbose: bool = False, stamps: bool = False) -> str:
+    """Build libewsjf.so, or with stamps=True the instrumented
+    libewsjf_stamps.so (same kernels plus phase timestamps)."""
+    lib = LIB_STAMPS if stamps else LIB
+    os.makedirs(BUILD_STAMPS if stamps else BUILD, exist_ok=True)
     with ThreadPoolExecutor(max_workers=4) as ex:
-        objs = list(ex.map(lambda s: _compile(s, verbose), SOURCES))
-    tmp = LIB + ".tmp"
+        objs = list(ex.map(lambda s: _compile(s, verbose, stamps), SOURCES))
+    tmp = lib + ".tmp"
     cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, lib)
+    return lib
 
 
 if __name__ == "__main__":
-    print(build(verbose="-v" in sys.argv))
+    print(build(verbose="-v" in sys.argv, stamps="--stamps" in sys.argv))

@@ -15,6 +15,7 @@
 namespace {
 
 static_assert(offsetof(ewsjf_queue_table, lut) % 16 == 0, "routing lut must be 16-byte aligned");
+static_assert(offsetof(ewsjf_queue_table, route) % 16 == 0, "routing map must be 16-byte aligned");
 static_assert(sizeof(ewsjf_partition_params) == 40, "ABI layout");
 static_assert(sizeof(ewsjf_cost) == 24, "ABI layout");
 

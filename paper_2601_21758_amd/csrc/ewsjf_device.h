@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "ewsjf.h"
 
 namespace ewsjf {
@@ -47,6 +49,27 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t chunk_rsrc(const void* chunk_b
 
 __device__ __forceinline__ i32x4 chunk_load_i32x4(__amdgpu_buffer_rsrc_t rs, int lane) {
   return __builtin_amdgcn_raw_buffer_load_b128(rs, lane * 16, 0, kCachePolicyNT);
+}
+
+// A zero held in a vector register that the compiler cannot see through.
+// Loads indexed by it stay vector loads, counted in issue order with the
+// pool loads, instead of becoming scalar loads, whose waits also cover LDS
+// traffic.
+__device__ __forceinline__ int opaque_zero() {
+  int z;
+  asm volatile("v_mov_b32 %0, 0" : "=v"(z));
+  return z;
+}
+
+// Values the compiler must treat as produced at this point (an empty asm
+// that "modifies" them), so no computation on them moves above it.
+__device__ __forceinline__ void pin_one(float& x) { asm volatile("" : "+v"(x)); }
+__device__ __forceinline__ void pin_one(int& x) { asm volatile("" : "+v"(x)); }
+__device__ __forceinline__ void pin_one(double& x) { asm volatile("" : "+v"(x)); }
+__device__ __forceinline__ void pin_one(i32x4& x) { asm volatile("" : "+v"(x)); }
+template <class... T>
+__device__ __forceinline__ void pin(T&... x) {
+  (pin_one(x), ...);
 }
 
 // Per-queue scoring constants derived from one parameter vector, each already
@@ -305,6 +328,31 @@ __device__ __forceinline__ uint64_t xor_lane_u64_dyn(uint64_t x, int j) {
     case 16: return xor_lane_u64<16>(x);
     default: return xor_lane_u64<32>(x);
   }
+}
+
+// Descending bitonic sort of one value per lane across the wave: lane i
+// returns the value of rank i.  21 lane-exchange steps, no LDS.
+__device__ __forceinline__ uint64_t wave_sort_desc(uint64_t x) {
+  const int lane = threadIdx.x & (kWave - 1);
+  auto stage = [&](auto jc, int k) {
+    constexpr int j = decltype(jc)::value;
+    const uint64_t y = xor_lane_u64<j>(x);
+    const bool keep_max = ((lane & j) == 0) == ((lane & k) == 0);
+    x = keep_max ? (x > y ? x : y) : (x < y ? x : y);
+  };
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+  using I4 = std::integral_constant<int, 4>;
+  using I8 = std::integral_constant<int, 8>;
+  using I16 = std::integral_constant<int, 16>;
+  using I32 = std::integral_constant<int, 32>;
+  stage(I1{}, 2);
+  stage(I2{}, 4), stage(I1{}, 4);
+  stage(I4{}, 8), stage(I2{}, 8), stage(I1{}, 8);
+  stage(I8{}, 16), stage(I4{}, 16), stage(I2{}, 16), stage(I1{}, 16);
+  stage(I16{}, 32), stage(I8{}, 32), stage(I4{}, 32), stage(I2{}, 32), stage(I1{}, 32);
+  stage(I32{}, 64), stage(I16{}, 64), stage(I8{}, 64), stage(I4{}, 64), stage(I2{}, 64), stage(I1{}, 64);
+  return x;
 }
 
 __device__ __forceinline__ void cmpx_desc(uint64_t& a, uint64_t& b, bool desc) {
@@ -606,6 +654,14 @@ __device__ inline void stage_policy(const ewsjf_queue_table* tab, const ewsjf_th
   if (theta != nullptr) {
     for (int q = threadIdx.x; q < k; q += blockDim.x) qp[q] = make_qparams(*theta, tab->mean[q], q);
   }
+}
+
+// Queue of length b in [1, L] from the table's compact routing map: the
+// queue of length 32 (b / 32) - 1 plus the rises at lengths 32 (b / 32) .. b.
+constexpr int kRouteWords = EWSJF_ROUTE_WORDS;
+__device__ __forceinline__ int route_queue(const uint64_t* route, int b) {
+  const uint64_t w = route[b >> 5];
+  return (int)(uint32_t)(w >> 32) + __builtin_popcount((uint32_t)w << (31 - (b & 31)));
 }
 
 __device__ __forceinline__ int route_lut(int b, int L, const uint8_t* lut) {

@@ -62,48 +62,97 @@ __device__ __forceinline__ uint8_t lut_entry(int e, int L, bool gapped, P bounds
 
 constexpr int kLutWords = (EWSJF_MAX_LEN + 16) / 4;
 
-// Thread t of nthreads writes its share of the lut's 32-bit words: one
-// search places its first length, then the walk up the length axis moves to
-// the next queue start (or bound) as it is passed, and four entries go out
-// per store.  The same entries as lut_entry.
+// A walk up the length axis that gives the queue of each length in turn
+// (the same queue as lut_entry): one search places the walk's first
+// length, then the walk moves to the next queue start (or bound) as it is
+// passed.  Lengths must be visited one by one in increasing order from the
+// first, all within [1, L].
+template <class P>
+struct QueueWalk {
+  P bounds, lo, hi;
+  int k;
+  bool gapped;
+  // gapped: i = last queue starting at or below the length, nxt = the next
+  // start; contiguous: i = bounds passed, nxt = the next bound
+  int i, hi_i, nxt;
+  static constexpr int kBig = 0x7fffffff;
+
+  __device__ __forceinline__ void start(int b0) {
+    i = gapped ? count_le(lo, k, b0) - 1 : count_le(bounds, k - 1, b0);
+    hi_i = gapped && i >= 0 ? hi[i] : 0;
+    nxt = gapped ? (i + 1 < k ? lo[i + 1] : kBig) : (i < k - 1 ? bounds[i] : kBig);
+  }
+
+  __device__ __forceinline__ int at(int x) {
+    if (x >= nxt) {  // starts and bounds strictly increase, so at most one per length
+      ++i;
+      if (gapped) {
+        hi_i = hi[i];
+        nxt = i + 1 < k ? lo[i + 1] : kBig;
+      } else {
+        nxt = i < k - 1 ? bounds[i] : kBig;
+      }
+    }
+    if (!gapped || i < 0 || x <= hi_i || i == k - 1) return i < 0 ? 0 : i;
+    const int tq = gap_tolerance(x, hi_i, nxt, i);
+    return tq >= 0 ? tq : gap_nearer(x, hi_i, nxt, i);
+  }
+};
+
+// Thread t of nthreads writes its share of the lut's 32-bit words, four
+// entries per store.  The same entries as lut_entry.
 template <class P>
 __device__ void lut_fill(uint8_t* lut, int t, int nthreads, int L, bool gapped, P bounds, P lo, P hi, int k) {
   const int per = (kLutWords + nthreads - 1) / nthreads;
   const int w0 = t * per, w1 = min(kLutWords, w0 + per);
   if (w0 >= w1) return;
-  const int big = 0x7fffffff;
-  const int b0 = max(4 * w0, 1);
-  // gapped: i = last queue starting at or below the length, nxt = the next start;
-  // contiguous: i = bounds passed, nxt = the next bound
-  int i = gapped ? count_le(lo, k, b0) - 1 : count_le(bounds, k - 1, b0);
-  int hi_i = gapped && i >= 0 ? hi[i] : 0;
-  int nxt = gapped ? (i + 1 < k ? lo[i + 1] : big) : (i < k - 1 ? bounds[i] : big);
+  QueueWalk<P> qw{bounds, lo, hi, k, gapped, 0, 0, 0};
+  qw.start(max(4 * w0, 1));
   for (int w = w0; w < w1; ++w) {
     uint32_t word = 0;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int x = 4 * w + j;
-      int q = 0;
-      if (x >= 1 && x <= L) {
-        if (x >= nxt) {  // starts and bounds strictly increase, so at most one per length
-          ++i;
-          if (gapped) {
-            hi_i = hi[i];
-            nxt = i + 1 < k ? lo[i + 1] : big;
-          } else {
-            nxt = i < k - 1 ? bounds[i] : big;
-          }
-        }
-        if (!gapped || i < 0 || x <= hi_i || i == k - 1) {
-          q = i < 0 ? 0 : i;
-        } else {
-          const int tq = gap_tolerance(x, hi_i, nxt, i);
-          q = tq >= 0 ? tq : gap_nearer(x, hi_i, nxt, i);
-        }
-      }
+      const int q = (x >= 1 && x <= L) ? qw.at(x) : 0;
       word |= (uint32_t)q << (8 * j);
     }
     *reinterpret_cast<uint32_t*>(lut + 4 * w) = word;
+  }
+}
+
+// Thread t of nthreads writes its share of the compact routing map (the
+// table's route words): word w = (queue of length 32 w - 1) << 32 | the
+// mask of lengths 32 w + j in [1, L] whose queue is one above the queue of
+// the length before.  Under both readings the queue of a length never falls
+// and rises by at most one per length (contiguous bounds strictly increase;
+// in the gapped reading each gap is split once, lower part to the lower
+// queue), so the mask and the base give every queue.  Lengths past L keep
+// the queue of L.
+template <class P>
+__device__ void route_fill(uint64_t* route, int t, int nthreads, int L, bool gapped, P bounds, P lo, P hi, int k) {
+  const int per = (kRouteWords + nthreads - 1) / nthreads;
+  const int w0 = t * per, w1 = min(kRouteWords, w0 + per);
+  if (w0 >= w1) return;
+  QueueWalk<P> qw{bounds, lo, hi, k, gapped, 0, 0, 0};
+  int prev = 0;  // queue of length 32 w0 - 1 (lengths <= 0 count as queue 0)
+  if (w0 == 0) {
+    qw.start(1);
+  } else {
+    const int x = min(32 * w0 - 1, L);
+    qw.start(x);
+    prev = qw.at(x);
+  }
+  for (int w = w0; w < w1; ++w) {
+    const uint32_t base = (uint32_t)prev;
+    uint32_t mask = 0;
+    for (int j = 0; j < 32; ++j) {
+      const int x = 32 * w + j;
+      if (x < 1 || x > L) continue;
+      const int q = qw.at(x);
+      mask |= (uint32_t)(q != prev) << j;
+      prev = q;
+    }
+    route[w] = ((uint64_t)base << 32) | mask;
   }
 }
 

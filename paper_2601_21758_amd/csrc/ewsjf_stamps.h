@@ -1,0 +1,49 @@
+// Phase timestamps for the instrumented build (compiled with -DEWSJF_STAMPS
+// into libewsjf_stamps.so; paper_2601_21758_amd/phase_stamps.py reads them).
+// Thread 0 of workgroup (x < kStampBlocks, y == 0) of a kernel records the
+// device's constant 100 MHz clock at numbered points of the kernel.  In the
+// regular build EWSJF_STAMP expands to nothing.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ewsjf {
+
+constexpr int kStampKernels = 4;
+constexpr int kStampBlocks = 256;
+constexpr int kStampPhases = 8;
+constexpr int kStampSlots = kStampKernels * kStampBlocks * kStampPhases;
+
+// Kernel ids of the stamps.
+enum { kStampLocal = 0, kStampMergeRank = 1, kStampMergeExact = 2, kStampMulti = 3 };
+
+}  // namespace ewsjf
+
+#ifdef EWSJF_STAMPS
+namespace ewsjf {
+// One copy per translation unit that includes this header (no relocatable
+// device code): the select kernels' unit owns the one that is read.
+static __device__ uint64_t g_stamps[kStampSlots];
+}  // namespace ewsjf
+#define EWSJF_STAMP(kid, phase)                                                                            \
+  do {                                                                                                     \
+    if (threadIdx.x == 0 && blockIdx.y == 0 && blockIdx.x < (unsigned)::ewsjf::kStampBlocks)               \
+      ::ewsjf::g_stamps[((kid) * ::ewsjf::kStampBlocks + blockIdx.x) * ::ewsjf::kStampPhases + (phase)] =  \
+          __builtin_amdgcn_s_memrealtime();                                                                \
+  } while (0)
+// A value in place of a time (read back as is).
+#define EWSJF_STAMP_VALUE(kid, phase, value)                                                               \
+  do {                                                                                                     \
+    if (threadIdx.x == 0 && blockIdx.y == 0 && blockIdx.x < (unsigned)::ewsjf::kStampBlocks)               \
+      ::ewsjf::g_stamps[((kid) * ::ewsjf::kStampBlocks + blockIdx.x) * ::ewsjf::kStampPhases + (phase)] =  \
+          (uint64_t)(value);                                                                               \
+  } while (0)
+#else
+#define EWSJF_STAMP(kid, phase) \
+  do {                          \
+  } while (0)
+#define EWSJF_STAMP_VALUE(kid, phase, value) \
+  do {                                       \
+  } while (0)
+#endif

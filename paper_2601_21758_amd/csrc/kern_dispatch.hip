@@ -201,6 +201,7 @@ __global__ __launch_bounds__(kBlock) void dispatch_kernel(const int32_t* __restr
     tab->gapped = 1;
   }
   lut_fill(tab->lut, tid, kBlock, L, true, sm.lo, sm.lo, sm.hi, k1);
+  route_fill(tab->route, tid, kBlock, L, true, sm.lo, sm.lo, sm.hi, k1);
 }
 
 }  // namespace

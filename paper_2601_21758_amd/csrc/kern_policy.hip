@@ -15,6 +15,8 @@ __global__ __launch_bounds__(256) void build_lut_kernel(ewsjf_queue_table* tab) 
   const int t = blockIdx.x * blockDim.x + threadIdx.x;
   lut_fill(tab->lut, t, gridDim.x * blockDim.x, tab->max_len, tab->gapped != 0, tab->bounds, tab->lo, tab->hi,
            tab->k);
+  route_fill(tab->route, t, gridDim.x * blockDim.x, tab->max_len, tab->gapped != 0, tab->bounds, tab->lo, tab->hi,
+             tab->k);
 }
 
 hipError_t launch_build_lut(ewsjf_queue_table* table, hipStream_t stream) {

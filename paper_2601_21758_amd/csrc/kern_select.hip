@@ -25,6 +25,7 @@
 
 #include "ewsjf_device.h"
 #include "ewsjf_launch.h"
+#include "ewsjf_stamps.h"
 
 namespace ewsjf {
 
@@ -42,51 +43,67 @@ struct PoolSource {
   float now;
   CostF cost;
 
-  static constexpr int kLutVecs = kLutBytes / 16;                                     // 2049
-  static constexpr int kLutPerThread = (kLutVecs + kStageThreads - 1) / kStageThreads;  // 9
+  static constexpr int kRouteVecs = kRouteWords / 2;                                        // 513
+  static constexpr int kRoutePerThread = (kRouteVecs + kStageThreads - 1) / kStageThreads;  // 3
 
   struct Raw {
     i32x4 l;
     f32x4 a;
   };
   struct Shared {
-    uint8_t lut[kLutBytes];
+    uint64_t route[kRouteWords];
     QParams qp[EWSJF_MAX_QUEUES];
     int L;
   };
   struct Stage {
-    i32x4 v[kLutPerThread];
+    i32x4 v[kRoutePerThread];
     double mean;
-    int t;
+    i32x4 hdr;    // k, max_len, ...
+    float th[6];  // the parameter vector
   };
 
-  // Run by the first kStageThreads threads.  Branch-free on purpose: every
-  // load is issued unconditionally (the lookup table and the mean array are
-  // read whole, indices clamped into them).  The table's scalars and the
-  // parameter vector are read in stage_store: read here, their first use
-  // (hoisted by the compiler) put a wait for them ahead of the barrier that
-  // releases the pool loads, which then started one memory round trip late.
+  // Run by the first kStageThreads threads, before any pool load is issued.
+  // Branch-free on purpose: every load is issued unconditionally (the routing
+  // map and the mean array are read whole, indices clamped into them).  The
+  // table's header and the parameter vector are read with vector loads too
+  // (opaque_zero): scalar loads, issued here or after the pool loads, put
+  // their wait (which also covers LDS traffic) ahead of a barrier, or
+  // queued behind the pool stream.
   __device__ __forceinline__ void stage_load(Stage& st, int t) const {
-    const i32x4* src = reinterpret_cast<const i32x4*>(table->lut);
+    const int z = opaque_zero();
+    const i32x4* src = reinterpret_cast<const i32x4*>(table->route);
 #pragma unroll
-    for (int r = 0; r < kLutPerThread; ++r) {
+    for (int r = 0; r < kRoutePerThread; ++r) {
       const int i = threadIdx.x + r * kStageThreads;
-      st.v[r] = src[i < kLutVecs ? i : i - kStageThreads];  // a past-the-end slot reloads an earlier one
+      st.v[r] = src[i < kRouteVecs ? i : i - kStageThreads];  // a past-the-end slot reloads an earlier one
     }
     static_assert(EWSJF_MAX_QUEUES == kStageThreads, "one mean per staging thread");
     st.mean = table->mean[threadIdx.x];
-    st.t = t;
+    st.hdr = reinterpret_cast<const i32x4*>(table)[z];
+    const float2* tp = reinterpret_cast<const float2*>(theta + t);
+#pragma unroll
+    for (int j = 0; j < 3; ++j) {
+      const float2 w = tp[z + j];
+      st.th[2 * j] = w.x;
+      st.th[2 * j + 1] = w.y;
+    }
   }
 
-  __device__ __forceinline__ void stage_store(Shared& sh, const Stage& st) const {
-    i32x4* dst = reinterpret_cast<i32x4*>(sh.lut);
+  __device__ __forceinline__ void stage_store(Shared& sh, const Stage& st0) const {
+    // Pin the staged values here: the compiler would otherwise convert them
+    // (binary32 -> binary64) right after their loads, waiting for them ahead
+    // of the pool loads.
+    Stage st = st0;
+    pin(st.th[0], st.th[1], st.th[2], st.th[3], st.th[4], st.th[5], st.hdr, st.mean);
+    i32x4* dst = reinterpret_cast<i32x4*>(sh.route);
 #pragma unroll
-    for (int r = 0; r < kLutPerThread; ++r) {
+    for (int r = 0; r < kRoutePerThread; ++r) {
       const int i = threadIdx.x + r * kStageThreads;
-      if (r + 1 < kLutPerThread || i < kLutVecs) dst[i] = st.v[r];
+      if (r + 1 < kRoutePerThread || i < kRouteVecs) dst[i] = st.v[r];
     }
-    if ((int)threadIdx.x < table->k) sh.qp[threadIdx.x] = make_qparams(theta[st.t], st.mean, threadIdx.x);
-    if (threadIdx.x == 0) sh.L = table->max_len;
+    const ewsjf_theta th{st.th[0], st.th[1], st.th[2], st.th[3], st.th[4], st.th[5]};
+    if ((int)threadIdx.x < st.hdr.x) sh.qp[threadIdx.x] = make_qparams(th, st.mean, threadIdx.x);
+    if (threadIdx.x == 0) sh.L = st.hdr.y;
   }
 
   __device__ __forceinline__ Raw load4(int64_t base, int64_t n) const {
@@ -115,8 +132,8 @@ struct PoolSource {
   }
 
   __device__ __forceinline__ uint32_t key1(int b, float a, const Shared& sh) const {
-    const int bc = min(max(b, 0), sh.L);
-    const float phi = phi_f32(b, a, now, sh.qp[sh.lut[bc]], cost);
+    const int bc = min(max(b, 1), sh.L);
+    const float phi = phi_f32(b, a, now, sh.qp[route_queue(sh.route, bc)], cost);
     return b > 0 ? ukey_fast(phi) : 0u;
   }
 
@@ -142,43 +159,49 @@ struct FifoSource {
   const ewsjf_queue_table* table;
   const TacticalPlan* plan;
 
-  static constexpr int kLutVecs = kLutBytes / 16;
-  static constexpr int kLutPerThread = (kLutVecs + kStageThreads - 1) / kStageThreads;
+  static constexpr int kRouteVecs = kRouteWords / 2;
+  static constexpr int kRoutePerThread = (kRouteVecs + kStageThreads - 1) / kStageThreads;
 
   struct Raw {
     i32x4 l;
     f32x4 a;
   };
   struct Shared {
-    uint8_t lut[kLutBytes];
+    uint64_t route[kRouteWords];
     int L;
     int qsel;
   };
   struct Stage {
-    i32x4 v[kLutPerThread];
-    int t;
+    i32x4 v[kRoutePerThread];
+    i32x4 hdr;  // k, max_len, ...
+    int qsel;
   };
 
+  // As PoolSource::stage_load: vector loads only, issued before the pool's.
   __device__ __forceinline__ void stage_load(Stage& st, int t) const {
-    const i32x4* src = reinterpret_cast<const i32x4*>(table->lut);
+    const int z = opaque_zero();
+    const i32x4* src = reinterpret_cast<const i32x4*>(table->route);
 #pragma unroll
-    for (int r = 0; r < kLutPerThread; ++r) {
+    for (int r = 0; r < kRoutePerThread; ++r) {
       const int i = threadIdx.x + r * kStageThreads;
-      st.v[r] = src[i < kLutVecs ? i : i - kStageThreads];  // a past-the-end slot reloads an earlier one
+      st.v[r] = src[i < kRouteVecs ? i : i - kStageThreads];  // a past-the-end slot reloads an earlier one
     }
-    st.t = t;
+    st.hdr = reinterpret_cast<const i32x4*>(table)[z];
+    st.qsel = plan->q_sel[t + z];
   }
 
-  __device__ __forceinline__ void stage_store(Shared& sh, const Stage& st) const {
-    i32x4* dst = reinterpret_cast<i32x4*>(sh.lut);
+  __device__ __forceinline__ void stage_store(Shared& sh, const Stage& st0) const {
+    Stage st = st0;
+    pin(st.hdr, st.qsel);
+    i32x4* dst = reinterpret_cast<i32x4*>(sh.route);
 #pragma unroll
-    for (int r = 0; r < kLutPerThread; ++r) {
+    for (int r = 0; r < kRoutePerThread; ++r) {
       const int i = threadIdx.x + r * kStageThreads;
-      if (r + 1 < kLutPerThread || i < kLutVecs) dst[i] = st.v[r];
+      if (r + 1 < kRoutePerThread || i < kRouteVecs) dst[i] = st.v[r];
     }
     if (threadIdx.x == 0) {
-      sh.L = table->max_len;
-      sh.qsel = plan->q_sel[st.t];
+      sh.L = st.hdr.y;
+      sh.qsel = st.qsel;
     }
   }
 
@@ -207,8 +230,8 @@ struct FifoSource {
   }
 
   __device__ __forceinline__ uint32_t key1(int b, float a, const Shared& sh) const {
-    const int bc = min(max(b, 0), sh.L);
-    return (b > 0 && (int)sh.lut[bc] == sh.qsel) ? fifo_key(a) : 0u;
+    const int bc = min(max(b, 1), sh.L);
+    return (b > 0 && route_queue(sh.route, bc) == sh.qsel) ? fifo_key(a) : 0u;
   }
 
   __device__ __forceinline__ void keys4(const Raw& r, const Shared& sh, uint32_t out[4]) const {
@@ -385,6 +408,7 @@ struct ListShared {
   int rank[kShortList];  // ranks of a short list, summed over the waves
   uint32_t bar[kWavesPerBlock];
   int wcnt[kWavesPerBlock];
+  int wkeep[kWavesPerBlock];
   int ovf;
   int nout;
   int nspill;
@@ -516,6 +540,31 @@ __device__ __forceinline__ void publish_list(ListShared& ls, int cnt, uint64_t l
   if (threadIdx.x == 0) cb.over_cnt[slot] = (uint32_t)(listed - M);
 }
 
+// publish_list for a list of M < cnt <= kWave entries, by one wave (the
+// caller's; every lane of it calls): the wave sorts the list, one entry per
+// lane, so lane i holds the entry of rank i and places it.  No barrier.
+constexpr int kShortWave = kWave;
+__device__ __forceinline__ void publish_list_wave(const ListShared& ls, int cnt, uint64_t lowc, int M, size_t slot,
+                                                  const CandBufs& cb) {
+  const int lane = threadIdx.x & (kWave - 1);
+  uint64_t* out_list = cb.lists + slot * (size_t)M;
+  uint64_t* over_list = cb.over + slot * (size_t)kOverCap;
+  const int listed = min(cnt, M + kOverCap);
+  const uint64_t x = wave_sort_desc(lane < cnt ? ls.list2[lane] : 0ull);  // rank = lane
+  if (lane < M) out_list[lane] = x;
+  else if (lane < listed) over_list[lane - M] = x;
+  if (lane == M - 1) {
+    cb.counts[slot] = (uint32_t)M;
+    cb.bounds[slot] = x > lowc ? x : lowc;
+  }
+  if (lane == listed - 1) cb.bounds2[slot] = (cnt <= M + kOverCap || x < lowc) ? lowc : x;
+  if (lane == 0) cb.over_cnt[slot] = (uint32_t)(listed - M);
+}
+
+// Chunks each wave has in flight when it starts scoring (2, 3 or 4).
+constexpr int kAhead = 2;
+static_assert(kAhead >= 2 && kAhead <= kChunksPerPass, "chunks in flight");
+
 template <class Src>
 __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, int G, int lg, int M, CandBufs cb) {
   __shared__ typename Src::Shared sh;
@@ -533,6 +582,7 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
     }
     return;
   }
+  EWSJF_STAMP(kStampLocal, 0);
   const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
   const int64_t nchunks = (n + kChunk - 1) / kChunk;
   const int64_t my_chunks = nchunks > blockIdx.x ? (nchunks - blockIdx.x + G - 1) / G : 0;
@@ -555,6 +605,8 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
   typename Src::Raw raw[kChunksPerPass];
   load_one(src, n, G, 0, 0, raw[0]);
   load_one(src, n, G, 0, 1, raw[1]);
+  if constexpr (kAhead >= 3) load_one(src, n, G, 0, 2, raw[2]);
+  if constexpr (kAhead >= 4) load_one(src, n, G, 0, 3, raw[3]);
   if (stager) src.stage_store(sh, st);
   if (threadIdx.x == 0) {
     ls.ovf = 0;
@@ -566,6 +618,7 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
   static_assert(kListCap == kBlock, "one spill entry per thread");
   if constexpr (Src::kClustered) ls.spill[threadIdx.x] = 0ull;
   __syncthreads();
+  EWSJF_STAMP(kStampLocal, 1);
 
   // Each wave writes every element whose key is >= its bar into its own
   // region of the list.  The bar (wave_group_bar over the lane maxima of the
@@ -582,14 +635,16 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
     // A wave stalls at a load while the memory pipeline is full, so it
     // scores a chunk that has arrived before it issues the next load; the
     // other waves keep the pipeline full meanwhile.
+    // Chunk j >= kAhead is issued once chunk j - kAhead is scored.
     sched_fence();
     src.keys4(raw[0], sh, key + 0);
     sched_fence();
-    load_one(src, n, G, pass, 2, raw[2]);
+    if constexpr (kAhead == 2) load_one(src, n, G, pass, 2, raw[2]);
+    if constexpr (kAhead == 3) load_one(src, n, G, pass, 3, raw[3]);
     sched_fence();
     src.keys4(raw[1], sh, key + 4);
     sched_fence();
-    load_one(src, n, G, pass, 3, raw[3]);
+    if constexpr (kAhead == 2) load_one(src, n, G, pass, 3, raw[3]);
     sched_fence();
     src.keys4(raw[2], sh, key + 8);
     // The bar comes from the first three chunks, so it is ready while the
@@ -601,10 +656,12 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
     const uint32_t bar = wave_group_bar(lmax, lg);
     src.keys4(raw[3], sh, key + 12);
     sched_fence();
-    // The next pass's first two chunks (empty after the last pass): without
-    // a branch, so waits on the loads above keep their exact counts.
+    // The next pass's first chunks (empty after the last pass): without a
+    // branch, so waits on the loads above keep their exact counts.
     load_one(src, n, G, pass + 1, 0, raw[0]);
     load_one(src, n, G, pass + 1, 1, raw[1]);
+    if constexpr (kAhead >= 3) load_one(src, n, G, pass + 1, 2, raw[2]);
+    if constexpr (kAhead >= 4) load_one(src, n, G, pass + 1, 3, raw[3]);
     sched_fence();
     my_bar = bar > my_bar ? bar : my_bar;
     // Per element slot: one compare; the wave's mask of qualifying lanes
@@ -685,12 +742,14 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
       wcnt = __popcll(km);
     }
   }
+  EWSJF_STAMP(kStampLocal, 2);
   if (lane == 0) {
     ls.bar[wv] = my_bar;
     ls.wcnt[wv] = wcnt;
     if (wovf) ls.ovf = 1;
   }
   __syncthreads();
+  EWSJF_STAMP(kStampLocal, 3);
 
   // Publish into the workgroup's M fixed slots (unused slots hold 0).
   const size_t slot = (size_t)t * G + blockIdx.x;
@@ -703,6 +762,33 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
       cb.bounds2[slot] = ~0ull;
       cb.over_cnt[slot] = 0u;
     }
+    return;
+  }
+  if constexpr (!Src::kClustered) {
+    // The workgroup's bound: the largest wave bar (lane i < 16 reads wave i's).
+    // Each wave keeps its entries at or above it; a scan of the kept counts
+    // over the waves places them in list2.
+    const uint32_t T_bar = wave_max_u32(lane < kWavesPerBlock ? ls.bar[lane] : 0u);
+    const uint64_t lowc = (uint64_t)T_bar << 32;
+    const uint64_t x = lane < ls.wcnt[wv] ? region[lane] : 0ull;
+    const bool keep = x >= lowc && x != 0ull;
+    const uint64_t km = __ballot(keep);
+    if (lane == 0) ls.wkeep[wv] = __popcll(km);
+    __syncthreads();
+    const int kc = lane < kWavesPerBlock ? ls.wkeep[lane] : 0;
+    const int incl = wave_incl_scan_add(kc);
+    const int total = __builtin_amdgcn_readlane(incl, kWavesPerBlock - 1);
+    const int off = __builtin_amdgcn_readlane(incl - kc, wv);
+    if (keep) ls.list2[off + lanes_below(km)] = x;  // total <= kListCap: at most kWave per wave
+    __syncthreads();
+    EWSJF_STAMP(kStampLocal, 4);
+    EWSJF_STAMP_VALUE(kStampLocal, 6, total);
+    if (total > M && total <= kShortWave) {  // uniform: one wave ranks and places
+      if (wv == 0) publish_list_wave(ls, total, lowc, M, slot, cb);
+    } else {
+      publish_list<false>(ls, total, lowc, M, slot, cb);
+    }
+    EWSJF_STAMP(kStampLocal, 5);
     return;
   }
   // The workgroup's bound: the largest wave bar t1.  When the wave holding
@@ -768,7 +854,10 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
   keep_into_list2(lane < ls.wcnt[wv] ? ls.list[threadIdx.x] : 0ull);
   if (Src::kClustered && ls.nspill != 0) keep_into_list2(ls.spill[threadIdx.x]);  // uniform
   __syncthreads();
+  EWSJF_STAMP(kStampLocal, 4);
+  EWSJF_STAMP_VALUE(kStampLocal, 6, ls.nout);
   publish_list<false>(ls, ls.nout, lowc, M, slot, cb);
+  EWSJF_STAMP(kStampLocal, 5);
 }
 
 
@@ -790,7 +879,7 @@ constexpr int kThetaPerBlock = 16;
 
 __global__ __launch_bounds__(kBlock) void local_candidates_multi(PoolSource src, int64_t n, int n_theta, int G,
                                                                  int lg, int M, CandBufs cb) {
-  __shared__ uint8_t lut[kLutBytes];
+  __shared__ uint64_t route[kRouteWords];
   __shared__ QParams qp[kThetaPerBlock][EWSJF_MAX_QUEUES];
   __shared__ ListShared ls;
   __shared__ int s_ovf[2], s_nout[2];
@@ -804,9 +893,9 @@ __global__ __launch_bounds__(kBlock) void local_candidates_multi(PoolSource src,
 #pragma unroll
   for (int j = 0; j < kChunksPerPass; ++j) raw[j] = src.load_chunk(chunk_of(G, 0, j), n, lane);
   {
-    const i32x4* lsrc = reinterpret_cast<const i32x4*>(src.table->lut);
-    i32x4* ldst = reinterpret_cast<i32x4*>(lut);
-    for (int i = tid; i < kLutBytes / 16; i += kBlock) ldst[i] = lsrc[i];
+    const i32x4* lsrc = reinterpret_cast<const i32x4*>(src.table->route);
+    i32x4* ldst = reinterpret_cast<i32x4*>(route);
+    for (int i = tid; i < kRouteWords / 2; i += kBlock) ldst[i] = lsrc[i];
     const int k = src.table->k;
     for (int i = tid; i < nt * EWSJF_MAX_QUEUES; i += kBlock) {
       const int tt = i / EWSJF_MAX_QUEUES, q = i % EWSJF_MAX_QUEUES;
@@ -827,7 +916,7 @@ __global__ __launch_bounds__(kBlock) void local_candidates_multi(PoolSource src,
 #pragma unroll
   for (int e = 0; e < kElemsPerLane; ++e) {
     const int b = raw[e / 4].l[e & 3];
-    qv[e] = b > 0 ? (int)lut[min(b, L)] : -1;
+    qv[e] = b > 0 ? route_queue(route, min(b, L)) : -1;
     tm[e] = phi_terms(b, raw[e / 4].a[e & 3], src.now, src.cost);
   }
 
@@ -1017,15 +1106,26 @@ __device__ inline int merge_new(MergeShared& ms, int U0, int k, int B) {
   return total;
 }
 
+// LDS of the exact merge.
 template <class Src>
-__global__ __launch_bounds__(kBlock) void merge_candidates(Src src0, int64_t n, int G, int M, int B, CandBufs cb,
-                                                           int32_t* __restrict__ ids, float* __restrict__ top,
-                                                           int32_t* __restrict__ n_sel, int32_t* tomb_len) {
-  __shared__ MergeShared ms;
-  __shared__ typename Src::Shared sh;
-  __shared__ uint64_t sT[kMaxGrid];
-  __shared__ uint64_t sT2[kMaxGrid];
-  const int t = blockIdx.x;
+struct MergeLds {
+  MergeShared ms;
+  typename Src::Shared sh;
+  uint64_t sT[kMaxGrid];
+  uint64_t sT2[kMaxGrid];
+};
+
+// The exact top-B of row t (one workgroup): the union of the lists, then the
+// recovery of shares whose lists could miss members of the top-B.
+template <class Src>
+__device__ void merge_exact(const Src& src0, int t, int64_t n, int G, int M, int B, const CandBufs& cb,
+                            int32_t* __restrict__ ids, float* __restrict__ top, int32_t* __restrict__ n_sel,
+                            int32_t* tomb_len, MergeLds<Src>& lds) {
+  EWSJF_STAMP(kStampMergeExact, 0);
+  MergeShared& ms = lds.ms;
+  typename Src::Shared& sh = lds.sh;
+  uint64_t* sT = lds.sT;
+  uint64_t* sT2 = lds.sT2;
   const int tid = threadIdx.x;
   const Src src = bind_theta(src0, t);
   const size_t slot0 = (size_t)t * G;
@@ -1156,6 +1256,7 @@ __global__ __launch_bounds__(kBlock) void merge_candidates(Src src0, int64_t n, 
     }
   }
   uint64_t tau = (U >= B) ? ms.X[B - 1] : 0ull;
+  EWSJF_STAMP(kStampMergeExact, 1);
 
   // Shares whose slots could miss top-B members (rare), largest bound first:
   // each adds its entries in [cut, bound) -- from its overflow list when that
@@ -1285,6 +1386,174 @@ __global__ __launch_bounds__(kBlock) void merge_candidates(Src src0, int64_t n, 
   if (tomb_len != nullptr) {
     for (int r = tid; r < sel; r += kBlock) tomb_len[comp_id(ms.X[r])] = 0;
   }
+  EWSJF_STAMP(kStampMergeExact, 2);
+}
+
+template <class Src>
+__global__ __launch_bounds__(kBlock) void merge_candidates(Src src0, int64_t n, int G, int M, int B, CandBufs cb,
+                                                           int32_t* __restrict__ ids, float* __restrict__ top,
+                                                           int32_t* __restrict__ n_sel, int32_t* tomb_len) {
+  __shared__ MergeLds<Src> lds;
+  merge_exact(src0, (int)blockIdx.x, n, G, M, B, cb, ids, top, n_sel, tomb_len, lds);
+}
+
+// ---------------------------------------------------------------------------
+// Merge by rank counting (one parameter vector).  The lists hold distinct
+// composites; when every share's completeness bound is at most the B-th
+// largest listed composite tau, the top-B of the union is the exact top-B,
+// and an entry's output position is the number of larger entries.  That
+// holds when the largest bound T satisfies T <= 1 (every share listed all of
+// its elements) or at least B entries are >= T.  Workgroup w ranks the
+// kRankPer slots [w kRankPer, (w + 1) kRankPer) against all G x M slots,
+// counting with wave ballots, and writes the entries of rank < B to their
+// positions; no workgroup waits for another.  It ranks the first half of its
+// slots, then only those of the second half that lie above every slot
+// already found to rank >= B (a smaller entry ranks lower still): a list is
+// sorted, and few lists hold more than half of their entries in the top-B.
+// Otherwise (a share could be missing members of the top-B) workgroup 0 runs
+// the exact merge with its recovery and the others leave.  Every workgroup
+// reaches the same decision from the same slots and bounds.
+// ---------------------------------------------------------------------------
+constexpr int kRankPer = 16;
+constexpr int kRankHalf = kRankPer / 2;
+constexpr int kRankR = (kMergeCap + kBlock - 1) / kBlock;  // most slots per thread
+
+// NR: slots per thread, a compile-time bound >= ceil(G M / kBlock).
+template <class Src, int NR>
+__global__ __launch_bounds__(kBlock) void merge_rank(Src src, int64_t n, int G, int M, int B, CandBufs cb,
+                                                     int32_t* __restrict__ ids, float* __restrict__ top,
+                                                     int32_t* __restrict__ n_sel, int32_t* tomb_len) {
+  __shared__ MergeLds<Src> lds;
+  __shared__ uint64_t s_c[kRankPer];
+  __shared__ uint64_t s_T;
+  __shared__ int s_nz, s_ge;
+  __shared__ int s_rank[kRankPer];
+  EWSJF_STAMP(kStampMergeRank, 0);
+  const int tid = threadIdx.x, lane = tid & (kWave - 1);
+  const int GM = G * M;
+  const int p0 = (int)blockIdx.x * kRankPer;
+
+  // One round trip: the slots (slot tid + r kBlock in v[r]; past GM reads 0),
+  // the bounds and this workgroup's own slots.
+  const __amdgpu_buffer_rsrc_t lrs = __builtin_amdgcn_make_buffer_rsrc(cb.lists, (short)0, GM * 8, kBufferWord3);
+  uint64_t v[NR];
+#pragma unroll
+  for (int r = 0; r < NR; ++r) {
+    const auto w = __builtin_amdgcn_raw_buffer_load_b64(lrs, (tid + r * kBlock) * 8, 0, 0);
+    v[r] = ((uint64_t)w[1] << 32) | w[0];
+  }
+  const uint64_t bnd = tid < G ? cb.bounds[tid] : 0ull;
+  const uint64_t own = tid < kRankPer && p0 + tid < GM ? cb.lists[p0 + tid] : 0ull;
+  if (tid < kRankPer) {
+    s_c[tid] = own;
+    s_rank[tid] = 0;
+  }
+  if (tid == 0) {
+    s_T = 0ull;
+    s_nz = 0;
+    s_ge = 0;
+  }
+  __syncthreads();
+  int nz = 0;
+#pragma unroll
+  for (int r = 0; r < NR; ++r) nz += __popcll(__ballot(v[r] != 0ull));
+  const uint64_t wmax = wave_max_u64(bnd);
+  if (lane == 0) {
+    atomicMax(reinterpret_cast<unsigned long long*>(&s_T), (unsigned long long)wmax);
+    atomicAdd(&s_nz, nz);
+  }
+  __syncthreads();
+  EWSJF_STAMP(kStampMergeRank, 1);
+  const uint64_t T = s_T;
+  int ge = 0;
+#pragma unroll
+  for (int r = 0; r < NR; ++r) ge += __popcll(__ballot(v[r] >= T));
+  if (lane == 0) atomicAdd(&s_ge, ge);
+  // This wave's count of slots larger than own slot p (wave-uniform: ballots
+  // counted on the scalar unit, beside the compares on the vector unit),
+  // summed over the waves in LDS.
+  // The counts of one half of the own slots go to LDS in one add per wave
+  // (lane p adds the count of slot h + p).
+  uint64_t c[kRankPer];
+#pragma unroll
+  for (int p = 0; p < kRankPer; ++p) c[p] = s_c[p];
+  auto count_half = [&](int h, uint64_t above) {
+    int mine = 0;
+#pragma unroll
+    for (int p = 0; p < kRankHalf; ++p) {
+      if (c[h + p] > above) {  // uniform
+        int cnt = 0;
+#pragma unroll
+        for (int r = 0; r < NR; ++r) cnt += __popcll(__ballot(v[r] > c[h + p]));
+        mine = lane == p ? cnt : mine;
+      }
+    }
+    if (lane < kRankHalf && mine != 0) atomicAdd(&s_rank[h + lane], mine);
+  };
+  count_half(0, 0ull);
+  __syncthreads();
+  EWSJF_STAMP(kStampMergeRank, 2);
+  const bool safe = T <= 1ull || s_ge >= B;
+  if (!safe) {
+    EWSJF_STAMP(kStampMergeRank, 7);
+    if (blockIdx.x == 0) merge_exact(src, 0, n, G, M, B, cb, ids, top, n_sel, tomb_len, lds);
+    return;
+  }
+  // The largest own slot of the first half known to rank >= B: slots at or
+  // below it rank >= B too.
+  uint64_t out_bar = 0;
+#pragma unroll
+  for (int p = 0; p < kRankHalf; ++p)
+    if (c[p] != 0ull && s_rank[p] >= B && c[p] > out_bar) out_bar = c[p];
+  bool second = false;
+#pragma unroll
+  for (int p = kRankHalf; p < kRankPer; ++p) second = second || c[p] > out_bar;
+  if (second) {  // uniform
+    count_half(kRankHalf, out_bar);
+    __syncthreads();
+  }
+  EWSJF_STAMP(kStampMergeRank, 3);
+  const int nnz = s_nz;
+  const int sel = nnz < B ? nnz : B;
+  if (tid < kRankPer) {
+    const uint64_t x = s_c[tid];
+    const int rank = s_rank[tid];
+    if (x > out_bar && rank < B) {
+      const uint32_t id = comp_id(x);
+      ids[rank] = (int32_t)id;
+      top[rank] = float_of_ukey((uint32_t)(x >> 32));
+      if (tomb_len != nullptr) tomb_len[id] = 0;
+    }
+  }
+  // Positions past the selection: every workgroup takes every gridDim-th.
+  for (int r = (int)blockIdx.x + (int)gridDim.x * tid; r < B; r += (int)gridDim.x * kBlock) {
+    if (r >= sel) {
+      ids[r] = -1;
+      top[r] = __builtin_nanf("");
+    }
+  }
+  if (blockIdx.x == 0 && tid == 0) n_sel[0] = sel;
+  EWSJF_STAMP(kStampMergeRank, 4);
+}
+
+// Launches merge_rank with the smallest compiled slots-per-thread bound.
+template <class Src>
+static void launch_merge_rank(const SelectPlan& p, hipStream_t stream, hipEvent_t e0, hipEvent_t e1, const Src& src,
+                              int64_t n, int B, const CandBufs& cb, int32_t* ids, float* top, int32_t* n_sel,
+                              int32_t* tomb_len) {
+  const int nr = (p.G * p.M + kBlock - 1) / kBlock;
+  const dim3 grid((p.G * p.M + kRankPer - 1) / kRankPer), block(kBlock);
+  auto go = [&](auto kern) {
+    if (e0 != nullptr)
+      hipExtLaunchKernelGGL(kern, grid, block, 0, stream, e0, e1, 0, src, n, p.G, p.M, B, cb, ids, top, n_sel,
+                            tomb_len);
+    else
+      hipLaunchKernelGGL(kern, grid, block, 0, stream, src, n, p.G, p.M, B, cb, ids, top, n_sel, tomb_len);
+  };
+  if (nr <= 1) go(merge_rank<Src, 1>);
+  else if (nr <= 2) go(merge_rank<Src, 2>);
+  else if (nr <= 4) go(merge_rank<Src, 4>);
+  else go(merge_rank<Src, kRankR>);
 }
 
 // ---------------------------------------------------------------------------
@@ -1388,8 +1657,11 @@ hipError_t launch_step(const int32_t* len, const float* arrival, int64_t n, floa
                          p.lg, p.M, cb);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(merge_candidates<PoolSource>, dim3(n_theta), dim3(kBlock), 0, stream, src, n, p.G, p.M,
-                       B, cb, ids, top, n_sel, tomb_len);
+    if (n_theta == 1)
+      launch_merge_rank(p, stream, nullptr, nullptr, src, n, B, cb, ids, top, n_sel, tomb_len);
+    else
+      hipLaunchKernelGGL(merge_candidates<PoolSource>, dim3(n_theta), dim3(kBlock), 0, stream, src, n, p.G, p.M,
+                         B, cb, ids, top, n_sel, tomb_len);
     return hipGetLastError();
   }
   // The events take the start and end timestamps of each kernel's own
@@ -1402,8 +1674,11 @@ hipError_t launch_step(const int32_t* len, const float* arrival, int64_t n, floa
                           marks[1], 0, src, n, p.G, p.lg, p.M, cb);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipExtLaunchKernelGGL(merge_candidates<PoolSource>, dim3(n_theta), dim3(kBlock), 0, stream, marks[2], marks[3],
-                        0, src, n, p.G, p.M, B, cb, ids, top, n_sel, tomb_len);
+  if (n_theta == 1)
+    launch_merge_rank(p, stream, marks[2], marks[3], src, n, B, cb, ids, top, n_sel, tomb_len);
+  else
+    hipExtLaunchKernelGGL(merge_candidates<PoolSource>, dim3(n_theta), dim3(kBlock), 0, stream, marks[2], marks[3],
+                          0, src, n, p.G, p.M, B, cb, ids, top, n_sel, tomb_len);
   return hipGetLastError();
 }
 
@@ -1435,8 +1710,7 @@ hipError_t launch_ring_step(int32_t* ring_len, float* ring_arrival, int64_t capa
                      p.M, cb);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(merge_candidates<RingSource>, dim3(1), dim3(kBlock), 0, stream, src, capacity, p.G, p.M, B, cb,
-                     ids, top, n_sel, tomb_len);
+  launch_merge_rank(p, stream, nullptr, nullptr, src, capacity, B, cb, ids, top, n_sel, tomb_len);
   return hipGetLastError();
 }
 
@@ -1503,9 +1777,26 @@ hipError_t launch_select(const float* score, int64_t n, int32_t n_theta, int32_t
                      p.lg, p.M, cb);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(merge_candidates<ScoreSource>, dim3(n_theta), dim3(kBlock), 0, stream, src, n, p.G, p.M,
-                     B, cb, ids, top, n_sel, nullptr);
+  if (n_theta == 1)
+    launch_merge_rank(p, stream, nullptr, nullptr, src, n, B, cb, ids, top, n_sel, nullptr);
+  else
+    hipLaunchKernelGGL(merge_candidates<ScoreSource>, dim3(n_theta), dim3(kBlock), 0, stream, src, n, p.G, p.M,
+                       B, cb, ids, top, n_sel, nullptr);
   return hipGetLastError();
 }
 
 }  // namespace ewsjf
+
+#ifdef EWSJF_STAMPS
+// Instrumented build only: copy the phase stamps to the host (count <=
+// kStampSlots words) or clear them.
+extern "C" int ewsjf_debug_stamps(uint64_t* host, size_t count) {
+  if (count > (size_t)ewsjf::kStampSlots) count = ewsjf::kStampSlots;
+  return (int)hipMemcpyFromSymbol(host, HIP_SYMBOL(ewsjf::g_stamps), count * sizeof(uint64_t), 0,
+                                  hipMemcpyDeviceToHost);
+}
+extern "C" int ewsjf_debug_stamps_clear(void) {
+  static uint64_t zeros[ewsjf::kStampSlots];
+  return (int)hipMemcpyToSymbol(HIP_SYMBOL(ewsjf::g_stamps), zeros, sizeof(zeros), 0, hipMemcpyHostToDevice);
+}
+#endif

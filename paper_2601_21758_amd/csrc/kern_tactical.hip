@@ -381,6 +381,7 @@ __global__ __launch_bounds__(kBlock) void tac_finish(const TacticalPlan* __restr
   const int L = tab->max_len;
   const bool gapped = tab->gapped != 0;
   lut_fill(tab->lut, tid, kBlock, L, gapped, qb, qlo, qhi, k2);
+  route_fill(tab->route, tid, kBlock, L, gapped, qb, qlo, qhi, k2);
 }
 
 }  // namespace

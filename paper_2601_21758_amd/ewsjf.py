@@ -224,7 +224,20 @@ def read_table(table: torch.Tensor) -> dict:
         "count": np.array(h.count[:k], np.int64), "sum": np.array(h.sum[:k], np.int64),
         "mean": np.array(h.mean[:k], np.float64),
         "lut": np.frombuffer(bytes(h.lut), np.uint8)[:h.max_len + 1].copy(),
+        "route": np.frombuffer(bytes(h.route), np.uint64).copy(),
     }
+
+
+def route_map_queues(route: np.ndarray, max_len: int) -> np.ndarray:
+    """Decode a table's compact routing map: the queue of every length
+    0..max_len (length 0 decodes to 0), as the per-step kernels read it."""
+    b = np.arange(max_len + 1, dtype=np.int64)
+    w = route[b >> 5]
+    base = (w >> np.uint64(32)).astype(np.int64)
+    mask = (w & np.uint64(0xFFFFFFFF)).astype(np.uint64)
+    keep = (mask << (np.uint64(31) - (b & 31).astype(np.uint64))) & np.uint64(0xFFFFFFFF)
+    bits = np.unpackbits(keep.astype(">u4").view(np.uint8).reshape(-1, 4), axis=1).sum(axis=1)
+    return (base + bits).astype(np.int64)
 
 
 def route(length: torch.Tensor, table: torch.Tensor, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:

@@ -57,6 +57,7 @@ def check_table(E, tab, ref: oracle.Table, max_len=32768):
     assert np.array_equal(g["count"], ref.count) and np.array_equal(g["sum"], ref.sum), "counts"
     assert np.array_equal(g["mean"].view(np.uint64), ref.mean.view(np.uint64)), "means"
     assert np.array_equal(g["lut"][1:], oracle.route(np.arange(1, max_len + 1, dtype=np.int32), ref)), "lut"
+    assert np.array_equal(E.route_map_queues(g["route"], max_len)[1:], g["lut"][1:]), "compact routing map"
 
 
 def table_of(d):

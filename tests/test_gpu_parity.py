@@ -364,6 +364,8 @@ def test_partition_bit_exact(E, name):
     # the routing lut routes every length like the oracle
     lens = np.arange(1, g["max_len"] + 1, dtype=np.int32)
     assert np.array_equal(g["lut"][1:], oracle.route(lens, r))
+    # the compact map the per-step kernels read gives the same queues
+    assert np.array_equal(E.route_map_queues(g["route"], g["max_len"])[1:], g["lut"][1:])
 
 
 @pytest.mark.parametrize("seed", range(4))

@@ -75,6 +75,7 @@ def compare_step(E, tab, ec_dev, out, ref: oracle.TacticalResult, k0):
     assert np.array_equal(gt["lo"], rt.lo) and np.array_equal(gt["hi"], rt.hi)
     assert np.array_equal(gt["mean"].view(np.uint64), rt.mean.view(np.uint64))
     assert np.array_equal(gt["lut"][1:], oracle.route(np.arange(1, gt["max_len"] + 1), ref.table)), "lut"
+    assert np.array_equal(E.route_map_queues(gt["route"], gt["max_len"])[1:], gt["lut"][1:]), "compact routing map"
     assert np.array_equal(host(ec_dev)[:ref.table.k], ref.empty_cnt)
     return True
 
