@@ -134,7 +134,10 @@ typedef struct {
 } ewsjf_theta;
 
 /* Estimated prefill cost C_prefill(b) = c0 + c1*b + c2*b^2 seconds (host struct).
- * Requires c0 > 0, c1 >= 0, c2 >= 0, all finite. */
+ * The kernels evaluate it in binary32: c0 must lie in [FLT_MIN, FLT_MAX], c1
+ * and c2 must each be 0 or lie in that range, and (b + 1) C_prefill(b) must
+ * not exceed FLT_MAX / 2 for b = 2^31 - 1 (the longest length); otherwise
+ * EWSJF_ERR_ARG. */
 typedef struct {
   double c0, c1, c2;
 } ewsjf_cost;
@@ -192,9 +195,11 @@ size_t ewsjf_workspace_bytes(int op, int64_t n, int32_t n_theta, int32_t B, cons
  * from storage).  host_table: host struct with k, max_len, gapped, bounds, lo,
  * hi, count, sum, mean filled in (lut and diagnostics are ignored).  Requires
  * 1 <= k <= EWSJF_MAX_QUEUES, 1 <= max_len <= EWSJF_MAX_LEN and bounds strictly
- * increasing within [1, max_len], finite means; gapped is 0 or 1, and with 1
- * the intervals [lo_i, hi_i] lie in [1, max_len] in increasing order without
- * overlap.  The device copy and its
+ * increasing within [1, max_len], finite means; gapped is 0 or 1.  With
+ * gapped = 1 the intervals [lo_i, hi_i] lie in [1, max_len] in increasing
+ * order without overlap; with gapped = 0, lo_i = bounds[i-1] for i >= 1
+ * (queue i starts at its bound, as in the tables ewsjf_partition writes).
+ * Otherwise EWSJF_ERR_ARG.  The device copy and its
  * routing lut are written on `stream`; this set-up call then synchronizes
  * `stream` so the host struct may be released on return. */
 ewsjf_status ewsjf_table_upload(const ewsjf_queue_table* host_table, void* table, hipStream_t stream);

@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <atomic>
+#include <cfloat>
 #include <cmath>
 #include <cstddef>
 #include <cstring>
@@ -38,9 +39,16 @@ ewsjf_status check_device() {
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 
+// The kernels evaluate C_prefill and (b + 1) C_prefill(b) in binary32: c0
+// must be a normal binary32 value and c1, c2 zero or normal, and (b + 1) C(b)
+// must stay within half of FLT_MAX up to the longest int32 length (it grows
+// with b), so that C is finite and nonzero there for every request.
+bool f32_normal(double x) { return x >= (double)FLT_MIN && x <= (double)FLT_MAX; }
 bool cost_ok(const ewsjf_cost* c) {
-  return std::isfinite(c->c0) && std::isfinite(c->c1) && std::isfinite(c->c2) && c->c0 > 0.0 && c->c1 >= 0.0 &&
-         c->c2 >= 0.0;
+  if (!(f32_normal(c->c0) && (c->c1 == 0.0 || f32_normal(c->c1)) && (c->c2 == 0.0 || f32_normal(c->c2))))
+    return false;
+  const double b = 2147483647.0;
+  return (b + 1.0) * (c->c0 + c->c1 * b + c->c2 * b * b) <= 0.5 * (double)FLT_MAX;
 }
 
 bool params_ok(const ewsjf_partition_params* p) {
@@ -116,6 +124,12 @@ ewsjf_status ewsjf_table_upload(const ewsjf_queue_table* host_table, void* table
     for (int i = 0; i < h.k; ++i)
       if (h.lo[i] < 1 || h.hi[i] < h.lo[i] || h.hi[i] > h.max_len || (i > 0 && h.lo[i] <= h.hi[i - 1]))
         return EWSJF_ERR_ARG;
+  // Contiguous: queue i > 0 starts at its bound, the table Refine-and-Prune
+  // writes, so a later removal of a queue (ewsjf_tactical_step) that deletes
+  // the boundary it shares with its absorber leaves lo consistent.
+  if (!h.gapped)
+    for (int i = 1; i < h.k; ++i)
+      if (h.lo[i] != h.bounds[i - 1]) return EWSJF_ERR_ARG;
   const ewsjf_status ds = check_device();
   if (ds != EWSJF_OK) return ds;
   std::unique_ptr<ewsjf_queue_table> copy(new ewsjf_queue_table(h));

@@ -190,12 +190,18 @@ def dispatch(length: torch.Tensor, arrival: torch.Tensor, table: torch.Tensor, b
 def upload_table(bounds, mean, max_len: int = L.MAX_LEN, lo=None, hi=None, count=None, sum=None,
                  device=None, stream=None, gapped: bool = False) -> torch.Tensor:
     """Install a queue structure given on the host (bounds: k-1 ints, mean: k
-    floats; gapped: route by the lo/hi intervals)."""
+    floats; gapped: route by the lo/hi intervals).  Without lo/hi, each
+    queue's lo/hi are its routing interval (queue 0 from length 1, the last
+    queue up to max_len)."""
     bounds = np.asarray(bounds, np.int64).reshape(-1)
     mean = np.asarray(mean, np.float64).reshape(-1)
     k = mean.size
     if bounds.size != k - 1:
         raise ValueError("need k-1 bounds for k means")
+    if lo is None:
+        lo = np.concatenate([[1], bounds])
+    if hi is None:
+        hi = np.concatenate([bounds - 1, [max_len]])
     h = L.QueueTable()
     h.k, h.max_len, h.gapped = k, int(max_len), int(bool(gapped))
     for i, b in enumerate(bounds):

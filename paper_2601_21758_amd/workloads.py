@@ -155,11 +155,17 @@ class Streaming:
     `p_start` at step 0 to `p_end` at the last step.  Arrivals continue one
     Poisson process at `rate` per second (gaps summed in fp64, stored fp32).
     The partitioner window is the last `window` arrivals.
+
+    `start_step` > 0 starts a run part-way through the drift: the fill is
+    then the last `capacity` arrivals the run drew before that step (the
+    step-0 fill and every earlier step's arrivals, drawn in the same order),
+    oldest in slot 0, and steps start_step, start_step + 1, ... follow.
     """
 
     def __init__(self, seed: int = 4, capacity: int = 1 << 20, per_step: int = 4096,
                  steps: int = 10000, window: int = 65536, rp_every: int = 100, B: int = 512,
-                 K: int = 64, p_start: float = 0.9, p_end: float = 0.3, rate: float = 1e4):
+                 K: int = 64, p_start: float = 0.9, p_end: float = 0.3, rate: float = 1e4,
+                 start_step: int = 0):
         self.rng = np.random.Generator(np.random.PCG64(seed))
         self.capacity, self.per_step, self.steps = capacity, per_step, steps
         self.window_size, self.rp_every, self.B, self.K = window, rp_every, B, K
@@ -167,7 +173,8 @@ class Streaming:
         self.clock = 0.0
         self.theta = THETA_MID.reshape(1, 6).copy()
         self.cost = DEFAULT_COST
-        self.next_step = 0
+        self.start_step = start_step
+        self.next_step = start_step
 
     def p_short(self, s: int) -> float:
         if self.steps <= 1:
@@ -182,18 +189,29 @@ class Streaming:
         return length, t.astype(np.float32)
 
     def initial_fill(self):
-        """(length, arrival) for all `capacity` slots, at the step-0 weight."""
-        return self._chunk(self.capacity, self.p_start)
+        """(length, arrival) for all `capacity` slots: at the step-0 weight,
+        or from a later start step the last `capacity` arrivals before it."""
+        length, arrival = self._chunk(self.capacity, self.p_start)
+        if self.start_step == 0:
+            return length, arrival
+        pos = 0  # the ring slot the next arrival overwrites (the oldest)
+        for s in range(self.start_step):
+            ln, ar = self._chunk(self.per_step, self.p_short(s))
+            idx = (pos + np.arange(self.per_step)) % self.capacity
+            length[idx] = ln
+            arrival[idx] = ar
+            pos = (pos + self.per_step) % self.capacity
+        return np.roll(length, -pos), np.roll(arrival, -pos)
 
     def arrivals(self, s: int):
-        """Step s's arrivals; steps must be drawn in order 0, 1, 2, ..."""
+        """Step s's arrivals; steps must be drawn in order start_step, start_step + 1, ..."""
         if s != self.next_step:
             raise ValueError("streaming arrivals must be drawn in step order")
         self.next_step += 1
         return self._chunk(self.per_step, self.p_short(s))
 
     def slots(self, s: int) -> np.ndarray:
-        start = (s * self.per_step) % self.capacity
+        start = ((s - self.start_step) * self.per_step) % self.capacity
         return (start + np.arange(self.per_step)) % self.capacity
 
 

@@ -89,6 +89,14 @@ def test_step_argument_errors():
     assert step(cost=L.Cost(0.0, 1e-4, 0.0)) == L.ERR_ARG
     assert step(cost=L.Cost(0.01, -1e-4, 0.0)) == L.ERR_ARG
     assert step(cost=L.Cost(0.01, 1e-4, float("inf"))) == L.ERR_ARG
+    # costs the binary32 evaluation cannot hold: c0 rounding to 0 or a
+    # subnormal, c0/c1/c2 above FLT_MAX, a subnormal c1 or c2
+    for bad in [(1e-50, 0.0, 0.0), (1e-39, 0.0, 0.0), (1e39, 0.0, 0.0), (0.01, 1e39, 0.0), (0.01, 0.0, 1e39),
+                (0.01, 1e-40, 0.0), (0.01, 0.0, 1e-45), (float("nan"), 0.0, 0.0), (0.01, 0.0, 1e11),
+                (0.01, 1e20, 0.0), (1e29, 0.0, 0.0)]:
+        assert step(cost=L.Cost(*bad)) == L.ERR_ARG, bad
+    for good in [(1.2e-38, 0.0, 0.0), (1e28, 0.0, 0.0), (0.01, 1.2e-38, 2e-9), (0.01, 1e-4, 1e9)]:
+        assert step(cost=L.Cost(*good)) != L.ERR_ARG, good
     assert step(flags=2) == L.ERR_ARG
     assert step(flags=L.STEP_TOMBSTONE, nt=2) == L.ERR_ARG
     assert step(wsb=ws_need - 1) == L.ERR_WORKSPACE
@@ -281,6 +289,14 @@ def test_table_upload_argument_errors():
     assert lib.ewsjf_table_upload(C.byref(h), FAKE, None) == L.ERR_ARG
     h.lo[0], h.hi[0] = 60, 50            # empty interval
     assert lib.ewsjf_table_upload(C.byref(h), FAKE, None) == L.ERR_ARG
+    # the contiguous reading: queue i > 0 starts at its bound
+    h.gapped, h.lo[0], h.hi[0] = 0, 10, 50
+    h.lo[1], h.lo[2] = 100, 499          # lo[2] != bounds[1]
+    assert lib.ewsjf_table_upload(C.byref(h), FAKE, None) == L.ERR_ARG
+    h.lo[1], h.lo[2] = 0, 500            # lo[1] left at 0
+    assert lib.ewsjf_table_upload(C.byref(h), FAKE, None) == L.ERR_ARG
+    h.lo[1] = 100                        # consistent: passes validation, then needs a device
+    assert lib.ewsjf_table_upload(C.byref(h), FAKE, None) == L.ERR_DEVICE
 
 
 def test_trial_argument_errors():

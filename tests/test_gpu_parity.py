@@ -203,13 +203,21 @@ def test_step_full_4m_pool(E):
 
 
 def test_step_batched_theta(E):
+    # the batched-parameter workload at full shape: every one of the 256
+    # admission sets against the oracle (32 vectors per oracle call)
     p = W.config(3)
-    say(f"step cfg3 n={p.n} n_theta={p.theta.shape[0]}")
+    nt = p.theta.shape[0]
+    say(f"step cfg3 n={p.n} n_theta={nt}")
     t = oracle_table(p)
     ids, top, nsel, _ = run_step(E, p, t)
-    for ti in range(0, p.theta.shape[0], 37):
-        rids, rtop, rnsel, rs = oracle.step(p.length, p.arrival, p.now, t, p.theta[ti:ti + 1], p.B, p.cost)
-        check_admission(ids[ti], top[ti], nsel[ti], rids[0], rtop[0], rnsel[0], rs[0])
+    near = 0
+    for t0 in range(0, nt, 32):
+        rids, rtop, rnsel, rs = oracle.step(p.length, p.arrival, p.now, t, p.theta[t0:t0 + 32], p.B, p.cost)
+        for j in range(rids.shape[0]):
+            ti = t0 + j
+            near += check_admission(ids[ti], top[ti], nsel[ti], rids[j], rtop[j], rnsel[j], rs[j])
+        say(f"  vectors {t0}..{t0 + rids.shape[0] - 1} ok")
+    say(f"cfg3: {nt} admission sets checked, near-tie differences {near}")
 
 
 @pytest.mark.parametrize("n,nt,B", [(20011, 37, 64), (300001, 17, 4096), (4095, 2, 100), (1 << 20, 33, 256),
@@ -378,6 +386,31 @@ def test_partition_kmeans3_bit_exact(E, seed):
     kw = dict(init_mode=oracle.KMEANS3, max_queues=32)
     g, _ = gpu_partition(E, win, **kw)
     check_table(g, ora_partition(win, **kw))
+
+
+KMEANS_WINDOWS = {
+    "cfg0": lambda: W.config(0).window,
+    "cfg1": lambda: W.config(1).window,
+    "cfg2": lambda: W.config(2).window,
+    "cfg3": lambda: W.config(3).window,
+    "all_values_32768": lambda: np.arange(1, 32769, dtype=np.int32),
+}
+
+
+@pytest.mark.parametrize("name", list(KMEANS_WINDOWS))
+def test_partition_kmeans3_config_windows(E, name):
+    # Stage 1 as the paper states it (exact 3-means over the window's distinct
+    # values) on the workload windows: thousands of distinct values, so the
+    # grid-wide binary64 search meets near-ties in its objective and the
+    # lowest-split tie rule; the queue budget of each workload
+    win = KMEANS_WINDOWS[name]()
+    mq = {"cfg0": 16, "cfg2": 256}.get(name, 64)
+    kw = dict(init_mode=oracle.KMEANS3, max_queues=mq)
+    say(f"partition kmeans3 {name} W={len(win)} max_queues={mq}")
+    g, _ = gpu_partition(E, win, **kw)
+    r = ora_partition(win, **kw)
+    check_table(g, r)
+    say(f"  distinct={r.n_distinct} leaves={r.n_leaves} k={r.k}")
 
 
 def test_partition_then_step_end_to_end(E):

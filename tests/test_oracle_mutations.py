@@ -52,6 +52,10 @@ MUTANTS = [
     ("absorber_highest_utility", "utility(qs[r - 1], qs[r], eps) <= utility(qs[r], qs[r + 1], eps)",
      "utility(qs[r - 1], qs[r], eps) > utility(qs[r], qs[r + 1], eps)"),
     ("absorber_drops_counts", "A = {A.n + qs[r].n, A.S + qs[r].S,", "A = {A.n, A.S + qs[r].S,"),
+    ("removal_rebuilds_bounds_from_lo", "if (q > 0) bounds[q - 1] = bnd[q - 1];",
+     "if (q > 0) bounds[q - 1] = qs[q].lo;"),
+    ("removal_deletes_the_far_boundary", "bnd.erase(bnd.begin() + std::min(r, a));",
+     "bnd.erase(bnd.begin() + (a < r ? r : r + 1 < (int32_t)bnd.size() ? r + 1 : r - 1));"),
     # Algorithm 2 (bubble queues)
     ("bubble_lower_tolerance_strict", "if (10 * b <= 11 * max_len_i) return i;", "if (10 * b < 11 * max_len_i) return i;"),
     ("bubble_upper_tolerance_factor", "if (10 * b >= 9 * min_len_next) return i + 1;",

@@ -224,6 +224,30 @@ def test_removed_queue_goes_to_lower_utility_neighbour(seed):
     assert n2.mean.tolist() == (n2.sum / n2.count).tolist()
 
 
+@pytest.mark.parametrize("s3,to_lower", [(3200, True), (3900, False)])
+def test_removal_deletes_the_shared_boundary(s3, to_lower):
+    # Reading T6: the removed queue's boundary with its absorber goes; the
+    # other bounds stay where they were.  The window extremes lo/hi sit
+    # inside the routing intervals here (lo != the bounds), so a rule that
+    # rebuilt the bounds from lo would give other bounds.
+    t = table_of({"k": 4, "bounds": [100, 200, 300], "count": [10, 10, 10, 10], "sum": [500, 1500, 2600, s3],
+                  "lo": [1, 120, 230, 310], "hi": [90, 180, 290, 400]})
+    Q = [(t.count[j], t.sum[j], t.lo[j], t.hi[j]) for j in range(4)]
+    assert (utility_exact(Q[1], Q[2]) <= utility_exact(Q[2], Q[3])) == to_lower
+    # one request in queues 0, 1 and 3 (routed by the bounds); queue 2 is empty
+    L = np.array([50, 150, 350], np.int32)
+    r = oracle.tactical_step(L, np.zeros(3, np.float32), 60.0, t, np.zeros(4, np.int32), MID, 3, 0, COST)
+    assert r.removed.tolist() == [False, False, True, False]
+    n2 = r.table
+    assert n2.bounds.tolist() == ([100, 300] if to_lower else [100, 200])
+    j = 1 if to_lower else 2  # the merged queue
+    a = 1 if to_lower else 3
+    assert n2.count[j] == 20 and n2.sum[j] == t.sum[a] + t.sum[2]
+    assert n2.lo[j] == min(t.lo[a], t.lo[2]) and n2.hi[j] == max(t.hi[a], t.hi[2])
+    # routing of the merged set by the remaining bounds: 250 joins the absorber
+    assert oracle.route(np.array([250], np.int32), n2)[0] == j
+
+
 def test_batch_invariant_under_pool_permutation():
     p = W.config(0)
     t = oracle.partition(p.window, init_queues=p.init_queues, max_queues=p.max_queues)

@@ -63,6 +63,31 @@ def test_reference_ring_and_window_follow_the_generator():
         assert np.array_equal(np.sort(ref.win), np.sort(last))
 
 
+def test_late_start_fill_is_the_runs_last_arrivals():
+    # a run started at step 7 begins from the ring the run from step 0 would
+    # hold before step 7 (no admissions), oldest first, and draws the same
+    # step-7 arrivals into the same relative slots
+    cap, per = 1000, 300
+    full = W.Streaming(seed=4, capacity=cap, per_step=per, steps=20, window=256)
+    L0, A0 = full.initial_fill()
+    hist_l, hist_a = [L0], [A0]
+    for s in range(7):
+        l, a = full.arrivals(s)
+        hist_l.append(l)
+        hist_a.append(a)
+    late = W.Streaming(seed=4, capacity=cap, per_step=per, steps=20, window=256, start_step=7)
+    Lf, Af = late.initial_fill()
+    assert np.array_equal(Lf, np.concatenate(hist_l)[-cap:])
+    assert np.array_equal(Af, np.concatenate(hist_a)[-cap:])
+    l7, a7 = full.arrivals(7)
+    m7, b7 = late.arrivals(7)
+    assert np.array_equal(l7, m7) and np.array_equal(a7, b7)
+    assert late.p_short(7) == full.p_short(7)
+    assert np.array_equal(late.slots(7), np.arange(per))
+    with pytest.raises(ValueError):
+        late.arrivals(9)
+
+
 def test_constructor_rejects_window_larger_than_ring():
     from paper_2601_21758_amd import ewsjf
     with pytest.raises(ValueError):
@@ -71,10 +96,12 @@ def test_constructor_rejects_window_larger_than_ring():
 
 # ---- lockstep parity on the GPU ---------------------------------------------------
 def _lockstep(capacity, per_step, steps, window, rp_every, B, K, label, tombstone_check_every=0, fused=False,
-              incremental=True, bubbles=None, novel=0.0):
+              incremental=True, bubbles=None, novel=0.0, start=0, total=None, report_every=50):
+    """`steps` steps from step `start` of a drift schedule of `total` steps
+    (default: `steps`)."""
     from paper_2601_21758_amd import ewsjf
-    s = W.Streaming(seed=4, capacity=capacity, per_step=per_step, steps=steps, window=window, rp_every=rp_every,
-                    B=B, K=K)
+    s = W.Streaming(seed=4, capacity=capacity, per_step=per_step, steps=total or steps, window=window,
+                    rp_every=rp_every, B=B, K=K, start_step=start)
     prm = ewsjf.params(init_queues=K, max_queues=K)
     gpu = StreamingScheduler(capacity, window, B, prm, s.theta[0], s.cost, incremental=incremental, bubbles=bubbles)
     ref = OracleStream(capacity, window, B, K, K, s.theta, s.cost, bubbles=bubbles)
@@ -85,7 +112,7 @@ def _lockstep(capacity, per_step, steps, window, rp_every, B, K, label, tombston
     near = 0
     grown = 0
     novel_rng = np.random.default_rng(99)
-    for step in range(steps):
+    for step in range(start, start + steps):
         L, A = s.arrivals(step)
         if novel:  # a fraction of the arrivals are of lengths the window has not seen
             pick = novel_rng.random(L.size) < novel
@@ -123,9 +150,10 @@ def _lockstep(capacity, per_step, steps, window, rp_every, B, K, label, tombston
                 gpu.len[torch.from_numpy(extra.astype(np.int64)).cuda()] = torch.from_numpy(ref.len[extra]).cuda()
         gpu.apply_tombstones(rids[:rnsel])
         ref.tombstone(rids[:rnsel])
-        if step % 50 == 0 or step == steps - 1:
+        if step % report_every == 0 or step == start + steps - 1:
             assert np.array_equal(gpu.len.cpu().numpy(), ref.len), f"{label}: ring lengths diverged at step {step}"
-            print(f"{label}: step {step} ok (near-tie differences so far {near})", flush=True)
+            print(f"{label}: step {step} ok (short weight {s.p_short(step):.3f}, near-tie differences so far "
+                  f"{near})", flush=True)
     assert np.array_equal(gpu.arr.cpu().numpy(), ref.arr)
     assert np.array_equal(np.sort(gpu.window_lengths().cpu().numpy()), np.sort(ref.win)), f"{label}: window differs"
     if bubbles is not None:
@@ -230,3 +258,23 @@ def test_streaming_lockstep_full_size_prefix():
     # 101 steps, so two hand-overs (steps 0 and 100) are covered
     _lockstep(capacity=1 << 20, per_step=4096, steps=101, window=65536, rp_every=100, B=512, K=64, label="full",
               tombstone_check_every=25, fused=True)
+
+
+@pytest.mark.gpu
+def test_streaming_lockstep_full_size_late_drift():
+    # the streaming workload at full size late in its drift: the ring holds
+    # the last 1,048,576 arrivals drawn before step 9,799 of the 10,000-step
+    # schedule (short weight ~0.31), then steps 9,799..9,901 run in lockstep,
+    # so the partitions of steps 9,800 and 9,900 both take effect
+    _lockstep(capacity=1 << 20, per_step=4096, steps=103, window=65536, rp_every=100, B=512, K=64,
+              label="full-late", tombstone_check_every=25, fused=True, start=9799, total=10000, report_every=20)
+
+
+@pytest.mark.gpu
+def test_streaming_lockstep_whole_drift_reduced():
+    # the whole 10,000-step drift (short weight 0.9 -> 0.3) at reduced size:
+    # a 65,536-slot ring, 256 arrivals and B=32 admissions per step, a
+    # 4,096-length window partitioned every 100 steps into up to 64 queues;
+    # every step's admissions and every partition are compared
+    _lockstep(capacity=1 << 16, per_step=256, steps=10000, window=4096, rp_every=100, B=32, K=64,
+              label="drift", tombstone_check_every=97, fused=True, report_every=500)
