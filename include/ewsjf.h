@@ -86,7 +86,8 @@ enum {
   EWSJF_MAX_THETA = 1024,    /* parameter vectors per call */
   EWSJF_MAX_DISPATCH = 4096, /* requests per ewsjf_dispatch call */
   EWSJF_TRIAL_STATS = 8,     /* statistics per trial proposal (ewsjf_trial_step) */
-  EWSJF_ROUTE_WORDS = EWSJF_MAX_LEN / 32 + 2 /* 64-bit words of the compact routing map */
+  EWSJF_ROUTE_WORDS = EWSJF_MAX_LEN / 32 + 2, /* 64-bit words of the compact routing map */
+  EWSJF_STATIC_SCRATCH_BYTES = 4 << 20        /* scratch of ewsjf_step_static, per device */
 };
 
 /* Stage-1 initializers (Section 4.2, Stage 1). */
@@ -319,6 +320,26 @@ ewsjf_status ewsjf_step_timed(int32_t* len, const float* arrival, int64_t n, flo
                               const ewsjf_theta* theta, int32_t n_theta, const ewsjf_cost* cost, int32_t B,
                               int32_t flags, int32_t* ids, float* top, int32_t* n_sel, void* ws, size_t ws_bytes,
                               hipStream_t stream, hipEvent_t* marks);
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, serving loops and harnesses that may not call hipMalloc):
+ * ewsjf_step with its workspace in a fixed array of
+ * EWSJF_STATIC_SCRATCH_BYTES bytes that the library keeps on each device
+ * until the process ends, so the call allocates nothing.  Arguments, outputs
+ * and rules as for ewsjf_step, without ws/ws_bytes.  A size whose workspace,
+ * ewsjf_workspace_bytes(EWSJF_OP_STEP, n, n_theta, B, NULL), exceeds
+ * EWSJF_STATIC_SCRATCH_BYTES returns EWSJF_ERR_WORKSPACE before anything is
+ * enqueued (one vector: any pool up to 2^31 - 1 requests and any B; several
+ * vectors: up to 13 over 4,194,304 requests with B = 1,024, up to 55 over
+ * 1,048,576 requests with B = 256).  Every call on a device
+ * uses that device's one array: calls that can run at the same time on one
+ * device (other streams, other host threads) race and must be serialized by
+ * the caller.  No clearing is needed between calls (each call writes every
+ * scratch entry it reads).  The first call on a device looks the array up
+ * (hipGetSymbolAddress); EWSJF_ERR_LAUNCH if that fails. */
+ewsjf_status ewsjf_step_static(int32_t* len, const float* arrival, int64_t n, float now, const void* table,
+                               const ewsjf_theta* theta, int32_t n_theta, const ewsjf_cost* cost, int32_t B,
+                               int32_t flags, int32_t* ids, float* top, int32_t* n_sel, hipStream_t stream);
 
 /* Streaming pool update: the tactical loop admits from a pool that new
  * requests keep joining (Section 3.2), and the strategic loop partitions a

@@ -24,7 +24,8 @@ EXPORTED = ("ewsjf_queue_table_bytes", "ewsjf_workspace_bytes", "ewsjf_table_upl
             "ewsjf_route", "ewsjf_score", "ewsjf_select", "ewsjf_step", "ewsjf_step_timed", "ewsjf_ring_insert",
             "ewsjf_tactical_step", "ewsjf_ring_step", "ewsjf_window_histogram", "ewsjf_window_advance",
             "ewsjf_partition_hist", "ewsjf_dispatch", "ewsjf_trial_step", "ewsjf_trial_finish",
-            "ewsjf_status_string", "ewsjf_version")
+            "ewsjf_status_string", "ewsjf_version", "ewsjf_step_static")
+STATIC_SCRATCH_BYTES = 4 << 20
 
 
 class PartitionParams(C.Structure):
@@ -82,6 +83,8 @@ def lib():
         L.ewsjf_step_timed.argtypes = [vp, vp, i64, f32, vp, vp, i32, C.POINTER(Cost), i32, i32, vp, vp, vp, vp, sz,
                                        vp, vp]
         L.ewsjf_step_timed.restype = C.c_int
+        L.ewsjf_step_static.argtypes = [vp, vp, i64, f32, vp, vp, i32, C.POINTER(Cost), i32, i32, vp, vp, vp, vp]
+        L.ewsjf_step_static.restype = C.c_int
         L.ewsjf_ring_insert.argtypes = [vp, vp, i64, i64, vp, i64, i64, vp, vp, i64, vp]
         L.ewsjf_ring_insert.restype = C.c_int
         L.ewsjf_tactical_step.argtypes = [vp, vp, i64, f32, vp, vp, C.POINTER(Cost), i32, i32, vp, C.c_double, i32,

@@ -9,6 +9,7 @@
 #include <cstddef>
 #include <cstring>
 #include <memory>
+#include <mutex>
 
 #include "ewsjf.h"
 #include "ewsjf_launch.h"
@@ -374,6 +375,57 @@ ewsjf_status ewsjf_ring_step(int32_t* ring_len, float* ring_arrival, int64_t cap
                                           new_arrival, n_new, now, static_cast<const ewsjf_queue_table*>(table),
                                           theta, *cost, B, (flags & EWSJF_STEP_TOMBSTONE) ? ring_len : nullptr, ids,
                                           top, n_sel, ws, stream));
+}
+
+// ---------------------------------------------------------------------------
+// ewsjf_step_static: ewsjf_step with its workspace in a fixed device array,
+// for callers that cannot allocate.  Each device holds its own copy of
+// `scratch` (until the process ends); host code reaches it only through the
+// device address looked up on the first call on that device.
+// ---------------------------------------------------------------------------
+static __device__ __align__(256) uint8_t scratch[EWSJF_STATIC_SCRATCH_BYTES];
+
+static std::atomic<void*> g_scratch_ptr[kMaxDevices];
+static std::mutex g_scratch_mu;
+
+static ewsjf_status static_scratch(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return EWSJF_ERR_DEVICE;
+  void* p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+  if (p == nullptr) {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    p = g_scratch_ptr[dev].load(std::memory_order_relaxed);
+    if (p == nullptr) {
+      if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) return EWSJF_ERR_LAUNCH;
+      g_scratch_ptr[dev].store(p, std::memory_order_release);
+    }
+  }
+  *out = p;
+  return EWSJF_OK;
+}
+
+ewsjf_status ewsjf_step_static(int32_t* len, const float* arrival, int64_t n, float now, const void* table,
+                               const ewsjf_theta* theta, int32_t n_theta, const ewsjf_cost* cost, int32_t B,
+                               int32_t flags, int32_t* ids, float* top, int32_t* n_sel, hipStream_t stream) {
+  if ((n > 0 && (len == nullptr || arrival == nullptr)) || table == nullptr || theta == nullptr ||
+      cost == nullptr || ids == nullptr || top == nullptr || n_sel == nullptr)
+    return EWSJF_ERR_NULL;
+  if (n < 0 || n > kMaxN || n_theta < 1 || n_theta > EWSJF_MAX_THETA || B < 1 || B > EWSJF_MAX_B ||
+      !cost_ok(cost) || !std::isfinite(now))
+    return EWSJF_ERR_ARG;
+  if ((flags & ~EWSJF_STEP_TOMBSTONE) != 0) return EWSJF_ERR_ARG;
+  if ((flags & EWSJF_STEP_TOMBSTONE) && n_theta != 1) return EWSJF_ERR_ARG;
+  const size_t need = ewsjf::plan_step(n, n_theta, B).ws_bytes;
+  if (need > (size_t)EWSJF_STATIC_SCRATCH_BYTES) return EWSJF_ERR_WORKSPACE;
+  if (n > 0 && (!aligned16(len) || !aligned16(arrival))) return EWSJF_ERR_ALIGN;
+  const ewsjf_status ds = check_device();
+  if (ds != EWSJF_OK) return ds;
+  void* ws = nullptr;
+  const ewsjf_status ss = static_scratch(&ws);
+  if (ss != EWSJF_OK) return ss;
+  return launched(ewsjf::launch_step(len, arrival, n, now, static_cast<const ewsjf_queue_table*>(table), theta,
+                                     n_theta, *cost, B, (flags & EWSJF_STEP_TOMBSTONE) ? len : nullptr, ids, top,
+                                     n_sel, ws, stream, nullptr));
 }
 
 }  // extern "C"

@@ -315,6 +315,22 @@ def step(length: torch.Tensor, arrival: torch.Tensor, now: float, table: torch.T
     return ids, top, nsel
 
 
+def step_static(length: torch.Tensor, arrival: torch.Tensor, now: float, table: torch.Tensor, theta: torch.Tensor,
+                B: int, cost_=DEFAULT_COST, tombstone: bool = False, out=None, stream=None):
+    """ewsjf_step with the library's fixed per-device scratch (no workspace,
+    no allocation in the call; the outputs are allocated here unless given)."""
+    _need(length, torch.int32, "length")
+    _need(arrival, torch.float32, "arrival")
+    th = _theta(theta)
+    nt, n = th.shape[0], length.numel()
+    ids, top, nsel = _outs(nt, B, length.device, out)
+    c = _cost(cost_)
+    L.check(L.lib().ewsjf_step_static(_vp(length), _vp(arrival), n, float(now), _vp(table), _vp(th), nt, C.byref(c),
+                                      int(B), L.STEP_TOMBSTONE if tombstone else 0, _vp(ids), _vp(top), _vp(nsel),
+                                      _stream(stream)), "ewsjf_step_static")
+    return ids, top, nsel
+
+
 def ring_step(ring_len: torch.Tensor, ring_arrival: torch.Tensor, pos: int, new_len: torch.Tensor,
               new_arrival: torch.Tensor, now: float, table: torch.Tensor, theta: torch.Tensor, B: int,
               cost_=DEFAULT_COST, window: torch.Tensor | None = None, wpos: int = 0, tombstone: bool = False, out=None,

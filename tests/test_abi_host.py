@@ -104,6 +104,30 @@ def test_step_argument_errors():
     assert step(arr=FAKE_MIS) == L.ERR_ALIGN
 
 
+def test_step_static_argument_errors():
+    lib = L.lib()
+    c = L.Cost(0.01, 1e-4, 0.0)
+
+    def st(length=FAKE, arr=FAKE, n=1000, now=60.0, table=FAKE, theta=FAKE, nt=1, cost=c, B=64, flags=0,
+           ids=FAKE, top=FAKE, nsel=FAKE):
+        return lib.ewsjf_step_static(length, arr, n, now, table, theta, nt, C.byref(cost) if cost is not None else None,
+                                     B, flags, ids, top, nsel, None)
+
+    assert st(length=None) == L.ERR_NULL
+    assert st(ids=None) == L.ERR_NULL
+    assert st(cost=None) == L.ERR_NULL
+    assert st(n=-1) == L.ERR_ARG and st(B=0) == L.ERR_ARG and st(nt=0) == L.ERR_ARG
+    assert st(flags=L.STEP_TOMBSTONE, nt=2) == L.ERR_ARG
+    assert st(cost=L.Cost(1e-50, 0.0, 0.0)) == L.ERR_ARG
+    # sizes whose workspace exceeds the fixed scratch are refused before any device work
+    assert lib.ewsjf_workspace_bytes(L.OP_STEP, 4194304, 16, 4096, None) > L.STATIC_SCRATCH_BYTES
+    assert st(n=4194304, nt=16, B=4096) == L.ERR_WORKSPACE
+    assert st(n=1 << 20, nt=56, B=256) == L.ERR_WORKSPACE
+    # the largest pools with one vector fit; without a GPU the call stops at the device check
+    assert st(n=(1 << 31) - 1, B=4096) == L.ERR_DEVICE
+    assert st(n=1 << 20, nt=55, B=256) == L.ERR_DEVICE
+
+
 def test_select_route_score_argument_errors():
     lib = L.lib()
     c = L.Cost(0.01, 1e-4, 0.0)
