@@ -137,7 +137,8 @@ typedef struct {
 /* Estimated prefill cost C_prefill(b) = c0 + c1*b + c2*b^2 seconds (host struct).
  * The kernels evaluate it in binary32: c0 must lie in [FLT_MIN, FLT_MAX], c1
  * and c2 must each be 0 or lie in that range, and (b + 1) C_prefill(b) must
- * not exceed FLT_MAX / 2 for b = 2^31 - 1 (the longest length); otherwise
+ * not exceed 1 / (2 FLT_MIN) (about 4.25e37) for b = 2^31 - 1 (the longest
+ * length), which keeps its binary32 reciprocal a normal number; otherwise
  * EWSJF_ERR_ARG. */
 typedef struct {
   double c0, c1, c2;

@@ -40,16 +40,17 @@ ewsjf_status check_device() {
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 
-// The kernels evaluate C_prefill and (b + 1) C_prefill(b) in binary32: c0
-// must be a normal binary32 value and c1, c2 zero or normal, and (b + 1) C(b)
-// must stay within half of FLT_MAX up to the longest int32 length (it grows
-// with b), so that C is finite and nonzero there for every request.
+// The kernels evaluate C_prefill and the reciprocal of (b + 1) C_prefill(b)
+// in binary32: c0 must be a normal binary32 value and c1, c2 zero or normal,
+// and (b + 1) C(b) must stay at most 1 / (2 FLT_MIN) up to the longest int32
+// length (it grows with b), so that C is finite and nonzero and the
+// reciprocal a normal number for every request.
 bool f32_normal(double x) { return x >= (double)FLT_MIN && x <= (double)FLT_MAX; }
 bool cost_ok(const ewsjf_cost* c) {
   if (!(f32_normal(c->c0) && (c->c1 == 0.0 || f32_normal(c->c1)) && (c->c2 == 0.0 || f32_normal(c->c2))))
     return false;
   const double b = 2147483647.0;
-  return (b + 1.0) * (c->c0 + c->c1 * b + c->c2 * b * b) <= 0.5 * (double)FLT_MAX;
+  return (b + 1.0) * (c->c0 + c->c1 * b + c->c2 * b * b) <= 0.5 / (double)FLT_MIN;
 }
 
 bool params_ok(const ewsjf_partition_params* p) {

@@ -608,25 +608,27 @@ struct CostF {
 
 // Phi (Eq. 1 / Eq. 4) regrouped as three per-request terms and the folded
 // per-queue weights of one parameter vector:
-//   Phi = (q+1) w_b alpha + (q+1) w_u beta + (q+1) w_f ln2 gamma,
-//   alpha = 1/(b+1), beta = W / ((b+1) C), gamma = log2(b+1) / (b+1).
+//   Phi = ((q+1) w_b + (q+1) w_f ln2 lg) alpha + (q+1) w_u beta,
+//   alpha = 1/(b+1), beta = W / ((b+1) C), lg = log2(b+1).
 // Every kernel that forms a request's key uses these two functions, so a
 // request gets the same key wherever it is scored (the merge's re-reads
 // compare keys with the streaming kernel's).
 struct PhiTerms {
-  float al, be, ga;
+  float al, be, lg;
 };
+// kLinear: the caller knows c2 == 0 and C is one FMA; the value is the same
+// (fma(0, b, c1) = c1 exactly).
+template <bool kLinear = false>
 __device__ __forceinline__ PhiTerms phi_terms(int b, float arrival, float now, const CostF& c) {
   const float fb = (float)b;
   const float bp1 = fb + 1.0f;
   const float W = fmaxf(now - arrival, 0.0f);  // NaN arrival or future arrival -> 0
-  const float C = __builtin_fmaf(__builtin_fmaf(c.c2, fb, c.c1), fb, c.c0);
+  const float C = kLinear ? __builtin_fmaf(c.c1, fb, c.c0) : __builtin_fmaf(__builtin_fmaf(c.c2, fb, c.c1), fb, c.c0);
   const float r = __builtin_amdgcn_rcpf(bp1 * C);
-  const float al = C * r;
-  return PhiTerms{al, W * r, __builtin_amdgcn_logf(bp1) * al};
+  return PhiTerms{C * r, W * r, __builtin_amdgcn_logf(bp1)};
 }
 __device__ __forceinline__ float phi_of(const QParams& p, const PhiTerms& t) {
-  return __builtin_fmaf(p.wb, t.al, __builtin_fmaf(p.wu, t.be, p.wf2 * t.ga));
+  return __builtin_fmaf(__builtin_fmaf(p.wf2, t.lg, p.wb), t.al, p.wu * t.be);
 }
 __device__ __forceinline__ float phi_f32(int b, float arrival, float now, const QParams& p, const CostF& c) {
   return phi_of(p, phi_terms(b, arrival, now, c));
@@ -639,6 +641,21 @@ __device__ __forceinline__ uint32_t ukey_fast(float f) {
   f = f + 0.0f;                     // -0 + 0 = +0
   const uint32_t u = __float_as_uint(f);
   return u ^ ((uint32_t)((int32_t)u >> 31) | 0x80000000u);
+}
+
+// The same key for a score known to be +0, positive or +inf: the bits with
+// the sign bit set.  When every per-queue weight of the parameter vector is
+// positive, every request of length >= 1 has such a score: its three terms
+// are >= 0 and finite except beta (+inf for an arrival of -inf), and the
+// reciprocal stays a normal number under the cost bounds the library
+// enforces, so no product is NaN and no sum is -0.
+__device__ __forceinline__ uint32_t ukey_pos(float f) { return __float_as_uint(f) | 0x80000000u; }
+
+// min(max(b, 1), L) in one instruction.
+__device__ __forceinline__ int clamp_len(int b, int L) {
+  int r;
+  asm("v_med3_i32 %0, %1, 1, %2" : "=v"(r) : "v"(b), "s"(L));
+  return r;
 }
 
 // Stage the routing lut and per-queue constants of one parameter vector into

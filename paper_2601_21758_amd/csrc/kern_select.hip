@@ -51,8 +51,11 @@ struct PoolSource {
     f32x4 a;
   };
   struct Shared {
-    uint64_t route[kRouteWords];
+    // The routing map with each word's base queue scaled to its byte offset in
+    // qp (16 q), so a request's weights are found with one add.
+    uint64_t routeq[kRouteWords];
     QParams qp[EWSJF_MAX_QUEUES];
+    uint8_t qpos[EWSJF_MAX_QUEUES];  // 1: the queue's three weights are all positive (or the queue is unused)
     int L;
   };
   struct Stage {
@@ -60,6 +63,11 @@ struct PoolSource {
     double mean;
     i32x4 hdr;    // k, max_len, ...
     float th[6];  // the parameter vector
+  };
+  // How keys are formed (uniform; key_mode after the staging barrier).
+  struct KeyMode {
+    bool linear;    // c2 == 0
+    bool positive;  // every weight positive: ukey_pos
   };
 
   // Run by the first kStageThreads threads, before any pool load is issued.
@@ -95,15 +103,31 @@ struct PoolSource {
     // of the pool loads.
     Stage st = st0;
     pin(st.th[0], st.th[1], st.th[2], st.th[3], st.th[4], st.th[5], st.hdr, st.mean);
-    i32x4* dst = reinterpret_cast<i32x4*>(sh.route);
+    static_assert(sizeof(QParams) == 16, "a queue's weights are 16 bytes");
+    i32x4* dst = reinterpret_cast<i32x4*>(sh.routeq);
 #pragma unroll
     for (int r = 0; r < kRoutePerThread; ++r) {
       const int i = threadIdx.x + r * kStageThreads;
-      if (r + 1 < kRoutePerThread || i < kRouteVecs) dst[i] = st.v[r];
+      i32x4 v = st.v[r];  // two words: (mask, base) (mask, base)
+      v.y <<= 4;
+      v.w <<= 4;
+      if (r + 1 < kRoutePerThread || i < kRouteVecs) dst[i] = v;
     }
     const ewsjf_theta th{st.th[0], st.th[1], st.th[2], st.th[3], st.th[4], st.th[5]};
-    if ((int)threadIdx.x < st.hdr.x) sh.qp[threadIdx.x] = make_qparams(th, st.mean, threadIdx.x);
+    uint8_t pos = 1;
+    if ((int)threadIdx.x < st.hdr.x) {
+      const QParams q = make_qparams(th, st.mean, threadIdx.x);
+      sh.qp[threadIdx.x] = q;
+      pos = q.wb > 0.0f && q.wu > 0.0f && q.wf2 > 0.0f;
+    }
+    sh.qpos[threadIdx.x] = pos;
     if (threadIdx.x == 0) sh.L = st.hdr.y;
+  }
+
+  __device__ __forceinline__ KeyMode key_mode(const Shared& sh) const {
+    static_assert(EWSJF_MAX_QUEUES == 4 * kWave, "one word of four flags per lane");
+    const uint32_t w = reinterpret_cast<const uint32_t*>(sh.qpos)[threadIdx.x & (kWave - 1)];
+    return KeyMode{cost.c2 == 0.0f, __ballot(w != 0x01010101u) == 0ull};
   }
 
   __device__ __forceinline__ Raw load4(int64_t base, int64_t n) const {
@@ -131,17 +155,35 @@ struct PoolSource {
     return r;
   }
 
-  __device__ __forceinline__ uint32_t key1(int b, float a, const Shared& sh) const {
-    const int bc = min(max(b, 1), sh.L);
-    const float phi = phi_f32(b, a, now, sh.qp[route_queue(sh.route, bc)], cost);
-    return b > 0 ? ukey_fast(phi) : 0u;
+  template <bool kLinear, bool kPositive>
+  __device__ __forceinline__ uint32_t key1(int b, float a, const Shared& sh, int L) const {
+    const int bc = clamp_len(b, L);
+    const uint64_t w = sh.routeq[bc >> 5];
+    const uint32_t off = (uint32_t)(w >> 32) + ((uint32_t)__builtin_popcount((uint32_t)w << (31 - (bc & 31))) << 4);
+    const QParams& p = *reinterpret_cast<const QParams*>(reinterpret_cast<const uint8_t*>(sh.qp) + off);
+    const float phi = phi_of(p, phi_terms<kLinear>(b, a, now, cost));
+    return b > 0 ? (kPositive ? ukey_pos(phi) : ukey_fast(phi)) : 0u;
   }
 
-  __device__ __forceinline__ void keys4(const Raw& r, const Shared& sh, uint32_t out[4]) const {
-    out[0] = key1(r.l.x, r.a.x, sh);
-    out[1] = key1(r.l.y, r.a.y, sh);
-    out[2] = key1(r.l.z, r.a.z, sh);
-    out[3] = key1(r.l.w, r.a.w, sh);
+  template <bool kLinear, bool kPositive>
+  __device__ __forceinline__ void keys4_t(const Raw& r, const Shared& sh, uint32_t out[4]) const {
+    const int L = __builtin_amdgcn_readfirstlane(sh.L);
+    out[0] = key1<kLinear, kPositive>(r.l.x, r.a.x, sh, L);
+    out[1] = key1<kLinear, kPositive>(r.l.y, r.a.y, sh, L);
+    out[2] = key1<kLinear, kPositive>(r.l.z, r.a.z, sh, L);
+    out[3] = key1<kLinear, kPositive>(r.l.w, r.a.w, sh, L);
+  }
+
+  // The key of each of 4 requests (0 for an empty slot); one uniform branch
+  // picks the form.
+  __device__ __forceinline__ void keys4(const Raw& r, const Shared& sh, const KeyMode& km, uint32_t out[4]) const {
+    if (km.linear) {
+      if (km.positive) keys4_t<true, true>(r, sh, out);
+      else keys4_t<true, false>(r, sh, out);
+    } else {
+      if (km.positive) keys4_t<false, true>(r, sh, out);
+      else keys4_t<false, false>(r, sh, out);
+    }
   }
 
   __device__ __forceinline__ bool skip(int) const { return false; }
@@ -229,12 +271,15 @@ struct FifoSource {
     return r;
   }
 
+  struct KeyMode {};
+  __device__ __forceinline__ KeyMode key_mode(const Shared&) const { return {}; }
+
   __device__ __forceinline__ uint32_t key1(int b, float a, const Shared& sh) const {
     const int bc = min(max(b, 1), sh.L);
     return (b > 0 && route_queue(sh.route, bc) == sh.qsel) ? fifo_key(a) : 0u;
   }
 
-  __device__ __forceinline__ void keys4(const Raw& r, const Shared& sh, uint32_t out[4]) const {
+  __device__ __forceinline__ void keys4(const Raw& r, const Shared& sh, const KeyMode&, uint32_t out[4]) const {
     out[0] = key1(r.l.x, r.a.x, sh);
     out[1] = key1(r.l.y, r.a.y, sh);
     out[2] = key1(r.l.z, r.a.z, sh);
@@ -356,7 +401,10 @@ struct ScoreSource {
   // A NaN score marks an element that is not admissible.
   __device__ __forceinline__ static uint32_t key1(float s) { return (s != s) ? 0u : ukey_of(s); }
 
-  __device__ __forceinline__ void keys4(const Raw& r, const Shared&, uint32_t out[4]) const {
+  struct KeyMode {};
+  __device__ __forceinline__ KeyMode key_mode(const Shared&) const { return {}; }
+
+  __device__ __forceinline__ void keys4(const Raw& r, const Shared&, const KeyMode&, uint32_t out[4]) const {
     out[0] = key1(r.s.x);
     out[1] = key1(r.s.y);
     out[2] = key1(r.s.z);
@@ -563,6 +611,8 @@ __device__ __forceinline__ void publish_list_wave(const ListShared& ls, int cnt,
 
 // Chunks each wave has in flight when it starts scoring (2, 3 or 4).
 constexpr int kAhead = 2;
+// Stage the table before the first pool load is issued.
+constexpr bool kTableFirst = false;
 static_assert(kAhead >= 2 && kAhead <= kChunksPerPass, "chunks in flight");
 
 template <class Src>
@@ -598,27 +648,46 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
   const bool stager = wv < kStageWaves;  // wave-uniform
   typename Src::Stage st;
   if (stager) src.stage_load(st, t);
-  // The compute unit serves a workgroup's loads roughly in issue order; this
-  // barrier (which does not wait for the loads) puts every table load ahead
-  // of every pool load, so the table lands after one latency.
-  __builtin_amdgcn_s_barrier();
   typename Src::Raw raw[kChunksPerPass];
-  load_one(src, n, G, 0, 0, raw[0]);
-  load_one(src, n, G, 0, 1, raw[1]);
-  if constexpr (kAhead >= 3) load_one(src, n, G, 0, 2, raw[2]);
-  if constexpr (kAhead >= 4) load_one(src, n, G, 0, 3, raw[3]);
-  if (stager) src.stage_store(sh, st);
-  if (threadIdx.x == 0) {
-    ls.ovf = 0;
-    ls.nout = 0;
-    ls.nspill = 0;
-    ls.lowbar = 0u;
+  auto init_list = [&]() {
+    if (threadIdx.x == 0) {
+      ls.ovf = 0;
+      ls.nout = 0;
+      ls.nspill = 0;
+      ls.lowbar = 0u;
+    }
+    if (threadIdx.x < kShortList) ls.rank[threadIdx.x] = 0;
+    static_assert(kListCap == kBlock, "one spill entry per thread");
+    if constexpr (Src::kClustered) ls.spill[threadIdx.x] = 0ull;
+  };
+  if constexpr (kTableFirst) {
+    // The table lands in LDS before any pool load is issued, and the only
+    // barrier before scoring comes first too: a wave stalls at a vector load
+    // while the compute unit's memory queue is full, so a barrier behind pool
+    // loads waits until most of them have been served.
+    if (stager) src.stage_store(sh, st);
+    init_list();
+    __syncthreads();
+    EWSJF_STAMP(kStampLocal, 1);
+    load_one(src, n, G, 0, 0, raw[0]);
+    load_one(src, n, G, 0, 1, raw[1]);
+    if constexpr (kAhead >= 3) load_one(src, n, G, 0, 2, raw[2]);
+    if constexpr (kAhead >= 4) load_one(src, n, G, 0, 3, raw[3]);
+  } else {
+    // The compute unit serves a workgroup's loads roughly in issue order; this
+    // barrier (which does not wait for the loads) puts every table load ahead
+    // of every pool load.
+    __builtin_amdgcn_s_barrier();
+    load_one(src, n, G, 0, 0, raw[0]);
+    load_one(src, n, G, 0, 1, raw[1]);
+    if constexpr (kAhead >= 3) load_one(src, n, G, 0, 2, raw[2]);
+    if constexpr (kAhead >= 4) load_one(src, n, G, 0, 3, raw[3]);
+    if (stager) src.stage_store(sh, st);
+    init_list();
+    __syncthreads();
+    EWSJF_STAMP(kStampLocal, 1);
   }
-  if (threadIdx.x < kShortList) ls.rank[threadIdx.x] = 0;
-  static_assert(kListCap == kBlock, "one spill entry per thread");
-  if constexpr (Src::kClustered) ls.spill[threadIdx.x] = 0ull;
-  __syncthreads();
-  EWSJF_STAMP(kStampLocal, 1);
+  const auto km = src.key_mode(sh);
 
   // Each wave writes every element whose key is >= its bar into its own
   // region of the list.  The bar (wave_group_bar over the lane maxima of the
@@ -637,16 +706,16 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
     // other waves keep the pipeline full meanwhile.
     // Chunk j >= kAhead is issued once chunk j - kAhead is scored.
     sched_fence();
-    src.keys4(raw[0], sh, key + 0);
+    src.keys4(raw[0], sh, km, key + 0);
     sched_fence();
     if constexpr (kAhead == 2) load_one(src, n, G, pass, 2, raw[2]);
     if constexpr (kAhead == 3) load_one(src, n, G, pass, 3, raw[3]);
     sched_fence();
-    src.keys4(raw[1], sh, key + 4);
+    src.keys4(raw[1], sh, km, key + 4);
     sched_fence();
     if constexpr (kAhead == 2) load_one(src, n, G, pass, 3, raw[3]);
     sched_fence();
-    src.keys4(raw[2], sh, key + 8);
+    src.keys4(raw[2], sh, km, key + 8);
     // The bar comes from the first three chunks, so it is ready while the
     // last chunk is still in flight; every element (the last chunk's too)
     // at or above it is written.
@@ -654,7 +723,7 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
 #pragma unroll
     for (int e = 0; e < 12; ++e) lmax = key[e] > lmax ? key[e] : lmax;
     const uint32_t bar = wave_group_bar(lmax, lg);
-    src.keys4(raw[3], sh, key + 12);
+    src.keys4(raw[3], sh, km, key + 12);
     sched_fence();
     // The next pass's first chunks (empty after the last pass): without a
     // branch, so waits on the loads above keep their exact counts.
@@ -867,9 +936,9 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
 // and lists candidates for kThetaPerBlock vectors in turn.  Routing, the
 // log, the reciprocal and the wait are the same for every vector, so they
 // are computed once per request as three terms,
-//   alpha = 1 / (b+1),  beta = W / ((b+1) C),  gamma = log2(b+1) / (b+1),
-// and a vector's score is Phi = (q+1) w_b alpha + (q+1) w_u beta +
-// (q+1) w_f ln2 gamma (Eq. 1 / Eq. 4 regrouped), three FMAs with the
+//   alpha = 1 / (b+1),  beta = W / ((b+1) C),  lg = log2(b+1),
+// and a vector's score is Phi = ((q+1) w_b + (q+1) w_f ln2 lg) alpha +
+// (q+1) w_u beta (Eq. 1 / Eq. 4 regrouped), three operations with the
 // folded per-queue weights.  The list work per vector is as in
 // local_candidates; the counters it uses alternate between two copies, so
 // one vector's list can be published while the next vector's keys are
@@ -1350,7 +1419,7 @@ __device__ void merge_exact(const Src& src0, int t, int64_t n, int G, int M, int
         const int64_t b0 = cidx < nchunks ? cidx * kChunk + (int64_t)lane * 4 : n;
         const typename Src::Raw r = src.load4(b0, n);
         uint32_t k4[4];
-        src.keys4(r, sh, k4);
+        src.keys4(r, sh, src.key_mode(sh), k4);
         const uint64_t lowb = tau > 1ull ? tau : 1ull;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
