@@ -18,7 +18,7 @@ constexpr int kChunksPerPass = 4;            // chunks a wave holds in registers
 constexpr int kElemsPerLane = 4 * kChunksPerPass;
 constexpr int kMaxGrid = 256;                // streaming workgroups (one per CU)
 constexpr int kListCap = 1024;               // per-workgroup candidate list in LDS
-constexpr int kShortList = 256;              // lists ranked by all waves at once (up to 4 entries per lane)
+constexpr int kShortList = 512;              // lists ranked by all waves at once (up to 8 entries per lane)
 constexpr int kWaveCap = kListCap / (kBlock / kWave);  // one region of the list per wave
 constexpr int kOverCap = 128;                // overflow entries kept per workgroup
 constexpr int kDenseWave = 32;              // region entries that mark a wave holding a cluster of high keys

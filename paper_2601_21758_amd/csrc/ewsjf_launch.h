@@ -34,7 +34,12 @@ struct CandBufs {
 
 // packed: each workgroup takes a full pass of chunks (the many-vector step).
 // max_grid > 0 caps the streaming workgroups per row (default: one per CU).
-SelectPlan plan_select(int64_t n, int32_t n_theta, int32_t B, bool packed = false, int max_grid = 0);
+// spread: the source's highest keys are not expected to cluster in one
+// share (the pool and ring steps), so the candidate bars are set from the
+// expected spread of the B; otherwise for the worst case (all of a
+// workgroup's share of the B in one wave).  Sizes do not depend on it.
+SelectPlan plan_select(int64_t n, int32_t n_theta, int32_t B, bool packed = false, int max_grid = 0,
+                       bool spread = false);
 // The plan ewsjf_step uses: packed for several vectors over a pool that fits
 // one pass per workgroup.
 SelectPlan plan_step(int64_t n, int32_t n_theta, int32_t B);

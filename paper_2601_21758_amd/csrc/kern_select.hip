@@ -23,6 +23,8 @@
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
+#include <cmath>
+
 #include "ewsjf_device.h"
 #include "ewsjf_launch.h"
 #include "ewsjf_stamps.h"
@@ -834,22 +836,62 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
     return;
   }
   if constexpr (!Src::kClustered) {
-    // The workgroup's bound: the largest wave bar (lane i < 16 reads wave i's).
-    // Each wave keeps its entries at or above it; a scan of the kept counts
-    // over the waves places them in list2.
-    const uint32_t T_bar = wave_max_u32(lane < kWavesPerBlock ? ls.bar[lane] : 0u);
+    // The workgroup's bound would be the largest wave bar t1 (lane i < 16
+    // reads wave i's).  One wave holding a few high keys in each of its lane
+    // groups sets t1 alone, and t1 can then exceed the B-th key of the whole
+    // pool, which sends the merge back to the share.  So in a single pass
+    // (the keys are still in registers) the wave holding t1 also lists its
+    // keys in [t2, t1), t2 the second largest bar, and the bound drops to t2.
+    // Each wave keeps its entries at or above the bound; a scan of the kept
+    // counts over the waves places them in list2.
+    const uint32_t b = lane < kWavesPerBlock ? ls.bar[lane] : 0u;
+    const uint32_t t1 = wave_max_u32(b);
+    const int v1 = (int)__builtin_ctzll(__ballot(lane < kWavesPerBlock && b == t1));
+    const uint32_t t2 = wave_max_u32(lane != v1 ? b : 0u);
+    const bool lower = passes == 1 && t2 != 0u && t2 < t1;  // uniform
+    const uint32_t T_bar = lower ? t2 : t1;
     const uint64_t lowc = (uint64_t)T_bar << 32;
     const uint64_t x = lane < ls.wcnt[wv] ? region[lane] : 0ull;
     const bool keep = x >= lowc && x != 0ull;
     const uint64_t km = __ballot(keep);
     if (lane == 0) ls.wkeep[wv] = __popcll(km);
+    // The wave holding t1 hands its keys to the workgroup (key e of lane l
+    // at e * kWave + l); after the barrier wave w filters keys e = w, so the
+    // extra keys cost every wave a few instructions rather than one wave a
+    // long serial run.
+    uint32_t* const held = reinterpret_cast<uint32_t*>(ls.spill);
+    static_assert(kElemsPerLane == kWavesPerBlock && kElemsPerLane * kWave * 4 <= sizeof(ls.spill),
+                  "one handed-over key per wave and lane");
+    if (lower && wv == v1) {  // uniform
+#pragma unroll
+      for (int e = 0; e < kElemsPerLane; ++e) held[e * kWave + lane] = key[e];
+    }
     __syncthreads();
     const int kc = lane < kWavesPerBlock ? ls.wkeep[lane] : 0;
     const int incl = wave_incl_scan_add(kc);
-    const int total = __builtin_amdgcn_readlane(incl, kWavesPerBlock - 1);
+    const int nreg = __builtin_amdgcn_readlane(incl, kWavesPerBlock - 1);
     const int off = __builtin_amdgcn_readlane(incl - kc, wv);
-    if (keep) ls.list2[off + lanes_below(km)] = x;  // total <= kListCap: at most kWave per wave
+    if (keep) ls.list2[off + lanes_below(km)] = x;  // nreg <= kListCap: at most kWave per wave
+    if (lower) {  // uniform
+      // Keys of wave v1 in [t2, t1) go after the regions' entries, in any
+      // order (the list is ranked by value when published).
+      const uint32_t k = held[wv * kWave + lane];
+      const bool p = k >= t2 && k < t1;
+      const uint64_t sm = __ballot(p);
+      if (sm != 0ull) {
+        int base = 0;
+        if (lane == 0) base = atomicAdd(&ls.nout, __popcll(sm));
+        base = __shfl(base, 0);
+        const int at = nreg + base + lanes_below(sm);
+        // the chunk that element e = wv of wave v1 came from (single pass)
+        const int64_t c = (int64_t)blockIdx.x + (int64_t)G * (v1 + kWavesPerBlock * (wv / 4));
+        if (p && at < kListCap) ls.list2[at] = make_comp(k, (uint32_t)(c * kChunk + lane * 4 + (wv & 3)));
+      }
+    }
     __syncthreads();
+    // more than kListCap entries only with many extra keys: publish_list
+    // then marks the list incomplete
+    const int total = nreg + (lower ? ls.nout : 0);
     EWSJF_STAMP(kStampLocal, 4);
     EWSJF_STAMP_VALUE(kStampLocal, 6, total);
     if (total > M && total <= kShortWave) {  // uniform: one wave ranks and places
@@ -1628,7 +1670,30 @@ static void launch_merge_rank(const SelectPlan& p, hipStream_t stream, hipEvent_
 // ---------------------------------------------------------------------------
 // Host-side launch helpers.
 // ---------------------------------------------------------------------------
-SelectPlan plan_select(int64_t n, int32_t n_theta, int32_t B, bool packed, int max_grid) {
+// For a source whose highest keys fall anywhere in the pool (no cluster in
+// one share): the smallest lg in [2, worst] for which bars above the pool's
+// B-th key are rare.  A wave's bar (the least of 2^lg lane-group maxima
+// over its first three chunks) lies above that key when every group holds
+// one of the B; with the B spread at density d = B / n, a group of E / 2^lg
+// keys holds one with probability 1 - exp(-d E / 2^lg).  In a single pass
+// the workgroup's bound is its second largest bar, so two such waves in one
+// workgroup are needed, else one wave anywhere; either must be expected in
+// fewer than one step in a thousand.  Data that breaks the assumption only
+// sends the merge back to the share (exact, slower).
+static int spread_lg(int64_t n, int G, int B, int passes, int64_t chunks_per_wave, int worst) {
+  const double d = (double)B / (double)n;
+  const double E = (double)kChunk * (double)(chunks_per_wave < 3 ? chunks_per_wave : 3);
+  const double waves = (double)G * kWavesPerBlock * passes;
+  for (int lg = 2; lg < worst; ++lg) {
+    const double g = (double)(1 << lg);
+    const double pw = std::pow(-std::expm1(-d * E / g), g);  // one wave's bar above the B-th key
+    const double fail = passes == 1 ? (double)G * (kWavesPerBlock * (kWavesPerBlock - 1) / 2) * pw * pw : waves * pw;
+    if (fail <= 1e-3) return lg;
+  }
+  return worst;
+}
+
+SelectPlan plan_select(int64_t n, int32_t n_theta, int32_t B, bool packed, int max_grid, bool spread) {
   SelectPlan p;
   const int64_t nchunks = (n + kChunk - 1) / kChunk;
   // Packed: every wave holds all four chunks of its one pass.
@@ -1646,6 +1711,12 @@ SelectPlan plan_select(int64_t n, int32_t n_theta, int32_t B, bool packed, int m
   if (m > 64) m = 64;
   int lg = 0;
   while ((2 << lg) <= m) ++lg;
+  if (spread && !packed && n > 0) {
+    const int64_t my_chunks = (nchunks + G - 1) / G;
+    const int64_t per_pass = (int64_t)kWavesPerBlock * kChunksPerPass;
+    const int passes = (int)((my_chunks + per_pass - 1) / per_pass);
+    lg = spread_lg(n, p.G, B, passes, (my_chunks + kWavesPerBlock - 1) / kWavesPerBlock, lg);
+  }
   p.lg = lg;
   int M = pow2_ceil(4 * per);
   if (M < 16) M = 16;
@@ -1707,7 +1778,7 @@ hipError_t launch_step(const int32_t* len, const float* arrival, int64_t n, floa
                        const ewsjf_cost& cost, int32_t B, int32_t* tomb_len, int32_t* ids, float* top,
                        int32_t* n_sel, void* ws, hipStream_t stream, hipEvent_t* marks) {
   const bool packed = step_packed(n, n_theta);
-  const SelectPlan p = plan_select(n, n_theta, B, packed);
+  const SelectPlan p = plan_select(n, n_theta, B, packed, 0, true);
   const CandBufs cb = carve(p, ws);
   PoolSource src;
   src.len = len;
@@ -1756,7 +1827,7 @@ hipError_t launch_ring_step(int32_t* ring_len, float* ring_arrival, int64_t capa
                             int64_t n_new, float now, const ewsjf_queue_table* table, const ewsjf_theta* theta,
                             const ewsjf_cost& cost, int32_t B, int32_t* tomb_len, int32_t* ids, float* top,
                             int32_t* n_sel, void* ws, hipStream_t stream) {
-  const SelectPlan p = plan_select(capacity, 1, B);
+  const SelectPlan p = plan_select(capacity, 1, B, false, 0, true);
   const CandBufs cb = carve(p, ws);
   RingSource src;
   src.len = ring_len;

@@ -202,6 +202,20 @@ def test_step_full_4m_pool(E):
     check_admission(ids[0], top[0], nsel[0], rids[0], rtop[0], rnsel[0], rs[0])
 
 
+@pytest.mark.parametrize("draw", [1, 4, 5])
+def test_step_full_4m_pool_other_draws(E, draw):
+    # Independent draws of the 4M recipe in which one wave's bar alone lies
+    # above the pool's B-th key in some workgroup: the lowered workgroup
+    # bound (second largest wave bar) and the keys it adds are exercised on
+    # real data, and the merge's answer must not change.
+    p = W.config(2, draw=draw)
+    say(f"step cfg2 draw {draw} n={p.n}")
+    t = oracle_table(p)
+    ids, top, nsel, _ = run_step(E, p, t)
+    rids, rtop, rnsel, rs = oracle.step(p.length, p.arrival, p.now, t, p.theta, p.B, p.cost)
+    check_admission(ids[0], top[0], nsel[0], rids[0], rtop[0], rnsel[0], rs[0])
+
+
 def test_step_batched_theta(E):
     # the batched-parameter workload at full shape: every one of the 256
     # admission sets against the oracle (32 vectors per oracle call)
