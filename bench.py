@@ -8,31 +8,39 @@ parameter vector at the midpoint of its ranges, top B = 1,024 admissions.
 
 A timed step is one fused ewsjf_step: every pending request is routed,
 scored and considered for admission, and the top-B ids come back.  The pool
-sits in HBM; `--rotate` distinct copies (10 x 32 MiB by default, more than
-the 256 MiB Infinity Cache) are stepped in turn so each step reads HBM.
-Steps run from a captured HIP graph (chunks of up to 50 steps) so host
-launch cost does not bound the loop; an eager pass with per-kernel events
-gives each kernel's own duration (start/end events bound to the kernel's
-dispatch) for the roofline figure.  "step_percentiles_us" gives p10/p50/p90
-of the step per graph replay and per eager step, and of each kernel;
-"copy_reference" is a plain device-to-device copy's bandwidth on the same
-GPU.
+sits in HBM; `--rotate` independent draws of the same recipe (10 x 32 MiB by
+default, more than the 256 MiB Infinity Cache) are stepped in turn, so each
+step reads HBM and no step's input repeats the one before.  Steps run from
+captured HIP graphs (chunks of up to 50 steps, at least four replays) so
+host launch cost does not bound the loop; an eager pass with per-kernel
+events gives each kernel's own duration (start/end events bound to the
+kernel's dispatch) for the roofline figure.  "step_percentiles_us" gives
+p10/p50/p90 of the step per graph replay and per eager step, and of each
+kernel; "copy_reference" is a plain device-to-device copy's bandwidth on the
+same GPU.
 
-More workloads ride along in the same JSON line (skip them with
---no-extra): "tactical" -- Algorithm 1's own batch rule on the same 4M pool
-(ewsjf_tactical_step); "batched_theta" -- one 1,048,576-request pool scored and
-selected under 256 parameter vectors per step (top-256 each); "streaming"
--- 10,000 steps of the streaming scheduler (1,048,576-slot ring, 4,096
-arrivals and 512 admissions per step, Refine-and-Prune over the last
-65,536 arrivals every 100 steps on a side stream), per-step device latency
-p50/p99 over steps 100..9,999; "window_and_dispatch" -- the sliding-window
-histogram kernels and the Dispatcher with bubble queues on the streaming
-shapes; "trial" -- trials of 16 scoring-parameter proposals, each on its own
-1,048,576-slot ring with common arrivals (ewsjf_trial_step).
+More workloads ride along in the same JSON line (`--extra`, a comma list,
+default all; `--no-extra` for none): "small_configs" -- the same step on
+the 4,096-request and 262,144-request pools; "tactical" -- Algorithm 1's own
+batch rule on the 4M pool (ewsjf_tactical_step); "batched_theta" -- one
+1,048,576-request pool scored and selected under 256 parameter vectors per
+step (top-256 each), with its VALU roofline from the committed counters;
+"streaming" -- 10,000 steps of the streaming scheduler (1,048,576-slot
+ring, 4,096 arrivals and 512 admissions per step, Refine-and-Prune over the
+last 65,536 arrivals every 100 steps on a side stream), per-step device
+latency p50/p99 over steps 100..9,999; "window_and_dispatch" -- the
+sliding-window histogram kernels and the Dispatcher with bubble queues on
+the streaming shapes; "trial" -- trials of 16 scoring-parameter proposals,
+each on its own 1,048,576-slot ring with common arrivals
+(ewsjf_trial_step).
+
+"cpu_baseline" times the oracle (one thread) on each pool, median of three
+timed runs, with the host's CPU count and model.
 
 Prints one JSON line.  Flags: --gpus (only 1 is supported), --steps,
---warmup, --rotate, --no-cpu (skip the oracle baseline), --no-extra,
---stream-steps.
+--warmup, --rotate, --no-cpu (skip the oracle baseline), --extra,
+--no-extra, --stream-steps, --copy-probe-mib (calibration kernels for
+counter runs).
 """
 from __future__ import annotations
 
@@ -40,6 +48,7 @@ import argparse
 import ctypes as C
 import hashlib
 import json
+import math
 import os
 import sys
 import time
@@ -50,8 +59,12 @@ sys.path.insert(0, ROOT)
 METRIC = "pending requests routed+scored+selected per sec at 4M pool; % HBM peak"
 HBM_PEAK_GBS = 8000.0
 BYTES_PER_REQUEST = 8  # int32 prompt length + float32 arrival, each read once
-PROFILE = os.path.join(ROOT, "profiles", "local_candidates_large_mixed_4m.pmc.txt")
+PROFILE = os.path.join(ROOT, "profiles", "fused_step_large_mixed_4m.pmc.txt")
+PROFILE_BATCHED = os.path.join(ROOT, "profiles", "batched_theta_1m.pmc.txt")
 KERNEL_SOURCES = ("paper_2601_21758_amd/csrc/kern_select.hip", "paper_2601_21758_amd/csrc/ewsjf_device.h")
+# VALU issue peak: 256 CUs x 4 SIMDs, one wave64 VALU instruction per SIMD
+# every 4 cycles (16 lanes wide), at 2.4 GHz.
+VALU_PEAK_G = 256 * 4 * 2.4 / 4
 
 
 def kernel_source_hash() -> str:
@@ -62,22 +75,41 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def read_traffic(n_bytes_alg: int):
-    """HBM bytes per launch of the streaming kernel from the committed
-    rocprofv3 counter summary, or None when it is missing or stale."""
-    if not os.path.exists(PROFILE):
+def read_pmc(path: str):
+    """key = value lines of a committed rocprofv3 counter summary, or None
+    when it is missing or was taken on other kernel sources."""
+    if not os.path.exists(path):
         return None
     kv = {}
-    for line in open(PROFILE):
+    for line in open(path):
         if "=" in line and not line.startswith("#"):
             k, v = line.strip().split("=", 1)
             kv[k.strip()] = v.strip()
     if kv.get("kernel_source_sha256_16") != kernel_source_hash():
         return None
+    return kv
+
+
+def read_traffic():
+    """HBM bytes per launch of the streaming kernel, or None."""
+    kv = read_pmc(PROFILE)
     try:
-        return int(float(kv["hbm_bytes_per_dispatch"]))
+        return int(float(kv["local_candidates.hbm_bytes_per_dispatch"])) if kv else None
     except (KeyError, ValueError):
         return None
+
+
+def host_cpu() -> dict:
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"host_cpus": os.cpu_count(), "cpu_model": model}
 
 
 class Hip:
@@ -89,6 +121,7 @@ class Hip:
         self.rt.hipEventElapsedTime.argtypes = [C.POINTER(C.c_float), C.c_void_p, C.c_void_p]
         self.rt.hipEventSynchronize.argtypes = [C.c_void_p]
         self.rt.hipEventDestroy.argtypes = [C.c_void_p]
+        self.rt.hipEventRecord.argtypes = [C.c_void_p, C.c_void_p]
 
     def event(self):
         e = C.c_void_p()
@@ -135,20 +168,54 @@ def copy_reference(dev, mib: int = 512, reps: int = 20) -> dict:
             "method": f"torch copy_ between device buffers of {mib} MiB, median of {reps - 2}"}
 
 
+def oracle_rate(fn, units: int, budget_s: float, runs: int = 3):
+    """Median over `runs` timed runs of the oracle call `fn` (each run
+    repeats it for budget_s / runs seconds, at least once): units per
+    second, the last result, and the passes made."""
+    import numpy as np
+    rates, res, passes = [], None, 0
+    for _ in range(runs):
+        reps, t0 = 0, time.perf_counter()
+        while True:
+            res = fn()
+            reps += 1
+            el = time.perf_counter() - t0
+            if el >= budget_s / runs or reps >= 1000:
+                break
+        rates.append(reps * units / el)
+        passes += reps
+    return float(np.median(rates)), res, passes
+
+
 def cpu_baseline(pool, table_ref, budget_s: float):
+    """The oracle (single thread) on every pool: configs 0..2 whole, config
+    3 on a sample of its parameter vectors.  The line's value is the 4M
+    pool's rate."""
     import oracle
-    reps, t0 = 0, time.perf_counter()
-    res = None
-    while True:
-        res = oracle.step(pool.length, pool.arrival, pool.now, table_ref, pool.theta, pool.B, pool.cost)
-        reps += 1
-        el = time.perf_counter() - t0
-        if el >= budget_s or reps >= 200:
-            break
-    rate = reps * pool.n / el
-    return {"value": rate, "unit": "requests/s", "cores": 1, "kind": "oracle",
-            "sample": f"{reps} full passes of route+score+select (oracle_step) over the same "
-                      f"{pool.n:,}-request pool, single thread, {el:.1f} s"}, res
+    from paper_2601_21758_amd import workloads as W
+    rate, res, passes = oracle_rate(
+        lambda: oracle.step(pool.length, pool.arrival, pool.now, table_ref, pool.theta, pool.B, pool.cost),
+        pool.n, budget_s)
+    per = {pool.name: {"value": rate, "unit": "requests/s", "passes": passes}}
+    for idx in (0, 1):
+        p = W.config(idx)
+        t = oracle.partition(p.window, init_queues=p.init_queues, max_queues=p.max_queues)
+        r, _, k = oracle_rate(lambda: oracle.step(p.length, p.arrival, p.now, t, p.theta, p.B, p.cost), p.n,
+                              max(1.0, budget_s / 5))
+        per[p.name] = {"value": r, "unit": "requests/s", "passes": k}
+    p = W.config(3)
+    t = oracle.partition(p.window, init_queues=p.init_queues, max_queues=p.max_queues)
+    nv = 16
+    r, _, k = oracle_rate(lambda: oracle.step(p.length, p.arrival, p.now, t, p.theta[:nv], p.B, p.cost),
+                          p.n * nv, max(1.0, budget_s / 5))
+    per[p.name] = {"value": r, "unit": "request-theta pairs/s", "passes": k,
+                   "sample": f"the first {nv} of its 256 parameter vectors"}
+    out = {"value": rate, "unit": "requests/s", "cores": 1, "kind": "oracle",
+           "sample": f"route+score+select (oracle step) over the whole {pool.n:,}-request pool, {passes} passes "
+                     f"in three timed runs of ~{budget_s / 3:.1f} s, median rate; one thread",
+           "per_config": per}
+    out.update(host_cpu())
+    return out, res
 
 
 def batched_theta_bench(hip, steps: int = 20):
@@ -192,14 +259,120 @@ def batched_theta_bench(hip, steps: int = 20):
     ms = hip.elapsed_ms(e0, e1) / steps
     k1 = float(np.mean([hip.elapsed_ms(m[0], m[1]) for m in marks]))
     k2 = float(np.mean([hip.elapsed_ms(m[2], m[3]) for m in marks]))
-    return {"workload": "batched_theta_1m: 1,048,576 requests (3-mode lognormal mix), 64-queue policy, "
-                        "256 parameter vectors drawn in the stated ranges, top B=256 per vector",
-            "ms_per_step": ms, "request_theta_pairs_per_s": n * nt / (ms * 1e-3),
-            "kernels_ms": {"local_candidates": k1, "merge_candidates": k2}, "steps": steps,
+    out = {"workload": "batched_theta_1m: 1,048,576 requests (3-mode lognormal mix), 64-queue policy, "
+                       "256 parameter vectors drawn in the stated ranges, top B=256 per vector",
+           "ms_per_step": ms, "request_theta_pairs_per_s": n * nt / (ms * 1e-3),
+           "kernels_ms": {"local_candidates_multi": k1, "merge_candidates": k2}, "steps": steps,
+           "input_sha256": pool.digest()[:16], "roofline": None}
+    # The many-vector kernel does ~20 VALU operations per (request, vector)
+    # pair on 8 bytes per request: the VALU, not HBM, bounds it.  Its
+    # instruction counts come from the committed counter run (counts do not
+    # depend on timing), the duration from the events above.
+    kv = read_pmc(PROFILE_BATCHED)
+    if kv is not None:
+        valu = float(kv["local_candidates_multi.SQ_INSTS_VALU"])
+        ach = valu / (k1 * 1e-3) / 1e9
+        out["roofline"] = {
+            "bound": "alu", "kernel": "local_candidates_multi (route+score+local top-B, 16 vectors per workgroup)",
+            "achieved": ach, "peak": VALU_PEAK_G, "unit": "G VALU wave64 instructions/s", "frac": ach / VALU_PEAK_G,
+            "valu_insts_per_launch": valu, "kernel_ms": k1,
+            "lds_insts_per_launch": float(kv["local_candidates_multi.SQ_INSTS_LDS"]),
+            "lds_util": float(kv["local_candidates_multi.lds_util"]),
+            "lds_bank_conflict_per_access": float(kv["local_candidates_multi.lds_bank_conflict_per_access"]),
+            "hbm_frac": 8 * n / (k1 * 1e-3) / 1e9 / HBM_PEAK_GBS,
+            "counters": os.path.relpath(PROFILE_BATCHED, ROOT)}
+    return out
+
+
+def config_step_bench(hip, idx: int, steps: int = 200, chunk: int = 50, draws: int = 4):
+    """The fused step on a smaller pool (configs 0 and 1), from HIP graphs
+    over `draws` independent pool draws, with per-kernel events from an
+    eager pass.  These pools (32 KiB and 2 MiB) stay in the caches."""
+    import numpy as np
+    import torch
+
+    from paper_2601_21758_amd import _lib as L
+    from paper_2601_21758_amd import ewsjf as E
+    from paper_2601_21758_amd import workloads as W
+    dev = torch.device("cuda:0")
+    pools = [W.config(idx, draw=d) for d in range(draws)]
+    pool = pools[0]
+    n, B = pool.n, pool.B
+    lens = [torch.from_numpy(p.length).to(dev) for p in pools]
+    arrs = [torch.from_numpy(p.arrival).to(dev) for p in pools]
+    theta = torch.from_numpy(pool.theta).to(dev)
+    table = E.partition(torch.from_numpy(pool.window).to(dev),
+                        E.params(init_queues=pool.init_queues, max_queues=pool.max_queues))
+    ids = torch.empty((1, B), dtype=torch.int32, device=dev)
+    top = torch.empty((1, B), dtype=torch.float32, device=dev)
+    nsel = torch.empty((1,), dtype=torch.int32, device=dev)
+    wsb = E.workspace_bytes(L.OP_STEP, n, 1, B)
+    ws = torch.empty(max(256, wsb), dtype=torch.uint8, device=dev)
+    c = E.cost(*pool.cost)
+    lib = L.lib()
+    vp = C.c_void_p
+
+    def one(i, s, marks=None):
+        r = i % draws
+        a = (vp(lens[r].data_ptr()), vp(arrs[r].data_ptr()), n, float(pools[r].now), vp(table.data_ptr()),
+             vp(theta.data_ptr()), 1, C.byref(c), B, 0, vp(ids.data_ptr()), vp(top.data_ptr()),
+             vp(nsel.data_ptr()), vp(ws.data_ptr()), wsb, s)
+        st = lib.ewsjf_step(*a) if marks is None else lib.ewsjf_step_timed(*a, marks)
+        if st != 0:
+            raise L.EwsjfError(st, "ewsjf_step")
+
+    s0 = vp(torch.cuda.current_stream().cuda_stream)
+    for i in range(10):
+        one(i, s0)
+    torch.cuda.synchronize()
+    marks = [(hip.event(), hip.event(), hip.event(), hip.event()) for _ in range(steps)]
+    torch.cuda._sleep(int(2.4e9 * (0.02 + 3e-5 * steps)))
+    for i in range(steps):
+        one(i, s0, (vp * 4)(*marks[i]))
+    torch.cuda.synchronize()
+    k1 = [hip.elapsed_ms(m[0], m[1]) for m in marks]
+    k2 = [hip.elapsed_ms(m[2], m[3]) for m in marks]
+    for m in marks:
+        for e in m:
+            hip.rt.hipEventDestroy(e)
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        one(0, vp(side.cuda_stream))
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g):
+        cs = vp(torch.cuda.current_stream().cuda_stream)
+        for i in range(chunk):
+            one(i, cs)
+    g.replay()
+    torch.cuda.synchronize()
+    reps = max(4, steps // chunk)
+    gs = vp(torch.cuda.current_stream().cuda_stream)
+    ev = [hip.event() for _ in range(reps + 1)]
+    hip.rt.hipEventRecord(ev[0], gs)
+    for r in range(reps):
+        g.replay()
+        hip.rt.hipEventRecord(ev[r + 1], gs)
+    torch.cuda.synchronize()
+    ms = hip.elapsed_ms(ev[0], ev[reps]) / (reps * chunk)
+    per_rep = [hip.elapsed_ms(ev[r], ev[r + 1]) * 1e3 / chunk for r in range(reps)]
+    for e in ev:
+        hip.rt.hipEventDestroy(e)
+    del g
+    return {"workload": f"{pool.name}: {n:,} pending requests, {pool.init_queues}-queue policy, top B={B}",
+            "ms_per_step": ms, "requests_per_s": n / (ms * 1e-3),
+            "step_hbm_frac": 8 * n / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+            "kernels_ms": {"local_candidates": float(np.mean(k1)), "merge_candidates": float(np.mean(k2))},
+            "step_percentiles_us": {"graph_per_replay": pct(per_rep),
+                                    "local_candidates": pct([x * 1e3 for x in k1]),
+                                    "merge_candidates": pct([x * 1e3 for x in k2])},
+            "pool_draws": draws, "execution": f"HIP graph, {chunk} steps per graph, {reps} replays",
             "input_sha256": pool.digest()[:16]}
 
 
-def tactical_bench(hip, pool, table, lens, arrs, steps: int = 50):
+def tactical_bench(hip, pool, table, lens, arrs, nows, steps: int = 50):
     """Algorithm 1 (ewsjf_tactical_step) on the 4M pool: head-of-line pass,
     plan, queue-order selection of B requests, batch assembly.  No removals
     (threshold above the step count) and no tombstones, so every step sees
@@ -227,7 +400,7 @@ def tactical_bench(hip, pool, table, lens, arrs, steps: int = 50):
 
     def one(i):
         r = i % len(lens)
-        st = lib.ewsjf_tactical_step(vp(lens[r].data_ptr()), vp(arrs[r].data_ptr()), n, float(pool.now),
+        st = lib.ewsjf_tactical_step(vp(lens[r].data_ptr()), vp(arrs[r].data_ptr()), n, nows[r],
                                      vp(table.data_ptr()), vp(theta.data_ptr()), C.byref(c), B, 1 << 30,
                                      vp(ec.data_ptr()), 1e-6, 0, vp(ids.data_ptr()), nsel_p, qp_p,
                                      vp(hs.data_ptr()), vp(rm.data_ptr()), vp(ws.data_ptr()), wsb, s)
@@ -442,6 +615,9 @@ def streaming_bench(steps: int, handover: str = "next_step"):
             "slowest_steps": [[int(i), float(lat[i])] for i in np.argsort(lat)[::-1][:8]]}
 
 
+EXTRAS = ("small_configs", "tactical", "batched_theta", "streaming", "window_and_dispatch", "trial")
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -450,11 +626,17 @@ def main() -> int:
     ap.add_argument("--rotate", type=int, default=10)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
-    ap.add_argument("--no-extra", action="store_true", help="skip the batched-theta and streaming workloads")
+    ap.add_argument("--extra", default="all",
+                    help="comma list of the workloads beside the 4M step: " + ",".join(EXTRAS) + " (default all)")
+    ap.add_argument("--no-extra", action="store_true", help="only the 4M step")
     ap.add_argument("--stream-steps", type=int, default=10000)
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="run one device copy of this many MiB first (counter calibration under rocprofv3)")
     args = ap.parse_args()
+    extras = () if args.no_extra else EXTRAS if args.extra == "all" else tuple(x for x in args.extra.split(",") if x)
+    for x in extras:
+        if x not in EXTRAS:
+            ap.error(f"unknown workload {x!r}")
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py: the scheduler core runs on one GPU; runs on several GPUs are not supported "
@@ -486,8 +668,21 @@ def main() -> int:
 
     pool = W.config(2)
     n, B = pool.n, pool.B
-    lens = [torch.from_numpy(pool.length).to(dev) for _ in range(args.rotate)]
-    arrs = [torch.from_numpy(pool.arrival).to(dev) for _ in range(args.rotate)]
+    # independent draws of the pool (draw 0 is the workload itself), each
+    # scored at its own clock (its latest arrival)
+    lens, arrs, nows = [], [], []
+    for r in range(args.rotate):
+        pr = pool if r == 0 else W.config(2, draw=r)
+        lens.append(torch.from_numpy(pr.length).to(dev))
+        arrs.append(torch.from_numpy(pr.arrival).to(dev))
+        nows.append(float(pr.now))
+        del pr
+    if args.copy_probe_mib > 0:
+        # plain reads of every rotated pool copy (torch's sum kernel, 16 MiB
+        # each): a second calibration, by a read-only kernel, of the counters
+        for t in lens + arrs:
+            t.sum()
+        torch.cuda.synchronize()
     theta = torch.from_numpy(pool.theta).to(dev)
     window = torch.from_numpy(pool.window).to(dev)
     prm = E.params(init_queues=pool.init_queues, max_queues=pool.max_queues)
@@ -499,7 +694,6 @@ def main() -> int:
     stream = torch.cuda.current_stream()
     e0, e1 = hip.event(), hip.event()
     rt = hip.rt
-    rt.hipEventRecord.argtypes = [C.c_void_p, C.c_void_p]
     rt.hipEventRecord(e0, C.c_void_p(stream.cuda_stream))
     for _ in range(10):
         E.partition(window, prm, table=table, ws=pws)
@@ -530,16 +724,15 @@ def main() -> int:
                       top=vp(top.data_ptr()), nsel=vp(nsel.data_ptr()), ws=vp(ws.data_ptr()))
     lp = [vp(t.data_ptr()) for t in lens]
     ap_ = [vp(t.data_ptr()) for t in arrs]
-    now = float(pool.now)
 
     def step(i, s, marks=None):
         r = i % args.rotate
         if marks is None:
-            st = lib.ewsjf_step(lp[r], ap_[r], n, now, args_fixed["table"], args_fixed["theta"], 1, C.byref(cost), B,
+            st = lib.ewsjf_step(lp[r], ap_[r], n, nows[r], args_fixed["table"], args_fixed["theta"], 1, C.byref(cost), B,
                                 0, args_fixed["ids"], args_fixed["top"], args_fixed["nsel"], args_fixed["ws"],
                                 ws_bytes, s)
         else:
-            st = lib.ewsjf_step_timed(lp[r], ap_[r], n, now, args_fixed["table"], args_fixed["theta"], 1,
+            st = lib.ewsjf_step_timed(lp[r], ap_[r], n, nows[r], args_fixed["table"], args_fixed["theta"], 1,
                                       C.byref(cost), B, 0, args_fixed["ids"], args_fixed["top"], args_fixed["nsel"],
                                       args_fixed["ws"], ws_bytes, s, marks)
         if st != 0:
@@ -573,20 +766,32 @@ def main() -> int:
             rt.hipEventDestroy(e)
 
     # ---- graph pass: the timed steps ------------------------------------------
-    chunk = max(c for c in range(1, min(K, 50) + 1) if K % c == 0)
-    g = torch.cuda.CUDAGraph()
+    # Chunks of up to 50 steps with at least four replays.  Step i reads pool
+    # copy i % rotate; when the chunk does not cover whole rotations, one graph
+    # per starting copy keeps the order, so the replays walk all the copies.
+    cands = [c for c in range(1, min(K, 50) + 1) if K % c == 0 and K // c >= 4]
+    chunk = max(cands) if cands else K
+    gstep = math.gcd(chunk, args.rotate)
+    graphs = []
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(side):
         step(0, vp(side.cuda_stream))
     torch.cuda.current_stream().wait_stream(side)
     torch.cuda.synchronize()
-    with torch.cuda.graph(g):
-        cs = vp(torch.cuda.current_stream().cuda_stream)
-        for i in range(chunk):
-            step(i, cs)
-    for _ in range((args.warmup + chunk - 1) // chunk):
-        g.replay()
+    for off in range(0, args.rotate, gstep):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            cs = vp(torch.cuda.current_stream().cuda_stream)
+            for i in range(chunk):
+                step(off + i, cs)
+        graphs.append(g)
+
+    def replay(r):
+        graphs[((r * chunk) % args.rotate) // gstep].replay()
+
+    for r in range(max(len(graphs), (args.warmup + chunk - 1) // chunk)):
+        replay(r)
     torch.cuda.synchronize()
     gs = vp(torch.cuda.current_stream().cuda_stream)
     # One event per replay boundary: the whole interval gives the mean, the
@@ -595,20 +800,25 @@ def main() -> int:
     bounds_ev = [hip.event() for _ in range(reps + 1)]
     rt.hipEventRecord(bounds_ev[0], gs)
     for r in range(reps):
-        g.replay()
+        replay(r)
         rt.hipEventRecord(bounds_ev[r + 1], gs)
     torch.cuda.synchronize()
     graph_ms = hip.elapsed_ms(bounds_ev[0], bounds_ev[reps]) / K
     replay_step_us = [hip.elapsed_ms(bounds_ev[r], bounds_ev[r + 1]) * 1e3 / chunk for r in range(reps)]
     for e in bounds_ev:
         rt.hipEventDestroy(e)
+    # the last graph step and the last eager step both read copy (K-1) % rotate
     graph_ok = bool(torch.equal(ids, eager_ids))
+    del graphs
+    # draw 0 once more, for the comparison with the oracle
+    step(0, s_eager)
+    torch.cuda.synchronize()
 
     ms_per_step = graph_ms
     value = n / (ms_per_step * 1e-3)
     alg_bytes = BYTES_PER_REQUEST * n + 8 * B
     achieved = alg_bytes / (k1_ms * 1e-3) / 1e9
-    traffic = read_traffic(alg_bytes)
+    traffic = read_traffic()
 
     out = {
         "metric": METRIC, "value": value, "unit": "requests/s", "n_gpus": 1, "steps": K,
@@ -617,8 +827,9 @@ def main() -> int:
         "config": {"workload": "large_mixed_4m: 4,194,304 pending requests, 80/20 lognormal prompt-length mix, "
                                "Poisson arrivals at 10k/s, 256-queue Refine-and-Prune policy from a "
                                "1,048,576-length window, midpoint scoring parameters, top B=1024",
-                   "pool": n, "B": B, "queues": k_queues, "rotated_pool_copies": args.rotate,
-                   "execution": f"HIP graph, {chunk} steps per graph", "input_sha256": pool.digest()[:16]},
+                   "pool": n, "B": B, "queues": k_queues, "rotated_pool_draws": args.rotate,
+                   "execution": f"HIP graph, {chunk} steps per graph, {reps} replays",
+                   "input_sha256": pool.digest()[:16]},
         "roofline": {"bound": "hbm", "kernel": "local_candidates (route+score+local top-B)",
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": traffic, "bytes_per_launch": alg_bytes, "kernel_ms": k1_ms,
@@ -636,12 +847,18 @@ def main() -> int:
         "partition_ms": partition_ms,
         "partition_from_histogram_ms": partition_hist_ms,
     }
-    if not args.no_extra:
-        out["tactical"] = tactical_bench(hip, pool, table, lens, arrs)
+    if "small_configs" in extras:
+        out["small_configs"] = {"tiny_mixed_4k": config_step_bench(hip, 0), "mid_3mode_256k": config_step_bench(hip, 1)}
+    if "tactical" in extras:
+        out["tactical"] = tactical_bench(hip, pool, table, lens, arrs, nows)
+    if "batched_theta" in extras:
         out["batched_theta"] = batched_theta_bench(hip)
+    if "streaming" in extras:
         out["streaming"] = streaming_bench(args.stream_steps)
         out["streaming_nonblocking"] = streaming_bench(args.stream_steps // 2, "when_ready")
+    if "window_and_dispatch" in extras:
         out["window_and_dispatch"] = window_and_dispatch_bench(hip)
+    if "trial" in extras:
         out["trial"] = trial_bench(hip)
     if not args.no_cpu:
         import oracle

@@ -3,9 +3,10 @@
 libewsjf_stamps.so (python -m paper_2601_21758_amd.build --stamps) records,
 in thread 0 of each streaming workgroup and each merge workgroup, the
 device's 100 MHz constant clock at numbered points of the kernel.  This
-script runs the step on the large mixed pool (4,194,304 requests, the
-256-queue partition of its 1,048,576-length window, B = 1,024, rotated pool
-copies), in bursts of back-to-back steps (the stamps are the last step's),
+script runs the step on one of the pools (`--config`: 0 the 4,096-request
+pool, 1 the 262,144-request pool, 2 (default) the large mixed pool of
+4,194,304 requests with the 256-queue partition of its 1,048,576-length
+window and B = 1,024), rotating over independent draws of it, in bursts of back-to-back steps (the stamps are the last step's),
 and prints, per kernel and point, the median over steps of the median and
 the maximum over workgroups, in microseconds after the kernel's first
 workgroup started ("median_us", "max_us") and after the workgroup's own
@@ -43,6 +44,7 @@ TICK_US = 0.01  # 100 MHz
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--config", type=int, default=2, choices=(0, 1, 2))
     ap.add_argument("--rotate", type=int, default=10)
     ap.add_argument("--lib", default=os.path.join(PKG, "libewsjf_stamps.so"),
                     help="an instrumented build of the library (default: the package's)")
@@ -64,16 +66,19 @@ def main() -> int:
     lib.ewsjf_debug_stamps_clear.argtypes = []
     torch.cuda.set_device(0)
     dev = torch.device("cuda:0")
-    pool = W.config(2)
-    lens = [torch.from_numpy(pool.length).to(dev) for _ in range(args.rotate)]
-    arrs = [torch.from_numpy(pool.arrival).to(dev) for _ in range(args.rotate)]
+    pools = [W.config(args.config, draw=r) for r in range(args.rotate)]
+    pool = pools[0]
+    lens = [torch.from_numpy(p.length).to(dev) for p in pools]
+    arrs = [torch.from_numpy(p.arrival).to(dev) for p in pools]
+    nows = [float(p.now) for p in pools]
     theta = torch.from_numpy(pool.theta).to(dev)
     table = E.partition(torch.from_numpy(pool.window).to(dev),
                         E.params(init_queues=pool.init_queues, max_queues=pool.max_queues))
     ws = E.Workspace(dev)
     out = E._outs(1, pool.B, dev, None)
     for i in range(5):
-        E.step(lens[i % args.rotate], arrs[i % args.rotate], pool.now, table, theta, pool.B, pool.cost, out=out, ws=ws)
+        r = i % args.rotate
+        E.step(lens[r], arrs[r], nows[r], table, theta, pool.B, pool.cost, out=out, ws=ws)
     torch.cuda.synchronize()
     host = np.zeros(len(KERNELS) * BLOCKS * PHASES, np.uint64)
     per = {k: [] for k in KERNELS}
@@ -83,7 +88,7 @@ def main() -> int:
         torch.cuda._sleep(int(2.4e9 * 1e-3))  # hold the stream while the burst is enqueued
         for j in range(args.burst):
             r = (i * args.burst + j) % args.rotate
-            E.step(lens[r], arrs[r], pool.now, table, theta, pool.B, pool.cost, out=out, ws=ws)
+            E.step(lens[r], arrs[r], nows[r], table, theta, pool.B, pool.cost, out=out, ws=ws)
         torch.cuda.synchronize()
         assert lib.ewsjf_debug_stamps(host.ctypes.data, host.size) == 0
         st = host.reshape(len(KERNELS), BLOCKS, PHASES).astype(np.int64)
@@ -131,7 +136,7 @@ def main() -> int:
             rep["list_length"] = {"p10": float(np.percentile(ll, 10)), "p50": float(np.median(ll)),
                                   "p90": float(np.percentile(ll, 90)), "max": float(ll.max())}
         report[k] = rep
-    print(json.dumps({"workload": "large_mixed_4m step, B=1024", "steps": args.steps, "phases": report}, indent=1),
+    print(json.dumps({"workload": f"{pool.name} step, B={pool.B}, {args.rotate} pool draws", "steps": args.steps, "phases": report}, indent=1),
           flush=True)
     return 0
 

@@ -122,24 +122,27 @@ def make_pool(mix: str, n: int, seed: int, *, arrivals: str, horizon: float = 60
                 init_queues=K, max_queues=K, B=B, theta=theta)
 
 
-def config(idx: int, scale: float = 1.0) -> Pool:
+def config(idx: int, scale: float = 1.0, draw: int = 0) -> Pool:
     """The five evaluation workloads (0..3 here; 4 is `Streaming`).
 
     `scale` < 1 shrinks pool and window (keeping K and B) for quick tests.
+    `draw` > 0 gives another independent pool of the same recipe (seed
+    shifted by 7919 * draw); draw 0 is the workload itself.
     """
     def sz(x):
         return max(1, int(round(x * scale)))
+    sd = 7919 * draw
     if idx == 0:
-        return make_pool("two", sz(4096), 0, arrivals="uniform", horizon=60.0, window=None,
+        return make_pool("two", sz(4096), 0 + sd, arrivals="uniform", horizon=60.0, window=None,
                          K=16, B=64, name="tiny_mixed_4k")
     if idx == 1:
-        return make_pool("three", sz(262144), 1, arrivals="uniform", horizon=300.0,
+        return make_pool("three", sz(262144), 1 + sd, arrivals="uniform", horizon=300.0,
                          window=sz(65536), K=64, B=256, name="mid_3mode_256k")
     if idx == 2:
-        return make_pool("two", sz(4194304), 2, arrivals="poisson", rate=1e4,
+        return make_pool("two", sz(4194304), 2 + sd, arrivals="poisson", rate=1e4,
                          window=sz(1048576), K=256, B=1024, name="large_mixed_4m")
     if idx == 3:
-        return make_pool("three", sz(1048576), 3, arrivals="uniform", horizon=300.0,
+        return make_pool("three", sz(1048576), 3 + sd, arrivals="uniform", horizon=300.0,
                          window=sz(65536), K=64, B=256, n_theta=256,
                          name="batched_theta_1m")
     raise ValueError(idx)
