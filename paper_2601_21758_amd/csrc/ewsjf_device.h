@@ -248,10 +248,16 @@ __device__ __forceinline__ uint32_t xor_lane_u32(uint32_t x) {
     return (uint32_t)__builtin_amdgcn_update_dpp(0, y, 0x1B, 0xF, 0xF, false);  // quad_perm [3,2,1,0]
   } else if constexpr (J == 8) {
     return (uint32_t)__builtin_amdgcn_update_dpp(0, v, 0x128, 0xF, 0xF, false);  // row_ror:8
-  } else if constexpr (J == 16) {
-    return (uint32_t)__builtin_amdgcn_ds_swizzle(v, 0x401F);  // and 0x1F, xor 0x10
   } else {
-    return (uint32_t)__shfl_xor(v, 32);
+    // Rows of 16 lanes (J = 16) or halves of the wave (J = 32) trade places
+    // in registers: swapping x with a copy of itself leaves the partner's
+    // value in the first result on the lanes with bit J set, in the second
+    // on the others.
+    static_assert(J == 16 || J == 32, "xor distances 1 to 32");
+    const int lane = (int)(threadIdx.x & 63u);
+    const auto r = J == 16 ? __builtin_amdgcn_permlane16_swap(x, x, true, false)
+                           : __builtin_amdgcn_permlane32_swap(x, x, true, false);
+    return (lane & J) ? r[0] : r[1];
   }
 }
 

@@ -1601,7 +1601,11 @@ __global__ __launch_bounds__(kBlock) void merge_rank(Src src, int64_t n, int G, 
     }
     if (lane < kRankHalf && mine != 0) atomicAdd(&s_rank[h + lane], mine);
   };
-  count_half(0, 0ull);
+  // When the merge is safe (below), an entry under T has at least B entries
+  // above it, so own slots under T are not ranked (and not written); when it
+  // is not, no count is used.
+  const uint64_t below_T = T != 0ull ? T - 1ull : 0ull;
+  count_half(0, below_T);
   __syncthreads();
   EWSJF_STAMP(kStampMergeRank, 2);
   const bool safe = T <= 1ull || s_ge >= B;
@@ -1610,12 +1614,12 @@ __global__ __launch_bounds__(kBlock) void merge_rank(Src src, int64_t n, int G, 
     if (blockIdx.x == 0) merge_exact(src, 0, n, G, M, B, cb, ids, top, n_sel, tomb_len, lds);
     return;
   }
-  // The largest own slot of the first half known to rank >= B: slots at or
-  // below it rank >= B too.
-  uint64_t out_bar = 0;
+  // The largest own slot of the first half known to rank >= B (at least
+  // T - 1): slots at or below it rank >= B too.
+  uint64_t out_bar = below_T;
 #pragma unroll
   for (int p = 0; p < kRankHalf; ++p)
-    if (c[p] != 0ull && s_rank[p] >= B && c[p] > out_bar) out_bar = c[p];
+    if (c[p] > below_T && s_rank[p] >= B && c[p] > out_bar) out_bar = c[p];
   bool second = false;
 #pragma unroll
   for (int p = kRankHalf; p < kRankPer; ++p) second = second || c[p] > out_bar;
