@@ -1517,16 +1517,18 @@ __global__ __launch_bounds__(kBlock) void merge_candidates(Src src0, int64_t n, 
 // its elements) or at least B entries are >= T.  Workgroup w ranks the
 // kRankPer slots [w kRankPer, (w + 1) kRankPer) against all G x M slots,
 // counting with wave ballots, and writes the entries of rank < B to their
-// positions; no workgroup waits for another.  It ranks the first half of its
-// slots, then only those of the second half that lie above every slot
-// already found to rank >= B (a smaller entry ranks lower still): a list is
-// sorted, and few lists hold more than half of their entries in the top-B.
+// positions; no workgroup waits for another.  Only own slots at or above T
+// are ranked (below T an entry has at least B entries above it), all in one
+// pass (kRankOnePass).  The alternative two-half order ranks the second half
+// only above every first-half slot already known to rank >= B (a list is
+// sorted); it costs a second barrier for the few slots it would skip.
 // Otherwise (a share could be missing members of the top-B) workgroup 0 runs
 // the exact merge with its recovery and the others leave.  Every workgroup
 // reaches the same decision from the same slots and bounds.
 // ---------------------------------------------------------------------------
 constexpr int kRankPer = 16;
 constexpr int kRankHalf = kRankPer / 2;
+constexpr bool kRankOnePass = true;  // all own slots at once, or in two halves
 constexpr int kRankR = (kMergeCap + kBlock - 1) / kBlock;  // most slots per thread
 
 // NR: slots per thread, a compile-time bound >= ceil(G M / kBlock).
@@ -1605,7 +1607,23 @@ __global__ __launch_bounds__(kBlock) void merge_rank(Src src, int64_t n, int G, 
   // above it, so own slots under T are not ranked (and not written); when it
   // is not, no count is used.
   const uint64_t below_T = T != 0ull ? T - 1ull : 0ull;
-  count_half(0, below_T);
+  if constexpr (kRankOnePass) {
+    // Every own slot at or above T in one pass: lane p adds the count of slot
+    // p (few own slots reach T, so one pass beats a second barrier).
+    int mine = 0;
+#pragma unroll
+    for (int p = 0; p < kRankPer; ++p) {
+      if (c[p] > below_T) {  // uniform
+        int cnt = 0;
+#pragma unroll
+        for (int r = 0; r < NR; ++r) cnt += __popcll(__ballot(v[r] > c[p]));
+        mine = lane == p ? cnt : mine;
+      }
+    }
+    if (lane < kRankPer && mine != 0) atomicAdd(&s_rank[lane], mine);
+  } else {
+    count_half(0, below_T);
+  }
   __syncthreads();
   EWSJF_STAMP(kStampMergeRank, 2);
   const bool safe = T <= 1ull || s_ge >= B;
@@ -1617,15 +1635,17 @@ __global__ __launch_bounds__(kBlock) void merge_rank(Src src, int64_t n, int G, 
   // The largest own slot of the first half known to rank >= B (at least
   // T - 1): slots at or below it rank >= B too.
   uint64_t out_bar = below_T;
+  if constexpr (!kRankOnePass) {
 #pragma unroll
-  for (int p = 0; p < kRankHalf; ++p)
-    if (c[p] > below_T && s_rank[p] >= B && c[p] > out_bar) out_bar = c[p];
-  bool second = false;
+    for (int p = 0; p < kRankHalf; ++p)
+      if (c[p] > below_T && s_rank[p] >= B && c[p] > out_bar) out_bar = c[p];
+    bool second = false;
 #pragma unroll
-  for (int p = kRankHalf; p < kRankPer; ++p) second = second || c[p] > out_bar;
-  if (second) {  // uniform
-    count_half(kRankHalf, out_bar);
-    __syncthreads();
+    for (int p = kRankHalf; p < kRankPer; ++p) second = second || c[p] > out_bar;
+    if (second) {  // uniform
+      count_half(kRankHalf, out_bar);
+      __syncthreads();
+    }
   }
   EWSJF_STAMP(kStampMergeRank, 3);
   const int nnz = s_nz;
