@@ -39,11 +39,22 @@ static __device__ uint64_t g_stamps[kStampSlots];
       ::ewsjf::g_stamps[((kid) * ::ewsjf::kStampBlocks + blockIdx.x) * ::ewsjf::kStampPhases + (phase)] =  \
           (uint64_t)(value);                                                                               \
   } while (0)
+// The time once `dep` (a 32-bit value of the wave) has been computed: the
+// value is handed to an empty asm statement before the clock is read.
+#define EWSJF_STAMP_AFTER(kid, phase, dep)                                                                 \
+  do {                                                                                                     \
+    const int ewsjf_dep_ = __builtin_amdgcn_readfirstlane((int)(dep));                                     \
+    asm volatile("" ::"s"(ewsjf_dep_));                                                                    \
+    EWSJF_STAMP(kid, phase);                                                                               \
+  } while (0)
 #else
 #define EWSJF_STAMP(kid, phase) \
   do {                          \
   } while (0)
 #define EWSJF_STAMP_VALUE(kid, phase, value) \
   do {                                       \
+  } while (0)
+#define EWSJF_STAMP_AFTER(kid, phase, dep) \
+  do {                                     \
   } while (0)
 #endif

@@ -601,6 +601,7 @@ __device__ __forceinline__ void publish_list_wave(const ListShared& ls, int cnt,
   uint64_t* over_list = cb.over + slot * (size_t)kOverCap;
   const int listed = min(cnt, M + kOverCap);
   const uint64_t x = wave_sort_desc(lane < cnt ? ls.list2[lane] : 0ull);  // rank = lane
+  EWSJF_STAMP_AFTER(kStampLocal, 7, (uint32_t)x);
   if (lane < M) out_list[lane] = x;
   else if (lane < listed) over_list[lane - M] = x;
   if (lane == M - 1) {
@@ -1538,11 +1539,14 @@ __global__ __launch_bounds__(kBlock) void merge_rank(Src src, int64_t n, int G, 
                                                      int32_t* __restrict__ n_sel, int32_t* tomb_len) {
   __shared__ MergeLds<Src> lds;
   __shared__ uint64_t s_c[kRankPer];
-  __shared__ uint64_t s_T;
-  __shared__ int s_nz, s_ge;
+  // per-wave partials, each reduced by every wave itself (no LDS atomics and
+  // no barrier to clear them first): largest bound, nonzero slots, slots >= T
+  __shared__ uint64_t s_wT[kWavesPerBlock];
+  __shared__ int s_wnz[kWavesPerBlock], s_wge[kWavesPerBlock];
   __shared__ int s_rank[kRankPer];
   EWSJF_STAMP(kStampMergeRank, 0);
-  const int tid = threadIdx.x, lane = tid & (kWave - 1);
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = tid / kWave;
+  const bool pl = lane < kWavesPerBlock;  // lane i reads wave i's partial
   const int GM = G * M;
   const int p0 = (int)blockIdx.x * kRankPer;
 
@@ -1561,27 +1565,21 @@ __global__ __launch_bounds__(kBlock) void merge_rank(Src src, int64_t n, int G, 
     s_c[tid] = own;
     s_rank[tid] = 0;
   }
-  if (tid == 0) {
-    s_T = 0ull;
-    s_nz = 0;
-    s_ge = 0;
-  }
-  __syncthreads();
   int nz = 0;
 #pragma unroll
   for (int r = 0; r < NR; ++r) nz += __popcll(__ballot(v[r] != 0ull));
   const uint64_t wmax = wave_max_u64(bnd);
   if (lane == 0) {
-    atomicMax(reinterpret_cast<unsigned long long*>(&s_T), (unsigned long long)wmax);
-    atomicAdd(&s_nz, nz);
+    s_wT[wv] = wmax;
+    s_wnz[wv] = nz;
   }
   __syncthreads();
   EWSJF_STAMP(kStampMergeRank, 1);
-  const uint64_t T = s_T;
+  const uint64_t T = wave_max_u64(pl ? s_wT[lane] : 0ull);
   int ge = 0;
 #pragma unroll
   for (int r = 0; r < NR; ++r) ge += __popcll(__ballot(v[r] >= T));
-  if (lane == 0) atomicAdd(&s_ge, ge);
+  if (lane == 0) s_wge[wv] = ge;
   // This wave's count of slots larger than own slot p (wave-uniform: ballots
   // counted on the scalar unit, beside the compares on the vector unit),
   // summed over the waves in LDS.
@@ -1626,7 +1624,8 @@ __global__ __launch_bounds__(kBlock) void merge_rank(Src src, int64_t n, int G, 
   }
   __syncthreads();
   EWSJF_STAMP(kStampMergeRank, 2);
-  const bool safe = T <= 1ull || s_ge >= B;
+  const int n_ge = (int)__ockl_wfred_add_u32(pl ? (uint32_t)s_wge[lane] : 0u);
+  const bool safe = T <= 1ull || n_ge >= B;
   if (!safe) {
     EWSJF_STAMP(kStampMergeRank, 7);
     if (blockIdx.x == 0) merge_exact(src, 0, n, G, M, B, cb, ids, top, n_sel, tomb_len, lds);
@@ -1648,7 +1647,7 @@ __global__ __launch_bounds__(kBlock) void merge_rank(Src src, int64_t n, int G, 
     }
   }
   EWSJF_STAMP(kStampMergeRank, 3);
-  const int nnz = s_nz;
+  const int nnz = (int)__ockl_wfred_add_u32(pl ? (uint32_t)s_wnz[lane] : 0u);
   const int sel = nnz < B ? nnz : B;
   if (tid < kRankPer) {
     const uint64_t x = s_c[tid];
