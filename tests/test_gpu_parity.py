@@ -295,6 +295,26 @@ def test_step_clustered_on_a_full_grid(E, kind):
     check_admission(host(ids)[0], host(top)[0], host(nsel)[0], rids[0], rtop[0], rnsel[0], rs[0])
 
 
+@pytest.mark.parametrize("kind", ["lognormal", "oldest_first", "hot_blocks"])
+def test_step_several_passes(E, kind):
+    # 9,437,189 requests: with 256 workgroups a share holds three passes of
+    # 64 chunks (the last one ragged), so lists are trimmed between passes
+    # and the workgroup bound is the largest bar of all passes
+    n = 9 * (1 << 20) + 5
+    if kind == "lognormal":
+        p = W.make_pool("two", n, 21, arrivals="poisson", rate=1e4, window=1 << 20, K=256, B=1024)
+        L, A, now, B = p.length, p.arrival, p.now, p.B
+        t = oracle_table(p)
+    else:
+        L, A, now = W.adversarial(kind, n, 23)
+        B = 1024
+        t = oracle.partition(np.clip(L[-(1 << 20):], 1, None), init_queues=64, max_queues=64)
+    say(f"step several passes {kind} n={n}")
+    ids, top, nsel = E.step(dev(L), dev(A), now, upload(E, t), dev(W.THETA_MID), B)
+    rids, rtop, rnsel, rs = oracle.step(L, A, now, t, W.THETA_MID, B)
+    check_admission(host(ids)[0], host(top)[0], host(nsel)[0], rids[0], rtop[0], rnsel[0], rs[0])
+
+
 def test_step_small_and_empty_pools(E):
     t = oracle.partition([5, 50, 500], init_queues=2, max_queues=2)
     for n in (0, 1, 3, 4, 5, 63, 255, 257):
