@@ -602,11 +602,10 @@ __host__ __device__ inline int pow2_ceil(int x) {
 
 // ---------------------------------------------------------------------------
 // Scoring (Eq. 1 / Eq. 4) in binary32 for one request of prompt length b >= 1:
-//   Phi = (q+1)/(b+1) * (w_base + w_urg * W/C(b) + w_fair * ln(b+1))
-// evaluated as (q+1) * (w_base*C + w_urg*W + w_fair*ln(b+1)*C) / ((b+1)*C),
-// which needs one reciprocal and one log2.  With the parameter ranges of the
-// evaluation every term is positive, so the binary32 result is within a few
-// ulps of the exact value.
+//   Phi = (q+1)/(b+1) * (w_base + w_urg * W/C(b) + w_fair * ln(b+1)),
+// computed from one reciprocal of (b+1) C(b) and one log2 (below).  With the
+// parameter ranges of the evaluation every term is positive, so the binary32
+// result is within a few ulps of the exact value.
 // ---------------------------------------------------------------------------
 struct CostF {
   float c0, c1, c2;

@@ -1520,16 +1520,12 @@ __global__ __launch_bounds__(kBlock) void merge_candidates(Src src0, int64_t n, 
 // counting with wave ballots, and writes the entries of rank < B to their
 // positions; no workgroup waits for another.  Only own slots at or above T
 // are ranked (below T an entry has at least B entries above it), all in one
-// pass (kRankOnePass).  The alternative two-half order ranks the second half
-// only above every first-half slot already known to rank >= B (a list is
-// sorted); it costs a second barrier for the few slots it would skip.
-// Otherwise (a share could be missing members of the top-B) workgroup 0 runs
-// the exact merge with its recovery and the others leave.  Every workgroup
-// reaches the same decision from the same slots and bounds.
+// pass; the lists need no order.  Otherwise (a share could be missing
+// members of the top-B) workgroup 0 runs the exact merge with its recovery
+// and the others leave.  Every workgroup reaches the same decision from the
+// same slots and bounds.
 // ---------------------------------------------------------------------------
 constexpr int kRankPer = 16;
-constexpr int kRankHalf = kRankPer / 2;
-constexpr bool kRankOnePass = true;  // all own slots at once, or in two halves
 constexpr int kRankR = (kMergeCap + kBlock - 1) / kBlock;  // most slots per thread
 
 // NR: slots per thread, a compile-time bound >= ceil(G M / kBlock).
@@ -1583,31 +1579,16 @@ __global__ __launch_bounds__(kBlock) void merge_rank(Src src, int64_t n, int G, 
   // This wave's count of slots larger than own slot p (wave-uniform: ballots
   // counted on the scalar unit, beside the compares on the vector unit),
   // summed over the waves in LDS.
-  // The counts of one half of the own slots go to LDS in one add per wave
-  // (lane p adds the count of slot h + p).
   uint64_t c[kRankPer];
 #pragma unroll
   for (int p = 0; p < kRankPer; ++p) c[p] = s_c[p];
-  auto count_half = [&](int h, uint64_t above) {
-    int mine = 0;
-#pragma unroll
-    for (int p = 0; p < kRankHalf; ++p) {
-      if (c[h + p] > above) {  // uniform
-        int cnt = 0;
-#pragma unroll
-        for (int r = 0; r < NR; ++r) cnt += __popcll(__ballot(v[r] > c[h + p]));
-        mine = lane == p ? cnt : mine;
-      }
-    }
-    if (lane < kRankHalf && mine != 0) atomicAdd(&s_rank[h + lane], mine);
-  };
   // When the merge is safe (below), an entry under T has at least B entries
   // above it, so own slots under T are not ranked (and not written); when it
   // is not, no count is used.
   const uint64_t below_T = T != 0ull ? T - 1ull : 0ull;
-  if constexpr (kRankOnePass) {
+  {
     // Every own slot at or above T in one pass: lane p adds the count of slot
-    // p (few own slots reach T, so one pass beats a second barrier).
+    // p (few own slots reach T).
     int mine = 0;
 #pragma unroll
     for (int p = 0; p < kRankPer; ++p) {
@@ -1619,8 +1600,6 @@ __global__ __launch_bounds__(kBlock) void merge_rank(Src src, int64_t n, int G, 
       }
     }
     if (lane < kRankPer && mine != 0) atomicAdd(&s_rank[lane], mine);
-  } else {
-    count_half(0, below_T);
   }
   __syncthreads();
   EWSJF_STAMP(kStampMergeRank, 2);
@@ -1631,21 +1610,8 @@ __global__ __launch_bounds__(kBlock) void merge_rank(Src src, int64_t n, int G, 
     if (blockIdx.x == 0) merge_exact(src, 0, n, G, M, B, cb, ids, top, n_sel, tomb_len, lds);
     return;
   }
-  // The largest own slot of the first half known to rank >= B (at least
-  // T - 1): slots at or below it rank >= B too.
-  uint64_t out_bar = below_T;
-  if constexpr (!kRankOnePass) {
-#pragma unroll
-    for (int p = 0; p < kRankHalf; ++p)
-      if (c[p] > below_T && s_rank[p] >= B && c[p] > out_bar) out_bar = c[p];
-    bool second = false;
-#pragma unroll
-    for (int p = kRankHalf; p < kRankPer; ++p) second = second || c[p] > out_bar;
-    if (second) {  // uniform
-      count_half(kRankHalf, out_bar);
-      __syncthreads();
-    }
-  }
+  // own slots at or below T - 1 rank >= B
+  const uint64_t out_bar = below_T;
   EWSJF_STAMP(kStampMergeRank, 3);
   const int nnz = (int)__ockl_wfred_add_u32(pl ? (uint32_t)s_wnz[lane] : 0u);
   const int sel = nnz < B ? nnz : B;

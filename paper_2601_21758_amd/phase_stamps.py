@@ -20,9 +20,9 @@ Points:
                     length of the filtered list (entries at or above the
                     workgroup's bound), reported as "list_length"; 7 the
                     list sorted by one wave (lists of 17 to 64 entries)
-  merge_rank        0 start, 1 slots and bounds in (first barrier), 2 first
-                    half of the own slots counted, 3 second half counted, 4
-                    outputs written, 7 took the exact merge
+  merge_rank        0 start, 1 slots and bounds in (first barrier), 2 own
+                    slots counted, 3 merge found safe, 4 outputs written, 7
+                    took the exact merge
   merge_exact       0 start, 1 cut and order done, 2 published
 """
 from __future__ import annotations
