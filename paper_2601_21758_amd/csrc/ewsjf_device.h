@@ -336,31 +336,6 @@ __device__ __forceinline__ uint64_t xor_lane_u64_dyn(uint64_t x, int j) {
   }
 }
 
-// Descending bitonic sort of one value per lane across the wave: lane i
-// returns the value of rank i.  21 lane-exchange steps, no LDS.
-__device__ __forceinline__ uint64_t wave_sort_desc(uint64_t x) {
-  const int lane = threadIdx.x & (kWave - 1);
-  auto stage = [&](auto jc, int k) {
-    constexpr int j = decltype(jc)::value;
-    const uint64_t y = xor_lane_u64<j>(x);
-    const bool keep_max = ((lane & j) == 0) == ((lane & k) == 0);
-    x = keep_max ? (x > y ? x : y) : (x < y ? x : y);
-  };
-  using I1 = std::integral_constant<int, 1>;
-  using I2 = std::integral_constant<int, 2>;
-  using I4 = std::integral_constant<int, 4>;
-  using I8 = std::integral_constant<int, 8>;
-  using I16 = std::integral_constant<int, 16>;
-  using I32 = std::integral_constant<int, 32>;
-  stage(I1{}, 2);
-  stage(I2{}, 4), stage(I1{}, 4);
-  stage(I4{}, 8), stage(I2{}, 8), stage(I1{}, 8);
-  stage(I8{}, 16), stage(I4{}, 16), stage(I2{}, 16), stage(I1{}, 16);
-  stage(I16{}, 32), stage(I8{}, 32), stage(I4{}, 32), stage(I2{}, 32), stage(I1{}, 32);
-  stage(I32{}, 64), stage(I16{}, 64), stage(I8{}, 64), stage(I4{}, 64), stage(I2{}, 64), stage(I1{}, 64);
-  return x;
-}
-
 __device__ __forceinline__ void cmpx_desc(uint64_t& a, uint64_t& b, bool desc) {
   const uint64_t hi = a > b ? a : b, lo = a > b ? b : a;
   a = desc ? hi : lo;

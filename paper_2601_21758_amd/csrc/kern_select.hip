@@ -8,7 +8,7 @@
 //    many workgroups.  Each lane holds 16 requests' 64-bit composite keys in
 //    registers.  Every wave takes the m-th largest lane maximum as its bar,
 //    the workgroup the largest bar t; every element with key >= t goes to an
-//    LDS list, which is sorted and cut to at most M entries.  The workgroup
+//    LDS list, which is ranked and cut to its M largest entries.  The workgroup
 //    writes the list and a completeness bound T: every element of its share
 //    whose composite is >= T is in the list.
 //
@@ -530,8 +530,39 @@ __device__ __forceinline__ void publish_list(ListShared& ls, int cnt, uint64_t l
     }
     if (rank == listed - 1) cb.bounds2[slot] = (cnt <= M + kOverCap || x < lowc) ? lowc : x;
   };
+  if (cnt <= 2 * kWave) {
+    // The usual length: every wave holds entries lane and 64 + lane and
+    // compares them with its own kSmallPer entries (read as broadcasts,
+    // entries past the list masked to 0, which is never larger); the counts
+    // add up in LDS, and after one barrier the first two waves place the
+    // entries.  Straight-line code: no loop and no per-entry branch.
+    constexpr int kSmallPer = 2 * kWave / kWavesPerBlock;
+    static_assert(kSmallPer * kWavesPerBlock == 2 * kWave && 2 * kWave <= kShortList, "one slice per wave");
+    const uint64_t x0 = lane < cnt ? ls.list2[lane] : 0ull;
+    const uint64_t x1 = kWave + lane < cnt ? ls.list2[kWave + lane] : 0ull;
+    const int j0 = kSmallPer * wv;
+    if (j0 < cnt) {  // uniform
+      int r0 = 0, r1 = 0;
+#pragma unroll
+      for (int u = 0; u < kSmallPer; ++u) {
+        const uint64_t y0 = ls.list2[j0 + u];  // in the array for every wave (j0 + u < 2 kWave)
+        const uint64_t y = j0 + u < cnt ? y0 : 0ull;
+        r0 += y > x0;
+        r1 += y > x1;
+      }
+      if (lane < cnt && r0 != 0) atomicAdd(&ls.rank[lane], r0);
+      if (kWave + lane < cnt && r1 != 0) atomicAdd(&ls.rank[kWave + lane], r1);
+    }
+    __syncthreads();
+    if ((int)threadIdx.x < cnt) {
+      place(ls.list2[threadIdx.x], ls.rank[threadIdx.x]);
+      if (kClearRank) ls.rank[threadIdx.x] = 0;  // ready for the next list
+    }
+    if (threadIdx.x == 0) cb.over_cnt[slot] = (uint32_t)(listed - M);
+    return;
+  }
   if (cnt <= kShortList) {
-    // The common case: every wave holds all entries (up to 4 per lane),
+    // Longer lists: every wave holds all entries (up to 8 per lane),
     // compares them with its own few (entries w, w + 16, ...) and adds its
     // counts into LDS, so no wave runs a long serial chain.
     constexpr int kG = kShortList / kWave;
@@ -588,28 +619,6 @@ __device__ __forceinline__ void publish_list(ListShared& ls, int cnt, uint64_t l
   for (int o = 1; o < tpe; o <<= 1) rank += (int)xor_lane_u32_dyn((uint32_t)rank, o);
   if (e < cnt && part == 0) place(x, rank);
   if (threadIdx.x == 0) cb.over_cnt[slot] = (uint32_t)(listed - M);
-}
-
-// publish_list for a list of M < cnt <= kWave entries, by one wave (the
-// caller's; every lane of it calls): the wave sorts the list, one entry per
-// lane, so lane i holds the entry of rank i and places it.  No barrier.
-constexpr int kShortWave = kWave;
-__device__ __forceinline__ void publish_list_wave(const ListShared& ls, int cnt, uint64_t lowc, int M, size_t slot,
-                                                  const CandBufs& cb) {
-  const int lane = threadIdx.x & (kWave - 1);
-  uint64_t* out_list = cb.lists + slot * (size_t)M;
-  uint64_t* over_list = cb.over + slot * (size_t)kOverCap;
-  const int listed = min(cnt, M + kOverCap);
-  const uint64_t x = wave_sort_desc(lane < cnt ? ls.list2[lane] : 0ull);  // rank = lane
-  EWSJF_STAMP_AFTER(kStampLocal, 7, (uint32_t)x);
-  if (lane < M) out_list[lane] = x;
-  else if (lane < listed) over_list[lane - M] = x;
-  if (lane == M - 1) {
-    cb.counts[slot] = (uint32_t)M;
-    cb.bounds[slot] = x > lowc ? x : lowc;
-  }
-  if (lane == listed - 1) cb.bounds2[slot] = (cnt <= M + kOverCap || x < lowc) ? lowc : x;
-  if (lane == 0) cb.over_cnt[slot] = (uint32_t)(listed - M);
 }
 
 // Chunks each wave has in flight when it starts scoring (2, 3 or 4).
@@ -895,11 +904,7 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
     const int total = nreg + (lower ? ls.nout : 0);
     EWSJF_STAMP(kStampLocal, 4);
     EWSJF_STAMP_VALUE(kStampLocal, 6, total);
-    if (total > M && total <= kShortWave) {  // uniform: one wave ranks and places
-      if (wv == 0) publish_list_wave(ls, total, lowc, M, slot, cb);
-    } else {
-      publish_list<false>(ls, total, lowc, M, slot, cb);
-    }
+    publish_list<false>(ls, total, lowc, M, slot, cb);
     EWSJF_STAMP(kStampLocal, 5);
     return;
   }

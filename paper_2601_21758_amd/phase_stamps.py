@@ -18,8 +18,7 @@ Points:
                     with the pool, 3 every wave done with the pool, 4 list
                     filtered, 5 list published; 6 is not a time but the
                     length of the filtered list (entries at or above the
-                    workgroup's bound), reported as "list_length"; 7 the
-                    list sorted by one wave (lists of 17 to 64 entries)
+                    workgroup's bound), reported as "list_length"
   merge_rank        0 start, 1 slots and bounds in (first barrier), 2 own
                     slots counted, 3 merge found safe, 4 outputs written, 7
                     took the exact merge
