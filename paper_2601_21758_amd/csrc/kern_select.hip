@@ -771,7 +771,7 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
       const int need = wcnt - kWaveCap;
       int base = 0;
       if (lane == 0) base = atomicAdd(&ls.nspill, need);
-      base = __shfl(base, 0);
+      base = __builtin_amdgcn_readfirstlane(base);  // lane 0 (the whole wave is active)
       if (base + need <= kListCap) {
         int c = wcnt0;
 #pragma unroll
@@ -835,7 +835,12 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
   // Publish into the workgroup's M fixed slots (unused slots hold 0).
   const size_t slot = (size_t)t * G + blockIdx.x;
   uint64_t* out_list = cb.lists + slot * (size_t)M;
-  if (ls.ovf != 0) {
+  // The overflow flag, the wave bars (lane i reads wave i's) and this wave's
+  // region entry are read together: one LDS round trip.
+  const int any_ovf = ls.ovf;
+  const uint32_t bar_l = ls.bar[lane & (kWavesPerBlock - 1)];
+  const uint64_t reg_l = region[lane];  // the wave's region entry (valid for lane < wcnt)
+  if (any_ovf != 0) {
     for (int i = threadIdx.x; i < M; i += kBlock) out_list[i] = 0ull;
     if (threadIdx.x == 0) {
       cb.counts[slot] = 0u;
@@ -854,14 +859,14 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
     // keys in [t2, t1), t2 the second largest bar, and the bound drops to t2.
     // Each wave keeps its entries at or above the bound; a scan of the kept
     // counts over the waves places them in list2.
-    const uint32_t b = lane < kWavesPerBlock ? ls.bar[lane] : 0u;
+    const uint32_t b = lane < kWavesPerBlock ? bar_l : 0u;
     const uint32_t t1 = wave_max_u32(b);
     const int v1 = (int)__builtin_ctzll(__ballot(lane < kWavesPerBlock && b == t1));
     const uint32_t t2 = wave_max_u32(lane != v1 ? b : 0u);
     const bool lower = passes == 1 && t2 != 0u && t2 < t1;  // uniform
     const uint32_t T_bar = lower ? t2 : t1;
     const uint64_t lowc = (uint64_t)T_bar << 32;
-    const uint64_t x = lane < ls.wcnt[wv] ? region[lane] : 0ull;
+    const uint64_t x = lane < wcnt ? reg_l : 0ull;
     const bool keep = x >= lowc && x != 0ull;
     const uint64_t km = __ballot(keep);
     if (lane == 0) ls.wkeep[wv] = __popcll(km);
@@ -891,7 +896,7 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
       if (sm != 0ull) {
         int base = 0;
         if (lane == 0) base = atomicAdd(&ls.nout, __popcll(sm));
-        base = __shfl(base, 0);
+        base = __builtin_amdgcn_readfirstlane(base);  // lane 0 (the whole wave is active)
         const int at = nreg + base + lanes_below(sm);
         // the chunk that element e = wv of wave v1 came from (single pass)
         const int64_t c = (int64_t)blockIdx.x + (int64_t)G * (v1 + kWavesPerBlock * (wv / 4));
@@ -935,7 +940,7 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
       for (int e = 0; e < kElemsPerLane; ++e) need += __popcll(__ballot(key[e] >= lo2 && key[e] < t1));
       int base = 0;
       if (lane == 0) base = atomicAdd(&ls.nspill, need);
-      base = __shfl(base, 0);
+      base = __builtin_amdgcn_readfirstlane(base);  // lane 0 (the whole wave is active)
       if (base + need <= kListCap) {
         int c = base;
 #pragma unroll
@@ -1425,7 +1430,7 @@ __device__ void merge_exact(const Src& src0, int t, int64_t n, int G, int M, int
             const uint64_t m0 = __ballot(p0), m1 = __ballot(p1);
             int base = 0;
             if (lane == 0) base = atomicAdd(&ms.cntS, (int)(__popcll(m0) + __popcll(m1)));
-            base = __shfl(base, 0);
+            base = __builtin_amdgcn_readfirstlane(base);  // lane 0 (the whole wave is active)
             if (p0) ms.S[base + lanes_below(m0)] = x0;
             if (p1) ms.S[base + __popcll(m0) + lanes_below(m1)] = x1;
           }
