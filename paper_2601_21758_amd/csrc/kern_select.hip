@@ -1525,12 +1525,12 @@ __global__ __launch_bounds__(kBlock) void merge_candidates(Src src0, int64_t n, 
 // largest listed composite tau, the top-B of the union is the exact top-B,
 // and an entry's output position is the number of larger entries.  That
 // holds when the largest bound T satisfies T <= 1 (every share listed all of
-// its elements) or at least B entries are >= T.  Workgroup w ranks the
-// kRankPer slots [w kRankPer, (w + 1) kRankPer) against all G x M slots,
-// counting with wave ballots, and writes the entries of rank < B to their
-// positions; no workgroup waits for another.  Only own slots at or above T
-// are ranked (below T an entry has at least B entries above it), all in one
-// pass; the lists need no order.  Otherwise (a share could be missing
+// its elements) or at least B entries are >= T.  Each workgroup ranks
+// kRankPer own slots against all G x M slots, counting with wave ballots,
+// and writes the entries of rank < B to their positions; no workgroup waits
+// for another.  Only own slots at or above T are ranked (below T an entry
+// has at least B entries above it), all in one pass; correctness needs no
+// order in the lists (the order only balances the work).  Otherwise (a share could be missing
 // members of the top-B) workgroup 0 runs the exact merge with its recovery
 // and the others leave.  Every workgroup reaches the same decision from the
 // same slots and bounds.
@@ -1566,7 +1566,17 @@ __global__ __launch_bounds__(kBlock) void merge_rank(Src src, int64_t n, int G, 
     v[r] = ((uint64_t)w[1] << 32) | w[0];
   }
   const uint64_t bnd = tid < G ? cb.bounds[tid] : 0ull;
-  const uint64_t own = tid < kRankPer && p0 + tid < GM ? cb.lists[p0 + tid] : 0ull;
+  // Own slots: with M = kRankPer and G a multiple of it, workgroup w takes
+  // entry k of list 16 (w / 16) + (w + k) % 16, one entry of each rank from
+  // 16 lists (a bijection on each group of 16 lists).  Lists hold their
+  // entries by rank, so every workgroup gets a similar number of slots at or
+  // above T to count, rather than all of one list's.
+  int os = p0 + tid;
+  if (M == kRankPer && (G & (kRankPer - 1)) == 0) {
+    const int w = (int)blockIdx.x;
+    os = ((w & ~(kRankPer - 1)) | ((w + tid) & (kRankPer - 1))) * M + tid;
+  }
+  const uint64_t own = tid < kRankPer && os < GM ? cb.lists[os] : 0ull;
   if (tid < kRankPer) {
     s_c[tid] = own;
     s_rank[tid] = 0;
