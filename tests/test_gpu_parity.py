@@ -315,6 +315,21 @@ def test_step_several_passes(E, kind):
     check_admission(host(ids)[0], host(top)[0], host(nsel)[0], rids[0], rtop[0], rnsel[0], rs[0])
 
 
+@pytest.mark.parametrize("B", [16, 64, 300, 2048, 4096])
+def test_step_b_sweep_full_grid(E, B):
+    # 1,048,579 requests on the full 256-workgroup grid: B sets the list
+    # length M (16 to 64), the bar width and so the filtered lists' lengths,
+    # which move between the published paths (copied, ranked by every wave
+    # up to 128 entries, ranked in slices above that)
+    n = (1 << 20) + 3
+    p = W.make_pool("two", n, 31, arrivals="poisson", rate=1e4, window=1 << 16, K=64, B=B)
+    t = oracle_table(p)
+    say(f"step B sweep n={n} B={B}")
+    ids, top, nsel = E.step(dev(p.length), dev(p.arrival), p.now, upload(E, t), dev(W.THETA_MID), B)
+    rids, rtop, rnsel, rs = oracle.step(p.length, p.arrival, p.now, t, W.THETA_MID, B)
+    check_admission(host(ids)[0], host(top)[0], host(nsel)[0], rids[0], rtop[0], rnsel[0], rs[0])
+
+
 def test_step_small_and_empty_pools(E):
     t = oracle.partition([5, 50, 500], init_queues=2, max_queues=2)
     for n in (0, 1, 3, 4, 5, 63, 255, 257):
