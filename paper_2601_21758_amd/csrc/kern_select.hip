@@ -737,12 +737,15 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
     const uint32_t bar = wave_group_bar(lmax, lg);
     src.keys4(raw[3], sh, km, key + 12);
     sched_fence();
-    // The next pass's first chunks (empty after the last pass): without a
-    // branch, so waits on the loads above keep their exact counts.
-    load_one(src, n, G, pass + 1, 0, raw[0]);
-    load_one(src, n, G, pass + 1, 1, raw[1]);
-    if constexpr (kAhead >= 3) load_one(src, n, G, pass + 1, 2, raw[2]);
-    if constexpr (kAhead >= 4) load_one(src, n, G, pass + 1, 3, raw[3]);
+    // The next pass's first chunks, if there is a next pass (uniform): after
+    // the last pass, loads of chunks past the pool would still queue behind
+    // the wave's real ones before the list work can wait them out.
+    if (pass + 1 < passes) {
+      load_one(src, n, G, pass + 1, 0, raw[0]);
+      load_one(src, n, G, pass + 1, 1, raw[1]);
+      if constexpr (kAhead >= 3) load_one(src, n, G, pass + 1, 2, raw[2]);
+      if constexpr (kAhead >= 4) load_one(src, n, G, pass + 1, 3, raw[3]);
+    }
     sched_fence();
     my_bar = bar > my_bar ? bar : my_bar;
     // Per element slot: one compare; the wave's mask of qualifying lanes
