@@ -25,27 +25,43 @@ namespace ewsjf {
 // One copy per translation unit that includes this header (no relocatable
 // device code): the select kernels' unit owns the one that is read.
 static __device__ uint64_t g_stamps[kStampSlots];
+// The workgroup's stamps are kept in LDS while the kernel runs and written
+// out at its exits (EWSJF_STAMP_FLUSH): a global store per stamp would be
+// waited for by the next barrier (its release), which would lengthen the
+// phase being timed.
+static __shared__ uint64_t s_stamps[kStampKernels][kStampPhases];
 }  // namespace ewsjf
-#define EWSJF_STAMP(kid, phase)                                                                            \
-  do {                                                                                                     \
-    if (threadIdx.x == 0 && blockIdx.y == 0 && blockIdx.x < (unsigned)::ewsjf::kStampBlocks)               \
-      ::ewsjf::g_stamps[((kid) * ::ewsjf::kStampBlocks + blockIdx.x) * ::ewsjf::kStampPhases + (phase)] =  \
-          __builtin_amdgcn_s_memrealtime();                                                                \
+#define EWSJF_STAMP_ON (threadIdx.x == 0 && blockIdx.y == 0 && blockIdx.x < (unsigned)::ewsjf::kStampBlocks)
+// Point 0 also clears the kernel's other points (a point not reached reads 0).
+#define EWSJF_STAMP(kid, phase)                                                                     \
+  do {                                                                                              \
+    if (EWSJF_STAMP_ON) {                                                                           \
+      if ((phase) == 0)                                                                             \
+        for (int ewsjf_i_ = 1; ewsjf_i_ < ::ewsjf::kStampPhases; ++ewsjf_i_)                        \
+          ::ewsjf::s_stamps[(kid)][ewsjf_i_] = 0ull;                                                \
+      ::ewsjf::s_stamps[(kid)][(phase)] = __builtin_amdgcn_s_memrealtime();                         \
+    }                                                                                               \
   } while (0)
 // A value in place of a time (read back as is).
-#define EWSJF_STAMP_VALUE(kid, phase, value)                                                               \
-  do {                                                                                                     \
-    if (threadIdx.x == 0 && blockIdx.y == 0 && blockIdx.x < (unsigned)::ewsjf::kStampBlocks)               \
-      ::ewsjf::g_stamps[((kid) * ::ewsjf::kStampBlocks + blockIdx.x) * ::ewsjf::kStampPhases + (phase)] =  \
-          (uint64_t)(value);                                                                               \
+#define EWSJF_STAMP_VALUE(kid, phase, value)                                                        \
+  do {                                                                                              \
+    if (EWSJF_STAMP_ON) ::ewsjf::s_stamps[(kid)][(phase)] = (uint64_t)(value);                      \
   } while (0)
 // The time once `dep` (a 32-bit value of the wave) has been computed: the
 // value is handed to an empty asm statement before the clock is read.
-#define EWSJF_STAMP_AFTER(kid, phase, dep)                                                                 \
-  do {                                                                                                     \
-    const int ewsjf_dep_ = __builtin_amdgcn_readfirstlane((int)(dep));                                     \
-    asm volatile("" ::"s"(ewsjf_dep_));                                                                    \
-    EWSJF_STAMP(kid, phase);                                                                               \
+#define EWSJF_STAMP_AFTER(kid, phase, dep)                                                          \
+  do {                                                                                              \
+    const int ewsjf_dep_ = __builtin_amdgcn_readfirstlane((int)(dep));                              \
+    asm volatile("" ::"s"(ewsjf_dep_));                                                             \
+    EWSJF_STAMP(kid, phase);                                                                        \
+  } while (0)
+// At every exit of a stamped kernel: the workgroup's points to the device array.
+#define EWSJF_STAMP_FLUSH(kid)                                                                      \
+  do {                                                                                              \
+    if (EWSJF_STAMP_ON)                                                                             \
+      for (int ewsjf_i_ = 0; ewsjf_i_ < ::ewsjf::kStampPhases; ++ewsjf_i_)                          \
+        ::ewsjf::g_stamps[((kid) * ::ewsjf::kStampBlocks + blockIdx.x) * ::ewsjf::kStampPhases +    \
+                          ewsjf_i_] = ::ewsjf::s_stamps[(kid)][ewsjf_i_];                           \
   } while (0)
 #else
 #define EWSJF_STAMP(kid, phase) \
@@ -56,5 +72,8 @@ static __device__ uint64_t g_stamps[kStampSlots];
   } while (0)
 #define EWSJF_STAMP_AFTER(kid, phase, dep) \
   do {                                     \
+  } while (0)
+#define EWSJF_STAMP_FLUSH(kid) \
+  do {                         \
   } while (0)
 #endif

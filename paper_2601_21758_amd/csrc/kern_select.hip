@@ -543,12 +543,20 @@ __device__ __forceinline__ void publish_list(ListShared& ls, int cnt, uint64_t l
     const int j0 = kSmallPer * wv;
     if (j0 < cnt) {  // uniform
       int r0 = 0, r1 = 0;
+      if (cnt > kWave) {  // uniform: entries 64.. exist
 #pragma unroll
-      for (int u = 0; u < kSmallPer; ++u) {
-        const uint64_t y0 = ls.list2[j0 + u];  // in the array for every wave (j0 + u < 2 kWave)
-        const uint64_t y = j0 + u < cnt ? y0 : 0ull;
-        r0 += y > x0;
-        r1 += y > x1;
+        for (int u = 0; u < kSmallPer; ++u) {
+          const uint64_t y0 = ls.list2[j0 + u];  // in the array for every wave (j0 + u < 2 kWave)
+          const uint64_t y = j0 + u < cnt ? y0 : 0ull;
+          r0 += y > x0;
+          r1 += y > x1;
+        }
+      } else {
+#pragma unroll
+        for (int u = 0; u < kSmallPer; ++u) {
+          const uint64_t y0 = ls.list2[j0 + u];
+          r0 += (j0 + u < cnt ? y0 : 0ull) > x0;
+        }
       }
       if (lane < cnt && r0 != 0) atomicAdd(&ls.rank[lane], r0);
       if (kWave + lane < cnt && r1 != 0) atomicAdd(&ls.rank[kWave + lane], r1);
@@ -851,6 +859,7 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
       cb.bounds2[slot] = ~0ull;
       cb.over_cnt[slot] = 0u;
     }
+    EWSJF_STAMP_FLUSH(kStampLocal);
     return;
   }
   if constexpr (!Src::kClustered) {
@@ -914,6 +923,7 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
     EWSJF_STAMP_VALUE(kStampLocal, 6, total);
     publish_list<false>(ls, total, lowc, M, slot, cb);
     EWSJF_STAMP(kStampLocal, 5);
+    EWSJF_STAMP_FLUSH(kStampLocal);
     return;
   }
   // The workgroup's bound: the largest wave bar t1.  When the wave holding
@@ -983,6 +993,7 @@ __global__ __launch_bounds__(kBlock) void local_candidates(Src src0, int64_t n, 
   EWSJF_STAMP_VALUE(kStampLocal, 6, ls.nout);
   publish_list<false>(ls, ls.nout, lowc, M, slot, cb);
   EWSJF_STAMP(kStampLocal, 5);
+  EWSJF_STAMP_FLUSH(kStampLocal);
 }
 
 
@@ -1260,6 +1271,7 @@ __device__ void merge_exact(const Src& src0, int t, int64_t n, int G, int M, int
       top[(size_t)t * B + r] = __builtin_nanf("");
     }
     if (tid == 0) n_sel[t] = 0;
+    EWSJF_STAMP_FLUSH(kStampMergeExact);
     return;
   }
 
@@ -1512,6 +1524,7 @@ __device__ void merge_exact(const Src& src0, int t, int64_t n, int G, int M, int
     for (int r = tid; r < sel; r += kBlock) tomb_len[comp_id(ms.X[r])] = 0;
   }
   EWSJF_STAMP(kStampMergeExact, 2);
+  EWSJF_STAMP_FLUSH(kStampMergeExact);
 }
 
 template <class Src>
@@ -1631,6 +1644,7 @@ __global__ __launch_bounds__(kBlock) void merge_rank(Src src, int64_t n, int G, 
   if (!safe) {
     EWSJF_STAMP(kStampMergeRank, 7);
     if (blockIdx.x == 0) merge_exact(src, 0, n, G, M, B, cb, ids, top, n_sel, tomb_len, lds);
+    EWSJF_STAMP_FLUSH(kStampMergeRank);
     return;
   }
   // own slots at or below T - 1 rank >= B
@@ -1657,6 +1671,7 @@ __global__ __launch_bounds__(kBlock) void merge_rank(Src src, int64_t n, int G, 
   }
   if (blockIdx.x == 0 && tid == 0) n_sel[0] = sel;
   EWSJF_STAMP(kStampMergeRank, 4);
+  EWSJF_STAMP_FLUSH(kStampMergeRank);
 }
 
 // Launches merge_rank with the smallest compiled slots-per-thread bound.
